@@ -1,0 +1,24 @@
+"""Plain fp64 CPU oracle of tree verification.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import, call or
+link this package: only the tests, the package smoke check and the CPU
+baseline leg of the benchmark use it.  It shares no code with the HIP path.
+
+Contents
+  tree_attention  -- tree-masked softmax attention with the full mask
+                     materialised (Sec. 2.2, tree-causal mask and masked
+                     attention equations).
+  tree_accept     -- per-node target argmax and greedy deepest-path
+                     acceptance (Sec. 2.4 greedy rule; App. E).
+  brute           -- pure-Python loop versions of both for tiny inputs, used
+                     only to pin the two functions above.
+
+Parity is pinned for both functions (brute force, closed forms, invariants
+and library special cases in the tests).
+"""
+from .tree_attention import (decode_bf16, tree_structure, full_mask,
+                             tree_attention)
+from .tree_accept import target_argmax, tree_accept
+
+__all__ = ["decode_bf16", "tree_structure", "full_mask", "tree_attention",
+           "target_argmax", "tree_accept"]

@@ -1,0 +1,102 @@
+"""Pure-Python brute force for tiny inputs (test infrastructure only).
+
+Independent constructions used to pin the oracle:
+  * attention: the visible key list of node i is built by walking parent
+    pointers from i to the root (not from the ancestor matrix), scores and
+    the softmax use Python floats and math.exp, no numpy;
+  * acceptance: every root-to-node path is enumerated explicitly and checked
+    token by token against a loop argmax; the best path is chosen by
+    (length, then lowest end node).
+"""
+from __future__ import annotations
+
+import math
+
+
+def _valid_tree(par):
+    if len(par) == 0 or par[0] != -1:
+        return False
+    return all(0 <= par[i] < i for i in range(1, len(par)))
+
+
+def _root_path(par, i):
+    """Nodes from the root to i (inclusive), by walking parents."""
+    out = [i]
+    while par[out[-1]] != -1:
+        out.append(par[out[-1]])
+    return out[::-1]
+
+
+def attention(q, k_cache, v_cache, k_tree, v_tree, parent, kv_len, scale=None):
+    """Nested-list (or array) inputs; returns nested lists [B][N][Hq][D]."""
+    B, N, Hq, D = len(q), len(q[0]), len(q[0][0]), len(q[0][0][0])
+    Hkv = len(k_cache[0][0])
+    G = Hq // Hkv
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    out = []
+    for b in range(B):
+        par = [int(x) for x in parent[b]]
+        ok = _valid_tree(par)
+        ob = []
+        for i in range(N):
+            oi = []
+            for h in range(Hq):
+                if not ok:
+                    oi.append([float("nan")] * D)
+                    continue
+                g = h // G
+                keys, vals = [], []
+                for j in range(int(kv_len[b])):
+                    keys.append([float(x) for x in k_cache[b][j][g]])
+                    vals.append([float(x) for x in v_cache[b][j][g]])
+                for u in _root_path(par, i):
+                    keys.append([float(x) for x in k_tree[b][u][g]])
+                    vals.append([float(x) for x in v_tree[b][u][g]])
+                qv = [float(x) for x in q[b][i][h]]
+                s = [scale * sum(qv[d] * kk[d] for d in range(D)) for kk in keys]
+                mx = max(s)
+                w = [math.exp(x - mx) for x in s]
+                tot = sum(w)
+                oi.append([sum(w[t] * vals[t][d] for t in range(len(w))) / tot
+                           for d in range(D)])
+            ob.append(oi)
+        out.append(ob)
+    return out
+
+
+def argmax_first(row):
+    best_i, best_v = 0, float(row[0])
+    for i in range(1, len(row)):
+        if float(row[i]) > best_v:
+            best_i, best_v = i, float(row[i])
+    return best_i
+
+
+def accept(logits, draft_tok, parent, Dmax):
+    """Returns (accept_len list, path lists, tgt lists)."""
+    B = len(parent)
+    lens, paths, tgts = [], [], []
+    for b in range(B):
+        par = [int(x) for x in parent[b]]
+        N = len(par)
+        tgt = [argmax_first(logits[b][i]) for i in range(N)]
+        tgts.append(tgt)
+        if not _valid_tree(par):
+            lens.append(-1)
+            paths.append([-1] * Dmax)
+            continue
+        best = None
+        for v in range(N):
+            pth = _root_path(par, v)
+            if all(int(draft_tok[b][pth[t]]) == tgt[pth[t - 1]]
+                   for t in range(1, len(pth))):
+                if best is None or len(pth) > len(best):
+                    best = pth
+        if len(best) > Dmax:
+            lens.append(-1)
+            paths.append([-1] * Dmax)
+        else:
+            lens.append(len(best))
+            paths.append(best + [-1] * (Dmax - len(best)))
+    return lens, paths, tgts

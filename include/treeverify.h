@@ -1,0 +1,144 @@
+/*
+ * treeverify.h -- C ABI of the tree-verification hot path on MI355X (gfx950).
+ *
+ * Two calls make up one verification step of parallel tree drafting
+ * speculative decoding:
+ *
+ *   tv_tree_verify_attention  every draft-tree node's query attends to its
+ *                             sequence's KV cache and to its own ancestors and
+ *                             itself in the tree (Sec. 2.2: the tree-causal mask
+ *                             M[v,u] = 0 iff u is an ancestor of v or v itself,
+ *                             the prefix being visible to all nodes, and the
+ *                             masked attention softmax(Q_v K^T / sqrt(d) + M_v) V;
+ *                             App. E: the ancestor relation is built inside the
+ *                             kernel, no dense per-request mask exists).
+ *   tv_tree_accept            the target's greedy prediction (argmax) at every
+ *                             node, then the deepest fully accepted root-to-node
+ *                             path: a node is accepted when its token equals the
+ *                             prediction at its parent and its parent is accepted
+ *                             (Sec. 2.4, greedy rule; App. E).
+ *
+ * Conventions shared by both calls
+ *   - Every tensor pointer is caller-owned DEVICE memory, row-major and
+ *     contiguous, 16-byte aligned.  The library never allocates or frees.
+ *   - Calls are asynchronous on `stream` (0 = the null stream) and never
+ *     synchronise the host.  They keep no global mutable state; concurrent
+ *     calls are safe when they use distinct workspaces.
+ *   - The workspace is caller-owned device memory of at least the size the
+ *     matching *_workspace() query returns.  It must be zero-filled once
+ *     before its first use; the kernels leave it ready for the next call.
+ *     Do not modify it between calls.
+ *   - Node 0 of every sequence is the root (the token already sampled by the
+ *     previous step, App. E); parent[b,0] = -1 and 0 <= parent[b,i] < i for
+ *     i >= 1 (children follow their parent, as in Alg. 1).
+ *   - Return value: TV_OK or a negative tv_status for errors the host can
+ *     detect (null pointers, bad sizes, unsupported shapes, misalignment,
+ *     a workspace that is too small, launch failures).  Nothing is launched
+ *     when an error is returned.
+ *   - Errors found on the device do not stop the host: a sequence whose
+ *     parent array breaks the rule above gets NaN in all its attention output
+ *     rows, and accept_len[b] = -1 with path[b,:] = -1 from tv_tree_accept
+ *     (also when its accepted path would need more than Dmax entries).
+ */
+#ifndef TREEVERIFY_H
+#define TREEVERIFY_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { TV_BF16 = 0, TV_F32 = 1 } tv_dtype;
+
+typedef enum {
+  TV_OK = 0,
+  TV_ERR_NULL = -1,         /* a required pointer is NULL */
+  TV_ERR_SHAPE = -2,        /* a size is < 1 (or < 0 where 0 is allowed) or inconsistent */
+  TV_ERR_DTYPE = -3,        /* unknown logits dtype */
+  TV_ERR_UNSUPPORTED = -4,  /* D not in {64,128}, N above TV_MAX_NODES, ... */
+  TV_ERR_WORKSPACE = -5,    /* workspace NULL or smaller than required */
+  TV_ERR_LAUNCH = -6,       /* the HIP runtime rejected a launch */
+  TV_ERR_ALIGN = -7         /* a tensor pointer is not 16-byte aligned */
+} tv_status;
+
+/* Largest tree (nodes per sequence, root included) either call accepts. */
+#define TV_MAX_NODES 2048
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char* tv_status_string(int status);
+
+/* ABI version, bumped on any incompatible change. */
+int tv_version(void);
+
+/*
+ * Workspace bytes tv_tree_verify_attention needs for these sizes (0 when the
+ * sizes are invalid).  Depends only on the arguments, never on kv_len.
+ */
+size_t tv_tree_verify_attention_workspace(int B, int N, int Hq, int Hkv, int D,
+                                          int Lmax);
+
+/*
+ * Tree-masked grouped-query attention of all draft-tree nodes (Sec. 2.2).
+ *
+ *   q       [B, N, Hq, D]     bf16  queries of the tree nodes (post-RoPE)
+ *   k_cache [B, Lmax, Hkv, D] bf16  cached prefix keys (post-RoPE)
+ *   v_cache [B, Lmax, Hkv, D] bf16  cached prefix values
+ *   k_tree  [B, N, Hkv, D]    bf16  keys of the tree nodes
+ *   v_tree  [B, N, Hkv, D]    bf16  values of the tree nodes
+ *   parent  [B, N]            int32 parent node index, -1 for the root
+ *   kv_len  [B]               int32 valid cache length per sequence, in
+ *                                   [0, Lmax]; NULL means Lmax for all.
+ *                                   Cache rows >= kv_len[b] are never read.
+ *   out     [B, N, Hq, D]     bf16  result, round-to-nearest-even
+ *
+ * Query head h uses KV head h / (Hq / Hkv).  Node i of sequence b sees cache
+ * rows [0, kv_len[b]) and tree nodes on its root path, itself included.
+ * Scores are scaled by `scale` (<= 0 selects 1/sqrt(D)); the softmax and all
+ * accumulation run in fp32, products of bf16 operands on the matrix cores.
+ * Requirements: Hq % Hkv == 0, D in {64, 128}, 1 <= N <= TV_MAX_NODES,
+ * B >= 1, Lmax >= 0; visible keys and values must be finite.
+ */
+int tv_tree_verify_attention(const void* q, const void* k_cache,
+                             const void* v_cache, const void* k_tree,
+                             const void* v_tree, const int32_t* parent,
+                             const int32_t* kv_len, void* out, int B, int N,
+                             int Hq, int Hkv, int D, int Lmax, float scale,
+                             void* workspace, size_t workspace_bytes,
+                             hipStream_t stream);
+
+/* Workspace bytes tv_tree_accept needs for these sizes (0 when invalid). */
+size_t tv_tree_accept_workspace(int B, int N, int V);
+
+/*
+ * Greedy tree acceptance (Sec. 2.4; App. E).
+ *
+ *   logits     [B, N, V] bf16 or fp32  target logits at every tree node
+ *   draft_tok  [B, N]    int32  drafted token of every node (node 0 ignored)
+ *   parent     [B, N]    int32  as above
+ *   accept_len [B]       int32  out: entries of the accepted path, root
+ *                               included (>= 1), or -1 on a device error
+ *   path       [B, Dmax] int32  out: node indices root first, -1 padded
+ *   tgt_argmax [B, N]    int32  out (optional, may be NULL): first index of
+ *                               the maximum logit of every node; the
+ *                               correction token of sequence b is
+ *                               tgt_argmax[b, path[b, accept_len[b]-1]]
+ *
+ * Ties in the argmax go to the lowest vocabulary index, values compared as
+ * numbers (-0.0 == +0.0); logits must not be NaN.  Among equally deep
+ * accepted nodes the lowest node index ends the path.
+ * Requirements: 1 <= N <= TV_MAX_NODES, V >= 1, B >= 1, Dmax >= 1.
+ */
+int tv_tree_accept(const void* logits, int logits_dtype,
+                   const int32_t* draft_tok, const int32_t* parent, int B,
+                   int N, int V, int Dmax, int32_t* accept_len, int32_t* path,
+                   int32_t* tgt_argmax, void* workspace,
+                   size_t workspace_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TREEVERIFY_H */

@@ -1,0 +1,24 @@
+"""MI355X-native tree verification for parallel tree drafting speculative
+decoding: tree-masked GQA attention and greedy tree acceptance as HIP kernels
+for gfx950 behind a C ABI (include/treeverify.h).
+
+Importing the package loads nothing; the first call loads libtreeverify.so
+and raises if it is missing.
+"""
+
+__all__ = ["tree_verify_attention", "tree_accept", "load_library"]
+
+
+def tree_verify_attention(*args, **kwargs):
+    from .binding import tree_verify_attention as f
+    return f(*args, **kwargs)
+
+
+def tree_accept(*args, **kwargs):
+    from .binding import tree_accept as f
+    return f(*args, **kwargs)
+
+
+def load_library():
+    from .binding import load_library as f
+    return f()

@@ -1,0 +1,164 @@
+"""Thin ctypes binding of libtreeverify.so.
+
+Argument marshalling only: torch tensors serve as device buffers and the
+current torch stream as the HIP stream; every step of the computation runs in
+the library's HIP kernels.  There is no fallback: if the library is missing
+or the tensors are not on a GPU, the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtreeverify.so")
+
+TV_BF16, TV_F32 = 0, 1
+MAX_NODES = 2048
+
+_lib = None
+_lock = threading.Lock()
+_workspaces = {}
+
+
+def load_library() -> ctypes.CDLL:
+    """Load the built library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                "libtreeverify.so is not built (run __graft_entry__.build() or "
+                "python paper_2606_18394_amd/build.py)")
+        lib = ctypes.CDLL(LIB_PATH)
+        vp, i32p, ci, sz = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+        lib.tv_status_string.restype = ctypes.c_char_p
+        lib.tv_status_string.argtypes = [ci]
+        lib.tv_version.restype = ci
+        lib.tv_version.argtypes = []
+        lib.tv_tree_verify_attention_workspace.restype = sz
+        lib.tv_tree_verify_attention_workspace.argtypes = [ci] * 6
+        lib.tv_tree_verify_attention.restype = ci
+        lib.tv_tree_verify_attention.argtypes = (
+            [vp] * 5 + [i32p, i32p, vp] + [ci] * 6 + [ctypes.c_float, vp, sz, vp])
+        lib.tv_tree_accept_workspace.restype = sz
+        lib.tv_tree_accept_workspace.argtypes = [ci] * 3
+        lib.tv_tree_accept.restype = ci
+        lib.tv_tree_accept.argtypes = (
+            [vp, ci, i32p, i32p] + [ci] * 4 + [i32p, i32p, i32p, vp, sz, vp])
+        _lib = lib
+        return lib
+
+
+def status_string(rc: int) -> str:
+    return load_library().tv_status_string(rc).decode()
+
+
+def _check(rc: int) -> None:
+    if rc != 0:
+        raise RuntimeError(status_string(rc))
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _need(t, name, dtype, shape=None, device=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+
+
+def workspace(kind: str, nbytes: int, device, stream_ptr: int) -> torch.Tensor:
+    """Zero-filled workspace cached per (kind, device, stream); grows as needed."""
+    key = (kind, str(device), stream_ptr)
+    ws = _workspaces.get(key)
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=device)
+        _workspaces[key] = ws
+    return ws
+
+
+def tree_verify_attention(q, k_cache, v_cache, k_tree, v_tree, parent, out,
+                          kv_len=None, scale=None, workspace_tensor=None):
+    """out[b,i,h] = tree-masked attention of node i (bf16 in, bf16 out).
+
+    q [B,N,Hq,D], k_cache/v_cache [B,Lmax,Hkv,D], k_tree/v_tree [B,N,Hkv,D]
+    (bf16); parent [B,N] int32; kv_len [B] int32 or None; out [B,N,Hq,D].
+    """
+    lib = load_library()
+    B, N, Hq, D = q.shape
+    Lmax, Hkv = k_cache.shape[1], k_cache.shape[2]
+    dev = q.device
+    _need(q, "q", torch.bfloat16, device=dev)
+    _need(k_cache, "k_cache", torch.bfloat16, (B, Lmax, Hkv, D), dev)
+    _need(v_cache, "v_cache", torch.bfloat16, (B, Lmax, Hkv, D), dev)
+    _need(k_tree, "k_tree", torch.bfloat16, (B, N, Hkv, D), dev)
+    _need(v_tree, "v_tree", torch.bfloat16, (B, N, Hkv, D), dev)
+    _need(parent, "parent", torch.int32, (B, N), dev)
+    _need(out, "out", torch.bfloat16, (B, N, Hq, D), dev)
+    if kv_len is not None:
+        _need(kv_len, "kv_len", torch.int32, (B,), dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    need = lib.tv_tree_verify_attention_workspace(B, N, Hq, Hkv, D, Lmax)
+    if need == 0:
+        _check(-2)
+    ws = workspace_tensor if workspace_tensor is not None else workspace("attn", need, dev, stream)
+    _check(lib.tv_tree_verify_attention(
+        _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(k_tree), _ptr(v_tree), _ptr(parent),
+        _ptr(kv_len), _ptr(out), B, N, Hq, Hkv, D, Lmax,
+        0.0 if scale is None else float(scale), _ptr(ws), ws.numel(), ctypes.c_void_p(stream)))
+    return out
+
+
+def tree_accept(logits, draft_tok, parent, Dmax, accept_len=None, path=None,
+                tgt_argmax=None, with_argmax=True, workspace_tensor=None):
+    """Greedy tree acceptance.  Returns (accept_len [B], path [B,Dmax],
+    tgt_argmax [B,N] or None), all int32 on the logits' device."""
+    lib = load_library()
+    B, N, V = logits.shape
+    dev = logits.device
+    if logits.dtype == torch.bfloat16:
+        dt = TV_BF16
+    elif logits.dtype == torch.float32:
+        dt = TV_F32
+    else:
+        raise TypeError("logits must be bfloat16 or float32")
+    _need(logits, "logits", logits.dtype, device=dev)
+    _need(draft_tok, "draft_tok", torch.int32, (B, N), dev)
+    _need(parent, "parent", torch.int32, (B, N), dev)
+    if accept_len is None:
+        accept_len = torch.empty(B, dtype=torch.int32, device=dev)
+    if path is None:
+        path = torch.empty(B, Dmax, dtype=torch.int32, device=dev)
+    if tgt_argmax is None and with_argmax:
+        tgt_argmax = torch.empty(B, N, dtype=torch.int32, device=dev)
+    _need(accept_len, "accept_len", torch.int32, (B,), dev)
+    _need(path, "path", torch.int32, (B, Dmax), dev)
+    if tgt_argmax is not None:
+        _need(tgt_argmax, "tgt_argmax", torch.int32, (B, N), dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    need = lib.tv_tree_accept_workspace(B, N, V)
+    if need == 0:
+        _check(-2)
+    ws = workspace_tensor if workspace_tensor is not None else workspace("accept", need, dev, stream)
+    _check(lib.tv_tree_accept(
+        _ptr(logits), dt, _ptr(draft_tok), _ptr(parent), B, N, V, int(Dmax),
+        _ptr(accept_len), _ptr(path), _ptr(tgt_argmax), _ptr(ws), ws.numel(),
+        ctypes.c_void_p(stream)))
+    return accept_len, path, tgt_argmax

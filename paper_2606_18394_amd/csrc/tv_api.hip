@@ -1,0 +1,105 @@
+// C entry points: argument checks, workspace sizing and launches.  No
+// allocation, no host synchronisation, no global mutable state.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/treeverify.h"
+#include "tv_plan.h"
+
+static_assert(TV_MAX_NODES == tv::kMaxNodes, "node limit mismatch");
+
+namespace tv {
+hipError_t launch_attention(const void* q, const void* kc, const void* vc, const void* kt,
+                            const void* vt, const int32_t* parent, const int32_t* kv_len,
+                            void* out, int B, int N, int Hq, int Hkv, int D, int Lmax,
+                            float scale, void* ws, const AttnPlan& p, hipStream_t st);
+hipError_t launch_accept(const void* logits, int f32, const int32_t* draft, const int32_t* parent,
+                         int B, int N, int V, int Dmax, int32_t* accept_len, int32_t* path,
+                         int32_t* tgt_out, void* ws, hipStream_t st);
+}  // namespace tv
+
+static bool misaligned(const void* p) { return ((uintptr_t)p & 15u) != 0; }
+
+static int check_attention_sizes(int B, int N, int Hq, int Hkv, int D, int Lmax) {
+  if (B < 1 || N < 1 || Hq < 1 || Hkv < 1 || Lmax < 0) return TV_ERR_SHAPE;
+  if (Hq % Hkv != 0) return TV_ERR_SHAPE;
+  if (D != 64 && D != 128) return TV_ERR_UNSUPPORTED;
+  if (N > TV_MAX_NODES) return TV_ERR_UNSUPPORTED;
+  // element offsets are formed in 64-bit, but row indices stay in int32
+  if ((long long)B * N * Hq > (1ll << 31) || (long long)B * Lmax > (1ll << 31)) return TV_ERR_UNSUPPORTED;
+  return TV_OK;
+}
+
+static int check_accept_sizes(int B, int N, int V, int Dmax) {
+  if (B < 1 || N < 1 || V < 1 || Dmax < 1) return TV_ERR_SHAPE;
+  if (N > TV_MAX_NODES) return TV_ERR_UNSUPPORTED;
+  if ((long long)B * N > (1ll << 24)) return TV_ERR_UNSUPPORTED;
+  return TV_OK;
+}
+
+extern "C" {
+
+const char* tv_status_string(int status) {
+  switch (status) {
+    case TV_OK: return "TV_OK";
+    case TV_ERR_NULL: return "TV_ERR_NULL: a required pointer is NULL";
+    case TV_ERR_SHAPE: return "TV_ERR_SHAPE: invalid or inconsistent sizes";
+    case TV_ERR_DTYPE: return "TV_ERR_DTYPE: unknown logits dtype";
+    case TV_ERR_UNSUPPORTED: return "TV_ERR_UNSUPPORTED: shape outside the supported range";
+    case TV_ERR_WORKSPACE: return "TV_ERR_WORKSPACE: workspace missing or too small";
+    case TV_ERR_LAUNCH: return "TV_ERR_LAUNCH: the HIP runtime rejected a launch";
+    case TV_ERR_ALIGN: return "TV_ERR_ALIGN: tensor pointer not 16-byte aligned";
+    default: return "unknown treeverify status";
+  }
+}
+
+int tv_version(void) { return 1; }
+
+size_t tv_tree_verify_attention_workspace(int B, int N, int Hq, int Hkv, int D, int Lmax) {
+  if (check_attention_sizes(B, N, Hq, Hkv, D, Lmax) != TV_OK) return 0;
+  const tv::AttnPlan p = tv::attn_plan(B, N, Hq, Hkv, D, Lmax);
+  return p.ws_bytes > 0 ? p.ws_bytes : 256;
+}
+
+int tv_tree_verify_attention(const void* q, const void* k_cache, const void* v_cache,
+                             const void* k_tree, const void* v_tree, const int32_t* parent,
+                             const int32_t* kv_len, void* out, int B, int N, int Hq, int Hkv,
+                             int D, int Lmax, float scale, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream) {
+  int rc = check_attention_sizes(B, N, Hq, Hkv, D, Lmax);
+  if (rc != TV_OK) return rc;
+  if (!q || !k_tree || !v_tree || !parent || !out) return TV_ERR_NULL;
+  if (Lmax > 0 && (!k_cache || !v_cache)) return TV_ERR_NULL;
+  if (misaligned(q) || misaligned(k_tree) || misaligned(v_tree) || misaligned(out) ||
+      (Lmax > 0 && (misaligned(k_cache) || misaligned(v_cache))))
+    return TV_ERR_ALIGN;
+  const tv::AttnPlan p = tv::attn_plan(B, N, Hq, Hkv, D, Lmax);
+  if (p.ws_bytes > 0 && (!workspace || workspace_bytes < p.ws_bytes)) return TV_ERR_WORKSPACE;
+  if (misaligned(workspace)) return TV_ERR_ALIGN;
+  if (!(scale > 0.f)) scale = 1.0f / sqrtf((float)D);
+  hipError_t e = tv::launch_attention(q, k_cache, v_cache, k_tree, v_tree, parent, kv_len, out,
+                                      B, N, Hq, Hkv, D, Lmax, scale, workspace, p, stream);
+  return e == hipSuccess ? TV_OK : TV_ERR_LAUNCH;
+}
+
+size_t tv_tree_accept_workspace(int B, int N, int V) {
+  if (check_accept_sizes(B, N, V, 1) != TV_OK) return 0;
+  return tv::accept_ws_bytes(B, N);
+}
+
+int tv_tree_accept(const void* logits, int logits_dtype, const int32_t* draft_tok,
+                   const int32_t* parent, int B, int N, int V, int Dmax, int32_t* accept_len,
+                   int32_t* path, int32_t* tgt_argmax, void* workspace, size_t workspace_bytes,
+                   hipStream_t stream) {
+  int rc = check_accept_sizes(B, N, V, Dmax);
+  if (rc != TV_OK) return rc;
+  if (logits_dtype != TV_BF16 && logits_dtype != TV_F32) return TV_ERR_DTYPE;
+  if (!logits || !draft_tok || !parent || !accept_len || !path) return TV_ERR_NULL;
+  if (!workspace || workspace_bytes < tv::accept_ws_bytes(B, N)) return TV_ERR_WORKSPACE;
+  if (misaligned(workspace)) return TV_ERR_ALIGN;
+  hipError_t e = tv::launch_accept(logits, logits_dtype == TV_F32, draft_tok, parent, B, N, V,
+                                   Dmax, accept_len, path, tgt_argmax, workspace, stream);
+  return e == hipSuccess ? TV_OK : TV_ERR_LAUNCH;
+}
+
+}  // extern "C"

@@ -1,0 +1,122 @@
+"""The C-ABI library loads, exports every symbol the header declares, and
+rejects bad arguments on the host (no GPU needed: nothing is launched)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "treeverify.h")
+
+
+def _lib():
+    from paper_2606_18394_amd import binding
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2606_18394_amd import build
+        build.build()
+    return binding.load_library()
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(tv_\w+)\s*\(", src)))
+
+
+def test_header_declares_the_api():
+    names = _declared()
+    for n in ["tv_tree_verify_attention", "tv_tree_accept", "tv_tree_verify_attention_workspace",
+              "tv_tree_accept_workspace", "tv_status_string", "tv_version"]:
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported():
+    lib = _lib()
+    for n in _declared():
+        assert hasattr(lib, n), n
+
+
+def test_status_strings_and_version():
+    lib = _lib()
+    assert lib.tv_version() == 1
+    for code in [0, -1, -2, -3, -4, -5, -6, -7]:
+        assert lib.tv_status_string(code)
+    assert b"unknown" in lib.tv_status_string(123)
+
+
+def test_workspace_queries():
+    lib = _lib()
+    assert lib.tv_tree_verify_attention_workspace(1, 64, 32, 8, 128, 4096) > 0
+    assert lib.tv_tree_verify_attention_workspace(1, 64, 30, 8, 128, 4096) == 0   # Hq % Hkv
+    assert lib.tv_tree_verify_attention_workspace(1, 64, 32, 8, 96, 4096) == 0    # D
+    assert lib.tv_tree_verify_attention_workspace(1, 4096, 32, 8, 128, 16) == 0   # N too big
+    assert lib.tv_tree_verify_attention_workspace(0, 64, 32, 8, 128, 16) == 0
+    assert lib.tv_tree_verify_attention_workspace(1, 16, 4, 2, 64, 0) > 0        # empty cache ok
+    assert lib.tv_tree_accept_workspace(1, 64, 151936) > 0
+    assert lib.tv_tree_accept_workspace(1, 0, 10) == 0
+    assert lib.tv_tree_accept_workspace(1, 4096, 10) == 0
+
+
+FAKE = 0x100000  # 16-byte aligned non-null address; never dereferenced
+
+
+def _attn(lib, **kw):
+    a = dict(q=FAKE, kc=FAKE, vc=FAKE, kt=FAKE, vt=FAKE, parent=FAKE, kv_len=None, out=FAKE,
+             B=1, N=64, Hq=32, Hkv=8, D=128, Lmax=4096, scale=0.0, ws=FAKE, wsb=1 << 40)
+    a.update(kw)
+    return lib.tv_tree_verify_attention(
+        a["q"], a["kc"], a["vc"], a["kt"], a["vt"], a["parent"], a["kv_len"], a["out"],
+        a["B"], a["N"], a["Hq"], a["Hkv"], a["D"], a["Lmax"], ctypes.c_float(a["scale"]),
+        a["ws"], a["wsb"], None)
+
+
+def _acc(lib, **kw):
+    a = dict(logits=FAKE, dt=0, draft=FAKE, parent=FAKE, B=1, N=64, V=151936, Dmax=9,
+             ln=FAKE, path=FAKE, tgt=None, ws=FAKE, wsb=1 << 40)
+    a.update(kw)
+    return lib.tv_tree_accept(a["logits"], a["dt"], a["draft"], a["parent"], a["B"], a["N"],
+                              a["V"], a["Dmax"], a["ln"], a["path"], a["tgt"], a["ws"],
+                              a["wsb"], None)
+
+
+def test_attention_host_errors():
+    lib = _lib()
+    assert _attn(lib, q=None) == -1
+    assert _attn(lib, out=None) == -1
+    assert _attn(lib, parent=None) == -1
+    assert _attn(lib, kc=None) == -1
+    assert _attn(lib, B=0) == -2
+    assert _attn(lib, N=0) == -2
+    assert _attn(lib, Hq=30) == -2
+    assert _attn(lib, Lmax=-1) == -2
+    assert _attn(lib, D=96) == -4
+    assert _attn(lib, N=2049) == -4
+    assert _attn(lib, q=FAKE + 8) == -7
+    assert _attn(lib, out=FAKE + 2) == -7
+    assert _attn(lib, ws=None) == -5
+    assert _attn(lib, wsb=16) == -5
+
+
+def test_accept_host_errors():
+    lib = _lib()
+    assert _acc(lib, logits=None) == -1
+    assert _acc(lib, path=None) == -1
+    assert _acc(lib, ln=None) == -1
+    assert _acc(lib, dt=7) == -3
+    assert _acc(lib, B=0) == -2
+    assert _acc(lib, V=0) == -2
+    assert _acc(lib, Dmax=0) == -2
+    assert _acc(lib, N=2049) == -4
+    assert _acc(lib, ws=None) == -5
+    assert _acc(lib, wsb=8) == -5
+    assert _acc(lib, ws=FAKE + 4) == -7
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    from paper_2606_18394_amd import tree_accept
+    _lib()
+    with pytest.raises(ValueError):
+        tree_accept(torch.zeros(1, 2, 8), torch.zeros(1, 2, dtype=torch.int32),
+                    torch.tensor([[-1, 0]], dtype=torch.int32), 2)

@@ -1,0 +1,173 @@
+"""GPU parity of tree_verify_attention against the fp64 oracle (through the
+C ABI).  Bar: max-abs error <= 1e-2 on bf16 N(0,1) inputs; invariances are
+checked bit for bit."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_18394_amd import synth
+from helpers import gpu_attention, oracle_attention
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-2
+
+
+def _sample_nodes(parent_row, k, rng):
+    N = len(parent_row)
+    d = np.zeros(N, dtype=int)
+    for i in range(1, N):
+        d[i] = d[parent_row[i]] + 1
+    pick = {0, N - 1, int(np.argmax(d))}
+    pick |= set(rng.choice(N, size=min(k, N), replace=False).tolist())
+    return sorted(pick)
+
+
+@pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
+def test_workload_parity(name):
+    w = synth.WORKLOADS[name]
+    inp = synth.draw(w, with_logits=False)
+    got, ok = gpu_attention(inp, canary=4096)
+    assert ok, "write outside out"
+    assert np.isfinite(got).all()
+    rng = np.random.default_rng(7)
+    if name in ("tiny", "qwen3_8b"):
+        ref = oracle_attention(inp)
+        err = np.abs(got - ref).max()
+    else:
+        heads = sorted(rng.choice(w.Hq, size=min(8, w.Hq), replace=False).tolist())
+        err = 0.0
+        for b in range(w.B):
+            nodes = _sample_nodes(inp["parent"][b], 16 if w.B == 1 else 4, rng)
+            sub = {k: (v[b:b + 1] if isinstance(v, np.ndarray) and v.ndim >= 1 and
+                       v.shape[0] == w.B else v) for k, v in inp.items()}
+            ref = oracle_attention(sub, nodes=nodes, heads=heads)[0]
+            err = max(err, np.abs(got[b][nodes][:, heads] - ref).max())
+    print(f"{name}: max abs err {err:.3e}")
+    assert err <= TOL
+
+
+FUZZ = [
+    # (B, N, Hq, Hkv, D, Lmax, kv_lens, tree)
+    (1, 1, 4, 4, 64, 0, [0], "random"),
+    (1, 1, 8, 2, 128, 1, [1], "random"),
+    (1, 2, 4, 1, 64, 63, [63], "chain"),
+    (2, 3, 8, 8, 128, 64, [64, 0], "star"),
+    (1, 17, 16, 2, 128, 65, [65], "random"),
+    (3, 63, 8, 1, 64, 1000, [1000, 1, 517], "random"),
+    (1, 64, 32, 8, 128, 64, [33], "chain"),
+    (2, 65, 32, 4, 128, 1000, [999, 64], "random"),
+    (1, 129, 8, 2, 64, 100, [100], "star"),
+    (1, 129, 32, 8, 128, 0, [0], "random"),
+    (1, 512, 16, 2, 128, 65, [65], "random"),
+    (1, 512, 8, 8, 64, 16, [16], "chain"),
+    (4, 40, 24, 8, 128, 300, [0, 300, 17, 255], "random"),
+    (1, 2048, 2, 1, 128, 40, [40], "random"),
+    (1, 300, 64, 8, 128, 2000, [1999], "random"),
+]
+
+
+@pytest.mark.parametrize("case", range(len(FUZZ)))
+def test_fuzz_parity(case):
+    B, N, Hq, Hkv, D, Lmax, kvl, kind = FUZZ[case]
+    rng = np.random.default_rng(1000 + case)
+    if kind == "chain":
+        trees = np.stack([synth.chain_tree(N)] * B)
+    elif kind == "star":
+        trees = np.stack([synth.star_tree(N)] * B)
+    else:
+        trees = np.stack([synth.random_tree(rng, N, depth=max(1, min(N - 1, 12)), branching=4)
+                          for _ in range(B)]) if N > 1 else np.full((B, 1), -1, np.int32)
+    inp = synth.make_inputs(rng, B=B, N=N, Hq=Hq, Hkv=Hkv, D=D, Lmax=Lmax, V=8,
+                            trees=trees, kv_len=np.array(kvl), with_logits=False)
+    print(f"fuzz case {FUZZ[case]}", flush=True)
+    got, ok = gpu_attention(inp, canary=1024)
+    assert ok
+    if N * Hq <= 4096:
+        ref = oracle_attention(inp)
+        err = np.abs(got - ref).max()
+    else:
+        nodes = _sample_nodes(trees[0], 64, rng)
+        ref = oracle_attention(inp, nodes=nodes)
+        err = np.abs(got[:, nodes] - ref).max()
+    assert err <= TOL, err
+
+
+@pytest.mark.parametrize("kvl", [0, 5, 40])
+def test_zero_keys_closed_form(kvl):
+    """K = 0: every visible key has the same score, so a wrong mask moves the
+    output by O(1 / #visible) -- far above the tolerance at small kv_len."""
+    rng = np.random.default_rng(kvl)
+    B, N, Hq, Hkv, D, Lmax = 2, 200, 16, 4, 128, 64
+    trees = np.stack([synth.random_tree(rng, N, depth=10, branching=3) for _ in range(B)])
+    inp = synth.make_inputs(rng, B=B, N=N, Hq=Hq, Hkv=Hkv, D=D, Lmax=Lmax, V=8, trees=trees,
+                            kv_len=np.array([kvl, Lmax]), with_logits=False)
+    inp["k_cache"][:] = 0
+    inp["k_tree"][:] = 0
+    got, _ = gpu_attention(inp)
+    ref = oracle_attention(inp)
+    assert np.abs(got - ref).max() <= TOL
+
+
+def test_masked_keys_have_no_influence():
+    rng = np.random.default_rng(5)
+    B, N, Hq, Hkv, D, Lmax = 1, 96, 8, 2, 128, 200
+    trees = synth.random_tree(rng, N, depth=8, branching=3)[None]
+    inp = synth.make_inputs(rng, B=B, N=N, Hq=Hq, Hkv=Hkv, D=D, Lmax=Lmax, V=8, trees=trees,
+                            kv_len=np.array([150]), with_logits=False)
+    base, _ = gpu_attention(inp)
+    anc_of = []
+    for i in [0, 37, N - 1]:
+        anc, u = set(), i
+        while u != -1:
+            anc.add(u)
+            u = trees[0, u]
+        hidden = [u for u in range(N) if u not in anc]
+        pert = dict(inp)
+        for name in ["k_tree", "v_tree"]:
+            arr = inp[name].copy()
+            big = synth.bf16_bits(
+                (np.frombuffer((arr[0, hidden].astype(np.uint32) << 16).tobytes(),
+                               dtype=np.float32) * 1000).reshape(arr[0, hidden].shape))
+            arr[0, hidden] = big
+            pert[name] = arr
+        for name in ["k_cache", "v_cache"]:
+            arr = inp[name].copy()
+            arr[0, 150:] = np.uint16(0x7F7F)      # huge finite values beyond kv_len
+            pert[name] = arr
+        got, _ = gpu_attention(pert)
+        assert np.array_equal(got[0, i], base[0, i]), i
+
+
+def test_deterministic_and_kvlen_default():
+    w = synth.with_shape(synth.WORKLOADS["qwen3_8b"], L=1000)
+    inp = synth.draw(w, with_logits=False)
+    a, _ = gpu_attention(inp)
+    b, _ = gpu_attention(inp)
+    c, _ = gpu_attention(inp, kv_len=False)   # NULL kv_len means Lmax
+    assert np.array_equal(a, b) and np.array_equal(a, c)
+
+
+def test_scale_override():
+    rng = np.random.default_rng(3)
+    trees = synth.random_tree(rng, 20, depth=5)[None]
+    inp = synth.make_inputs(rng, B=1, N=20, Hq=4, Hkv=2, D=64, Lmax=50, V=8, trees=trees,
+                            kv_len=np.array([50]), with_logits=False)
+    got, _ = gpu_attention(inp, scale=0.3)
+    ref = oracle_attention(inp, scale=0.3)
+    assert np.abs(got - ref).max() <= TOL
+
+
+def test_invalid_tree_rows_are_nan():
+    rng = np.random.default_rng(9)
+    B, N = 3, 70
+    trees = np.stack([synth.random_tree(rng, N, depth=6, branching=4) for _ in range(B)])
+    trees[1, 0] = 0          # root must have parent -1
+    trees[2, 40] = 45        # parent after child
+    for Lmax in [64, 4000]:  # single split and split-KV paths
+        inp = synth.make_inputs(rng, B=B, N=N, Hq=8, Hkv=2, D=128, Lmax=Lmax, V=8,
+                                trees=trees, kv_len=np.full(B, Lmax), with_logits=False)
+        got, _ = gpu_attention(inp)
+        assert np.isnan(got[1]).all() and np.isnan(got[2]).all()
+        ref = oracle_attention({k: (v[:1] if isinstance(v, np.ndarray) and v.ndim and
+                                    v.shape[0] == B else v) for k, v in inp.items()})
+        assert np.abs(got[:1] - ref).max() <= TOL

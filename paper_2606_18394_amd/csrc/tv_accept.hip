@@ -5,18 +5,20 @@
 // prediction at its parent and the parent is accepted; the result is the
 // deepest accepted root-to-node path (Sec. 2.4 greedy rule; App. E).
 //
-// One workgroup per (node row, vocabulary split): 256 threads stream their
-// slice of the row with 16-byte loads and keep a running (value, index)
-// maximum; the workgroup reduces it with wave64 shuffles on a 64-bit key
-//   key = order-preserving(value) << 32 | (0xFFFFFFFF - index)
-// whose maximum is the largest value at its lowest index (-0.0 is folded
-// into +0.0 first, so equal values compare equal).  Every workgroup stores
-// its key and takes a ticket; the last workgroup of a sequence merges the
-// splits, validates the tree, computes acceptance for all nodes at once by
-// pointer jumping over the parent links (O(log depth) rounds), picks the
-// deepest accepted node (lowest index on ties) and writes the path.  It also
-// zeroes the keys it consumed and the sequence's ticket, so the workspace is
-// all-zero again after every call, whatever shapes the next call uses.
+// Two kernels, no atomics:
+//   scan    one workgroup per (node row, vocabulary split).  256 threads
+//           stream their slice with 16-byte loads, kScanLoadsPerThread of
+//           them in flight per thread, and keep a running first maximum;
+//           the workgroup reduces it with wave64 shuffles on the 64-bit key
+//             key = order-preserving(value) << 32 | (0xFFFFFFFF - index)
+//           whose maximum is the largest value at its lowest index (-0.0 is
+//           folded into +0.0 first, so equal values compare equal), and
+//           stores the key in the workspace.
+//   finish  one workgroup per sequence: merges the split keys into the
+//           per-node argmax, validates the tree, computes acceptance for all
+//           nodes at once by pointer jumping over the parent links
+//           (O(log depth) rounds), picks the deepest accepted node (lowest
+//           index on ties) and writes the path.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -32,7 +34,6 @@ struct AcceptArgs {
   int32_t* path;
   int32_t* tgt_out;
   unsigned long long* part;
-  unsigned int* tickets;
   int B, N, V, Dmax, nsplit;
   long long cps;  // chunks per split
 };
@@ -58,8 +59,8 @@ __device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long k)
   return k;
 }
 
-// Running first-maximum over a thread's elements, visited in increasing
-// index order: a strictly larger value replaces the current best.
+// Running first maximum over a thread's elements, visited in increasing
+// index order: only a strictly larger value replaces the current best.
 struct Best {
   float v;
   unsigned int i;
@@ -73,13 +74,27 @@ struct Best {
   }
 };
 
+template <bool F32>
+__device__ __forceinline__ void see_chunk(Best& best, const uint4& w, unsigned int i0) {
+  const unsigned int ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    if (F32) {
+      best.see(__uint_as_float(ws[k]), i0 + k);
+    } else {
+      best.see(__uint_as_float(ws[k] << 16), i0 + 2 * k);
+      best.see(__uint_as_float(ws[k] & 0xFFFF0000u), i0 + 2 * k + 1);
+    }
+  }
+}
+
 template <bool F32, bool VEC>
-__global__ __launch_bounds__(256) void accept_kernel(AcceptArgs a) {
-  constexpr int E = VEC ? (F32 ? 4 : 8) : 1;     // elements per chunk
+__global__ __launch_bounds__(kScanThreads) void accept_scan(AcceptArgs a) {
+  constexpr int E = VEC ? (F32 ? 4 : 8) : 1;  // elements per chunk
+  constexpr int L = kScanLoadsPerThread;
   const int tid = threadIdx.x;
-  const int row = blockIdx.x / a.nsplit;          // b * N + i
+  const int row = blockIdx.x / a.nsplit;       // b * N + i
   const int split = blockIdx.x % a.nsplit;
-  const int b = row / a.N;
   const long long nchunks = ((long long)a.V + E - 1) / E;
   const long long c0 = (long long)split * a.cps;
   const long long c1 = c0 + a.cps < nchunks ? c0 + a.cps : nchunks;
@@ -88,94 +103,69 @@ __global__ __launch_bounds__(256) void accept_kernel(AcceptArgs a) {
   if (VEC) {
     const uint4* base = reinterpret_cast<const uint4*>(
         (const char*)a.logits + (size_t)row * a.V * (F32 ? 4 : 2));
-    long long c = c0 + tid;
-    // four 16-byte loads in flight per thread
-    for (; c + 3 * 256 < c1; c += 4 * 256) {
-      uint4 w[4];
+    // rounds of L loads per thread, all issued before any is used
+    for (long long c = c0 + tid; c < c1; c += (long long)L * kScanThreads) {
+      uint4 w[L];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) w[u] = base[c + u * 256];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const unsigned int i0 = (unsigned int)((c + u * 256) * E);
-        const unsigned int ws[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          if (F32) {
-            best.see(__uint_as_float(ws[k]), i0 + k);
-          } else {
-            best.see(__uint_as_float(ws[k] << 16), i0 + 2 * k);
-            best.see(__uint_as_float(ws[k] & 0xFFFF0000u), i0 + 2 * k + 1);
-          }
-        }
+      for (int u = 0; u < L; ++u) {
+        const long long cu = c + (long long)u * kScanThreads;
+        if (cu < c1) w[u] = base[cu];
       }
-    }
-    for (; c < c1; c += 256) {
-      const uint4 w = base[c];
-      const unsigned int i0 = (unsigned int)(c * E);
-      const unsigned int ws[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        if (F32) {
-          best.see(__uint_as_float(ws[k]), i0 + k);
-        } else {
-          best.see(__uint_as_float(ws[k] << 16), i0 + 2 * k);
-          best.see(__uint_as_float(ws[k] & 0xFFFF0000u), i0 + 2 * k + 1);
-        }
+      for (int u = 0; u < L; ++u) {
+        const long long cu = c + (long long)u * kScanThreads;
+        if (cu < c1) see_chunk<F32>(best, w[u], (unsigned int)(cu * E));
       }
     }
   } else {
-    for (long long c = c0 + tid; c < c1; c += 256) {
+    for (long long c = c0 + tid; c < c1; c += kScanThreads) {
       float x;
       if (F32) {
         x = reinterpret_cast<const float*>(a.logits)[(size_t)row * a.V + c];
       } else {
-        const unsigned short h = reinterpret_cast<const unsigned short*>(a.logits)[(size_t)row * a.V + c];
+        const unsigned short h =
+            reinterpret_cast<const unsigned short*>(a.logits)[(size_t)row * a.V + c];
         x = __uint_as_float((unsigned int)h << 16);
       }
       best.see(x, (unsigned int)c);
     }
   }
 
-  __shared__ unsigned long long red[4];
-  __shared__ int last;
+  __shared__ unsigned long long red[kScanThreads / 64];
   unsigned long long key = best.any ? make_key(best.v, best.i) : 0ull;
   key = wave_max_u64(key);
   if ((tid & 63) == 0) red[tid >> 6] = key;
   __syncthreads();
   if (tid == 0) {
-    key = umax64(umax64(red[0], red[1]), umax64(red[2], red[3]));
+    key = red[0];
+#pragma unroll
+    for (int k = 1; k < kScanThreads / 64; ++k) key = umax64(key, red[k]);
     a.part[(size_t)row * a.nsplit + split] = key;
-    __threadfence();
-    const unsigned int ticket = atomicAdd(&a.tickets[b], 1u);
-    last = ticket == (unsigned int)(a.N * a.nsplit - 1);
   }
-  __syncthreads();
-  if (!last) return;
-  __threadfence();
+}
 
-  // ---- last workgroup of sequence b: finish the sequence
+__global__ __launch_bounds__(256) void accept_finish(AcceptArgs a) {
   __shared__ short par[kMaxNodes];
   __shared__ int tgt[kMaxNodes];
   __shared__ unsigned char ok[2][kMaxNodes];
   __shared__ short jmp[2][kMaxNodes];
   __shared__ short dep[2][kMaxNodes];
   __shared__ unsigned int best_key;
+  const int tid = threadIdx.x;
+  const int b = blockIdx.x;
   const int N = a.N;
   int bad = 0;
   for (int i = tid; i < N; i += 256) {
     const size_t r = (size_t)b * N + i;
     unsigned long long k = 0ull;
-    for (int s = 0; s < a.nsplit; ++s) {
-      k = umax64(k, __hip_atomic_load(&a.part[r * a.nsplit + s], __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_AGENT));
-      a.part[r * a.nsplit + s] = 0ull;  // leave the workspace all-zero
-    }
+    for (int s = 0; s < a.nsplit; ++s) k = umax64(k, a.part[r * a.nsplit + s]);
     const int t = (int)(0xFFFFFFFFu - (unsigned int)k);
     tgt[i] = t;
     if (a.tgt_out) a.tgt_out[r] = t;
     const int p = a.parent[r];
-    bad |= (i == 0) ? (p != -1) : (p < 0 || p >= i);
-    par[i] = (short)(bad ? 0 : p);
+    const int badi = (i == 0) ? (p != -1) : (p < 0 || p >= i);
+    bad |= badi;
+    par[i] = (short)(badi ? 0 : p);
   }
   if (tid == 0) best_key = 0u;
   bad = __syncthreads_or(bad);
@@ -192,8 +182,8 @@ __global__ __launch_bounds__(256) void accept_kernel(AcceptArgs a) {
       }
     }
     __syncthreads();
-    // pointer jumping: after the loop jmp = root, dep = depth, ok = every
-    // node on the root path matches its parent's prediction
+    // pointer jumping: afterwards jmp = root, dep = depth and ok = every
+    // node on the root path matches the prediction at its parent
     int cur = 0, more;
     do {
       const int nxt = cur ^ 1;
@@ -213,7 +203,7 @@ __global__ __launch_bounds__(256) void accept_kernel(AcceptArgs a) {
         const unsigned int k = ((unsigned int)dep[cur][i] << 16) | (0xFFFFu - (unsigned int)i);
         mk = mk > k ? mk : k;
       }
-    atomicMax(&best_key, mk);
+    atomicMax(&best_key, mk);  // LDS atomic, one per thread
     __syncthreads();
   }
   const unsigned int bk = best_key;
@@ -221,7 +211,7 @@ __global__ __launch_bounds__(256) void accept_kernel(AcceptArgs a) {
   const int len = bad || depth + 1 > a.Dmax ? -1 : depth + 1;
   int32_t* pth = a.path + (size_t)b * a.Dmax;
   for (int k = tid; k < a.Dmax; k += 256)
-    if (k >= len) pth[k] = -1;       // len == -1 clears the whole row
+    if (k >= len) pth[k] = -1;  // len == -1 clears the whole row
   if (tid == 0) {
     if (len > 0) {
       int u = (int)(0xFFFFu - (bk & 0xFFFFu));
@@ -231,7 +221,6 @@ __global__ __launch_bounds__(256) void accept_kernel(AcceptArgs a) {
       }
     }
     a.accept_len[b] = len;
-    a.tickets[b] = 0u;
   }
 }
 
@@ -249,21 +238,24 @@ hipError_t launch_accept(const void* logits, int f32, const int32_t* draft, cons
   a.accept_len = accept_len;
   a.path = path;
   a.tgt_out = tgt_out;
-  a.tickets = (unsigned int*)ws;
-  a.part = (unsigned long long*)((char*)ws + p.ticket_bytes);
+  a.part = (unsigned long long*)ws;
   a.B = B;
   a.N = N;
   a.V = V;
   a.Dmax = Dmax;
   a.nsplit = p.nsplit;
   a.cps = p.chunks_per_split;
+  const dim3 g(p.grid), t(kScanThreads);
   if (f32) {
-    if (vec) hipLaunchKernelGGL((accept_kernel<true, true>), dim3(p.grid), dim3(256), 0, st, a);
-    else hipLaunchKernelGGL((accept_kernel<true, false>), dim3(p.grid), dim3(256), 0, st, a);
+    if (vec) hipLaunchKernelGGL((accept_scan<true, true>), g, t, 0, st, a);
+    else hipLaunchKernelGGL((accept_scan<true, false>), g, t, 0, st, a);
   } else {
-    if (vec) hipLaunchKernelGGL((accept_kernel<false, true>), dim3(p.grid), dim3(256), 0, st, a);
-    else hipLaunchKernelGGL((accept_kernel<false, false>), dim3(p.grid), dim3(256), 0, st, a);
+    if (vec) hipLaunchKernelGGL((accept_scan<false, true>), g, t, 0, st, a);
+    else hipLaunchKernelGGL((accept_scan<false, false>), g, t, 0, st, a);
   }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(accept_finish, dim3(B), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

@@ -3,7 +3,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "../../include/treeverify.h"
+#include "treeverify.h"
 #include "tv_plan.h"
 
 static_assert(TV_MAX_NODES == tv::kMaxNodes, "node limit mismatch");

@@ -7,22 +7,28 @@
 // equations).  The ancestor relation is rebuilt inside each workgroup as a
 // bitmask in LDS from the parent array; no dense mask ever exists (App. E).
 //
-// Work decomposition (one workgroup = 4 wave64s):
-//   * rows of one (sequence b, KV head g) pair are the N*G (node, head in
-//     group) pairs; a workgroup takes RB consecutive rows;
-//   * the keys are cut into 32-key tiles: ceil(kv_len/32) cache tiles, then
-//     the tree tiles up to the last node of the row block (a node never sees
-//     a later node since parents precede children);
-//   * the tiles are split into S contiguous ranges (split-KV); inside a
-//     workgroup the 4 waves take every 4th tile, each with all RB rows, so
-//     every K/V byte is read from memory once per workgroup.
-// Per 32-key step a wave computes S^T = K Q^T with v_mfma_f32_16x16x32_bf16
-// (keys on the M side, rows on the N side), runs an fp32 online softmax in
-// base 2 on the accumulators, and accumulates O^T += V^T P^T, where P^T is
-// taken straight from the S^T accumulators (the 32 keys of one step are
-// ordered so the B operand needs no data movement) and V^T comes from LDS
-// with ds_read_b64_tr_b16 transposing reads.  The 4 waves merge their
-// (max, sum, O) in LDS; with S > 1 a second kernel merges the splits.
+// Work decomposition.  Rows of one (sequence b, KV head g) pair are the N*G
+// (node, head-in-group) pairs, row r = node * G + head.  Keys are cut into
+// 32-key tiles: ceil(kv_len/32) cache tiles, then the tree tiles up to the
+// last node of the row block (a node never sees a later node because
+// parents precede children).  The tiles are cut into S contiguous chunks of
+// a fixed size (split-KV).  One workgroup = 4 wave64s takes one row block
+// and one chunk, in one of two arrangements:
+//   * keys mode (64-row blocks, for short trees): every wave owns all 64
+//     rows and every 4th tile, streams its tiles through a private LDS ring,
+//     and the 4 waves merge their partial softmax states in LDS at the end;
+//   * rows mode (256-row blocks, for large trees or GQA groups): every wave
+//     owns 64 rows and all 4 waves consume one shared LDS ring, so each K/V
+//     byte fetched serves 256 rows.
+// K and V tiles move HBM -> LDS with global_load_lds_dwordx4 (no register
+// staging), rows XOR-swizzled in 16-byte chunks so the reads below are free
+// of bank conflicts.  Per 32-key tile a wave computes S^T = K Q^T with
+// v_mfma_f32_16x16x32_bf16 (keys on the M side, its 64 rows on the N side),
+// runs an fp32 base-2 online softmax on the accumulators with a lazily moved
+// reference maximum, and accumulates O^T += V^T P^T: P^T comes straight from
+// the S^T accumulators (the 32 keys are ordered so the B operand needs no
+// data movement) and V^T from ds_read_b64_tr_b16 transposing reads.  With
+// S > 1 a second kernel merges the chunks' (max, sum, O) partials.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -35,6 +41,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 struct AttnArgs {
   const __bf16* q;
@@ -47,7 +54,7 @@ struct AttnArgs {
   __bf16* out;
   f32x4* ws_o;
   float2* ws_ml;
-  int B, N, Hq, Hkv, Lmax, G, M, nRB, S, nwork;
+  int B, N, Hq, Hkv, Lmax, G, M, nRB, S, chunk, nwork;
   float c;  // scale * log2(e): scores live in base-2 exponent units
 };
 
@@ -57,44 +64,168 @@ __device__ __forceinline__ float wave_max_across_groups(float v) {
   return v;
 }
 
-__device__ __forceinline__ float wave_sum_across_groups(float v) {
-  v += __shfl_xor(v, 16);
-  v += __shfl_xor(v, 32);
-  return v;
+// 16 bytes per lane from global memory straight into LDS: lane i's bytes
+// land at lds_addr + 16 * i (lds_addr is wave-uniform).  Issued as inline assembly so the compiler does
+// not serialise every later LDS read behind it; completion is awaited with
+// explicit vmcnt waits.
+__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(gptr)
+               : "memory");
 }
 
-__device__ __forceinline__ void decode_work(const AttnArgs& a, int& b, int& g,
-                                            int& rb, int& s) {
-  // Consecutive work items (all row blocks and splits of one (b, g) pair)
-  // go to the same XCD: workgroups are dispatched round-robin over the 8
-  // XCDs, so item w runs on XCD w / per.
-  const int per = gridDim.x / kXcds;
-  int w = (blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
-  s = w % a.S;
-  w /= a.S;
-  rb = w % a.nRB;
-  w /= a.nRB;
-  g = w % a.Hkv;
-  b = w / a.Hkv;
+// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding).
+template <int n>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-template <int D, int RB>
+// n is (tiles still in flight) x (DMAs per tile); only these values occur
+__device__ __forceinline__ void wait_vm_dyn(int n) {
+  switch (n) {
+    case 2: wait_vm<2>(); break;
+    case 4: wait_vm<4>(); break;
+    case 6: wait_vm<6>(); break;
+    case 8: wait_vm<8>(); break;
+    case 12: wait_vm<12>(); break;
+    case 16: wait_vm<16>(); break;
+    case 24: wait_vm<24>(); break;
+    case 32: wait_vm<32>(); break;
+    case 48: wait_vm<48>(); break;
+    default: wait_vm<0>(); break;
+  }
+}
+
+// Layout of one 32-key tile in LDS: row-major, D bf16 per row, 16-byte
+// chunks XOR-swizzled by the row so 16 rows read at the same logical chunk
+// hit 16 different bank groups.
+template <int D>
+struct TileLayout {
+  static constexpr int kRowBytes = 2 * D;
+  static constexpr int kCPR = D / 8;               // 16-byte chunks per row
+  static constexpr int kBytes = kKeyTile * kRowBytes;
+  static constexpr int kDma = kBytes / 1024;       // 1 KB DMA instructions per tile
+  static constexpr int kRowsPerDma = 64 / kCPR;
+  __device__ static __forceinline__ int swz(int r) {
+    return D == 128 ? (r & 15) : ((r >> 1) & 7);
+  }
+  __device__ static __forceinline__ int off(int r, int chunk) {
+    return r * kRowBytes + ((chunk ^ swz(r)) << 4);
+  }
+};
+
+// Where a wave's K/V rows come from: the padded cache of one (sequence, KV
+// head) pair, then its tree K/V.
+struct TreeSrc {
+  const __bf16* kcache;
+  const __bf16* vcache;
+  const __bf16* ktree;
+  const __bf16* vtree;
+  int krow;   // elements between consecutive keys
+  int kvl;    // valid cache rows
+  int nct;    // cache tiles
+  int i_hi;   // last tree node the row block can see
+};
+
+// Issue this lane's DMA instructions for tile t into the stage at kdst (K
+// tile, then V tile).  Rows past the valid range are clamped onto a valid
+// row: the mask gives them zero weight, the clamp keeps reads in range.
+template <int D, bool ROWS, int PW>
+__device__ __forceinline__ void issue_tile(const TreeSrc& src, const int (&dma_off)[PW], int wave,
+                                           int lane, int t, uint32_t kdst) {
+  using TL = TileLayout<D>;
+  if (t < src.nct && (t + 1) * kKeyTile <= src.kvl) {
+    const size_t tofs = (size_t)t * kKeyTile * src.krow;
+#pragma unroll
+    for (int k = 0; k < PW; ++k) {
+      const int q = ROWS ? wave * PW + k : k;
+      const bool isv = q >= TL::kDma;
+      dma16((isv ? src.vcache : src.kcache) + tofs + dma_off[k],
+            kdst + (isv ? TL::kBytes : 0) + (q % TL::kDma) * 1024);
+    }
+    return;
+  }
+#pragma unroll
+  for (int k = 0; k < PW; ++k) {
+    const int q = ROWS ? wave * PW + k : k;
+    const bool isv = q >= TL::kDma;
+    const int r = (q % TL::kDma) * TL::kRowsPerDma + lane / TL::kCPR;
+    const int col = ((lane % TL::kCPR) ^ TL::swz(r)) * 8;
+    const __bf16* p;
+    if (t < src.nct) {
+      const int key = min(t * kKeyTile + r, src.kvl - 1);
+      p = (isv ? src.vcache : src.kcache) + (size_t)key * src.krow;
+    } else {
+      const int u = min((t - src.nct) * kKeyTile + r, src.i_hi);
+      p = (isv ? src.vtree : src.ktree) + (size_t)u * src.krow;
+    }
+    dma16(p + col, kdst + (isv ? TL::kBytes : 0) + (q % TL::kDma) * 1024);
+  }
+}
+
+// Softmax weights of one 32-key tile (base 2, reference m per row) as the
+// bf16 P^T operand, their row sums (ones^T P^T) into lacc, and O^T += V^T
+// P^T with V^T from transposing LDS reads: lane (g4, l16) receives
+// V[key 4*g4 + j (+16)][16*dt + l16], the key order of the P^T operand.
+template <int D, int NT>
+__device__ __forceinline__ void softmax_pv(const f32x4 (&sc)[2][NT], const float (&m)[NT], float c,
+                                           const unsigned char* vt_lds, const bf16x8& ones,
+                                           f32x4 (&o)[D / 16][NT], f32x4 (&lacc)[NT], int g4,
+                                           int l16) {
+  using TL = TileLayout<D>;
+  bf16x8 pf[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const float mref = fmaxf(m[nt], -3.0e38f);  // rows with nothing visible yet: weights 0
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        pf[nt][4 * tt + j] = (__bf16)__builtin_amdgcn_exp2f(fmaf(sc[tt][nt][j], c, -mref));
+    lacc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[nt], lacc[nt], 0, 0, 0);
+  }
+#pragma unroll
+  for (int dt = 0; dt < D / 16; ++dt) {
+    const int rr = 4 * g4 + (l16 >> 2);
+    const int chunk = 2 * dt + ((l16 & 3) >> 1);
+    const int inb = 8 * (l16 & 1);
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4*)(vt_lds + TL::off(rr, chunk) + inb));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4*)(vt_lds + TL::off(rr + 16, chunk) + inb));
+    const bf16x4 lob = __builtin_bit_cast(bf16x4, lo), hib = __builtin_bit_cast(bf16x4, hi);
+    const bf16x8 vf = {lob[0], lob[1], lob[2], lob[3], hib[0], hib[1], hib[2], hib[3]};
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+      o[dt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[nt], o[dt][nt], 0, 0, 0);
+  }
+}
+
+template <int D, bool ROWS>
 __global__ __launch_bounds__(256, 1) void attn_main(AttnArgs a) {
-  constexpr int NT = RB / 16;        // 16-row tiles
-  constexpr int NC = D / 32;         // 32-wide head-dim chunks (QK^T)
-  constexpr int DT = D / 16;         // 16-wide head-dim tiles (PV)
-  constexpr int CPR = D / 8;         // 16-byte chunks per K/V row
-  constexpr int VL = kKeyTile * CPR / 64;  // V chunks per lane per step
-  constexpr int VS = D * 2 + 32;     // LDS row stride of the V tile, bytes
+  using TL = TileLayout<D>;
+  constexpr int RB = ROWS ? kRowsModeRB : kKeysModeRB;  // rows per workgroup
+  constexpr int NT = 4;                // 16-row tiles per wave (64 rows)
+  constexpr int NTG = RB / 16;         // 16-row tiles per workgroup
+  constexpr int NC = D / 32;           // 32-wide head-dim chunks (QK^T)
+  constexpr int DT = D / 16;           // 16-wide head-dim tiles (PV)
+  constexpr int STAGE = 2 * TL::kBytes;                 // K tile + V tile
+  constexpr int NS = ring_stages(D, ROWS);              // ring depth
+  constexpr int PW = ROWS ? 2 * TL::kDma / kWaves : 2 * TL::kDma;  // DMAs per wave per tile
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
-  {
-    const int per = gridDim.x / kXcds;
-    const int w = (blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
-    if (w >= a.nwork) return;
-  }
-  int b, g, rb, s;
-  decode_work(a, b, g, rb, s);
+  const int per = gridDim.x / kXcds;
+  int w = (blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
+  if (w >= a.nwork) return;
+  const int s = w % a.S;
+  w /= a.S;
+  const int rb = w % a.nRB;
+  w /= a.nRB;
+  const int g = w % a.Hkv;
+  const int b = w / a.Hkv;
+  if (b >= a.B) return;  // never taken for a consistent plan
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g4 = lane >> 4, l16 = lane & 15;
 
@@ -106,42 +237,54 @@ __global__ __launch_bounds__(256, 1) void attn_main(AttnArgs a) {
   const int nct = (kvl + kKeyTile - 1) / kKeyTile;
   const int ntt = i_hi / kKeyTile + 1;
   const int T = nct + ntt;
-  const int per_split = (T + a.S - 1) / a.S;
-  const int t0 = s * per_split;
-  const int t1 = min(T, t0 + per_split);
-  const bool has_tree = t1 > nct;
+  const int t0 = s * a.chunk;
+  const int t1 = min(T, t0 + a.chunk);
+  const bool has_tree = t0 < t1 && t1 > nct;
 
-  unsigned char* vbuf = smem + (size_t)wave * kKeyTile * VS;
-  uint32_t* anc = reinterpret_cast<uint32_t*>(smem + (size_t)kWaves * kKeyTile * VS);
+  constexpr int RING = ROWS ? NS * STAGE : kWaves * NS * STAGE;
+  const uint32_t smem_base = (uint32_t)(uintptr_t)smem;
+  const uint32_t ring = smem_base + (ROWS ? 0 : wave * NS * STAGE);
+  const unsigned char* ring_ptr = smem + (ROWS ? 0 : wave * NS * STAGE);
+  uint32_t* anc = reinterpret_cast<uint32_t*>(smem + RING);
   const int anc_nodes = RB / a.G + 2;
   int32_t* par = reinterpret_cast<int32_t*>(anc + anc_nodes * ntt);
   int* flag = par + a.N;
 
-  const size_t cache_base = (size_t)b * a.Lmax * a.Hkv * D + (size_t)g * D;
-  const size_t tree_base = (size_t)b * a.N * a.Hkv * D + (size_t)g * D;
   const size_t krow = (size_t)a.Hkv * D;  // elements between consecutive keys
+  const __bf16* kcache = a.kc + (size_t)b * a.Lmax * krow + (size_t)g * D;
+  const __bf16* vcache = a.vc + (size_t)b * a.Lmax * krow + (size_t)g * D;
+  const __bf16* ktree = a.kt + (size_t)b * a.N * krow + (size_t)g * D;
+  const __bf16* vtree = a.vt + (size_t)b * a.N * krow + (size_t)g * D;
 
-  // Element offset of key kk (0..31) of tile t, and whether it is a tree key.
-  // Keys past the valid range are clamped onto a valid row; the mask zeroes
-  // their weight, so clamping only keeps the reads inside the tensors.
-  auto key_row = [&](int t, int kk, bool& tree) -> size_t {
-    if (t < nct) {
-      int k = t * kKeyTile + kk;
-      k = k < kvl ? k : kvl - 1;
-      tree = false;
-      return cache_base + (size_t)k * krow;
-    }
-    int u = (t - nct) * kKeyTile + kk;
-    u = u <= i_hi ? u : i_hi;
-    tree = true;
-    return tree_base + (size_t)u * krow;
-  };
+  // This lane's share of the DMA instructions of one tile: instruction q
+  // (q < kDma: K, else V) covers tile rows j*kRowsPerDma.. (j = q % kDma);
+  // lane i fetches row j*kRowsPerDma + i/kCPR at the logical chunk that the
+  // swizzle places at physical chunk i % kCPR.  dma_off is that element
+  // offset for a full cache tile starting at key 0.
+  int dma_off[PW];
+#pragma unroll
+  for (int k = 0; k < PW; ++k) {
+    const int q = ROWS ? wave * PW + k : k;
+    const int r = (q % TL::kDma) * TL::kRowsPerDma + lane / TL::kCPR;
+    dma_off[k] = r * (int)krow + ((lane % TL::kCPR) ^ TL::swz(r)) * 8;
+  }
+  const TreeSrc src{kcache, vcache, ktree, vtree, (int)krow, kvl, nct, i_hi};
+
+  // this wave's tiles: rows mode walks t0..t1-1 in step with the other
+  // waves, keys mode takes every 4th tile
+  const int my_first = ROWS ? t0 : t0 + wave;
+  const int my_step = ROWS ? 1 : kWaves;
+  const int n_my = my_first < t1 ? (t1 - my_first + my_step - 1) / my_step : 0;
+#pragma unroll
+  for (int i = 0; i < NS - 1; ++i)
+    if (i < n_my) issue_tile<D, ROWS, PW>(src, dma_off, wave, lane, my_first + i * my_step, ring + i * STAGE);
 
   // ---- queries: B operand of S^T = K Q^T, lane holds Q[row l16][8*g4 .. +8]
+  const int wrow0 = r0 + (ROWS ? 64 * wave : 0);
   bf16x8 qf[NT][NC];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    const int r = r0 + nt * 16 + l16;
+    const int r = wrow0 + nt * 16 + l16;
     const bool ok = r < a.M;
     const int node = ok ? r / a.G : 0;
     const int h = g * a.G + (ok ? r % a.G : 0);
@@ -165,14 +308,14 @@ __global__ __launch_bounds__(256, 1) void attn_main(AttnArgs a) {
     bad = __syncthreads_or(bad);
     const int nodes = i_hi - i_lo + 1;
     for (int t = tid; t < nodes; t += 256) {
-      uint32_t* w = anc + t * ntt;
-      for (int k = 0; k < ntt; ++k) w[k] = 0u;
+      uint32_t* wd = anc + t * ntt;
+      for (int k = 0; k < ntt; ++k) wd[k] = 0u;
       int u = i_lo + t;
       for (;;) {
-        w[u >> 5] |= 1u << (u & 31);
+        wd[u >> 5] |= 1u << (u & 31);
         if (u == 0) break;
         const int p = par[u];
-        if (p < 0 || p >= u) break;  // invalid tree: output becomes NaN
+        if (p < 0 || p >= u) break;  // invalid tree: the output becomes NaN
         u = p;
       }
     }
@@ -180,142 +323,176 @@ __global__ __launch_bounds__(256, 1) void attn_main(AttnArgs a) {
     __syncthreads();
   }
 
-  f32x4 o[DT][NT];
-  float m[NT], lsum[NT];
+  // O^T accumulators, and l: row sums of the bf16 weights, accumulated on
+  // the matrix cores as ones^T P^T so numerator and denominator see the same
+  // rounded weights (all 4 entries of lacc[nt] hold the lane's row sum)
+  f32x4 o[DT][NT], lacc[NT];
+  float m[NT];
+  const bf16x8 ones = {(__bf16)1.f, (__bf16)1.f, (__bf16)1.f, (__bf16)1.f,
+                       (__bf16)1.f, (__bf16)1.f, (__bf16)1.f, (__bf16)1.f};
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     m[nt] = -INFINITY;
-    lsum[nt] = 0.f;
+    lacc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) o[dt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
+  // node of this lane's row in each 16-row tile, relative to i_lo
+  int node_rel[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int r = wrow0 + nt * 16 + l16;
+    node_rel[nt] = (r < a.M ? r : a.M - 1) / a.G - i_lo;
+  }
 
-  // K fragments (A operand of S^T): lane holds K[key 16*tt + l16][32c + 8*g4 ..]
-  bf16x8 kn[2][NC];
-  // V chunks staged through registers: chunk lane + 64*j of the 32 x D tile
-  bf16x8 vn[VL];
-  auto load_tile = [&](int t) {
-#pragma unroll
-    for (int tt = 0; tt < 2; ++tt) {
-      bool tree;
-      const size_t off = key_row(t, 16 * tt + l16, tree) + 8 * g4;
-      const __bf16* kp = (tree ? a.kt : a.kc) + off;
-#pragma unroll
-      for (int c = 0; c < NC; ++c) kn[tt][c] = *reinterpret_cast<const bf16x8*>(kp + 32 * c);
-    }
-#pragma unroll
-    for (int j = 0; j < VL; ++j) {
-      const int id = lane + 64 * j;
-      bool tree;
-      const size_t off = key_row(t, id / CPR, tree) + 8 * (id % CPR);
-      vn[j] = *reinterpret_cast<const bf16x8*>((tree ? a.vt : a.vc) + off);
-    }
-  };
-
-  int t = t0 + wave;
-  if (t < t1) load_tile(t);
-  for (; t < t1; t += kWaves) {
-    // stage V of tile t into this wave's LDS tile (row-major, padded rows)
-#pragma unroll
-    for (int j = 0; j < VL; ++j) {
-      const int id = lane + 64 * j;
-      *reinterpret_cast<bf16x8*>(vbuf + (id / CPR) * VS + (id % CPR) * 16) = vn[j];
-    }
-    bf16x8 kc[2][NC];
-#pragma unroll
-    for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-      for (int c = 0; c < NC; ++c) kc[tt][c] = kn[tt][c];
-    const int tn = t + kWaves;
-    if (tn < t1) load_tile(tn);
-
-    // S^T tile: lane holds S^T[key 16*tt + 4*g4 + j][row 16*nt + l16]
-    f32x4 sc[2][NT];
-#pragma unroll
-    for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int c = 0; c < NC; ++c)
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kc[tt][c], qf[nt][c], acc, 0, 0, 0);
-        sc[tt][nt] = acc;
+  // The tile loop runs without touching O on the vector ALUs, so the O
+  // accumulators stay in accumulation registers; a tile whose maximum moves
+  // a row's reference leaves the inner loop, O and l are rescaled, and the
+  // tile is finished outside.
+  constexpr float kSlack = 8.f;
+  f32x4 sc[2][NT];
+  float mx[NT];
+  const unsigned char* vt_lds = ring_ptr + TL::kBytes;
+  int i = 0;
+  while (i < n_my) {
+    bool pending = false;
+    for (; i < n_my; ++i) {
+      const int t = my_first + i * my_step;
+      if (ROWS) {
+        // my DMAs of tile i are done once at most min(later tiles, NS-2)
+        // tiles' DMAs are outstanding; the barrier makes everyone's visible
+        // and guarantees every wave has finished reading tile i-1's slot
+        const int later = min(n_my - 1 - i, NS - 2);
+        wait_vm_dyn(later * PW);
+        __syncthreads();
+        if (i + NS - 1 < n_my)
+          issue_tile<D, ROWS, PW>(src, dma_off, wave, lane, my_first + (i + NS - 1) * my_step,
+                                  ring + ((i + NS - 1) % NS) * STAGE);
+      } else {
+        if (i + NS - 1 < n_my)
+          issue_tile<D, ROWS, PW>(src, dma_off, wave, lane, my_first + (i + NS - 1) * my_step,
+                                  ring + ((i + NS - 1) % NS) * STAGE);
+        const int later = min(n_my - 1 - i, NS - 1);
+        wait_vm_dyn(later * PW);
       }
+      const unsigned char* kt_lds = ring_ptr + (i % NS) * STAGE;
+      vt_lds = kt_lds + TL::kBytes;
 
-    // masks: the cache tail and the tree tiles
-    if (t < nct) {
-      if ((t + 1) * kKeyTile > kvl) {
-#pragma unroll
-        for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const bool vis = t * kKeyTile + 16 * tt + 4 * g4 + j < kvl;
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt)
-              if (!vis) sc[tt][nt][j] = -INFINITY;
-          }
-      }
-    } else {
-      const int word = t - nct;
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int r = r0 + nt * 16 + l16;
-        int node = (r < a.M ? r : a.M - 1) / a.G - i_lo;
-        const uint32_t bits = anc[node * ntt + word];
-#pragma unroll
-        for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            if (!((bits >> (16 * tt + 4 * g4 + j)) & 1u)) sc[tt][nt][j] = -INFINITY;
-      }
-    }
-
-    // online softmax (base 2) and the bf16 P^T operand
-    bf16x8 pf[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      float mx = fmaxf(fmaxf(fmaxf(sc[0][nt][0], sc[0][nt][1]), fmaxf(sc[0][nt][2], sc[0][nt][3])),
-                       fmaxf(fmaxf(sc[1][nt][0], sc[1][nt][1]), fmaxf(sc[1][nt][2], sc[1][nt][3])));
-      mx = wave_max_across_groups(mx) * a.c;
-      const float mnew = fmaxf(m[nt], mx);
-      const float mref = mnew == -INFINITY ? 0.f : mnew;
-      const float alpha = __builtin_amdgcn_exp2f(m[nt] - mref);
-      m[nt] = mnew;
-      float ps = 0.f;
+      // S^T tile: lane holds S^T[key 16*tt + 4*g4 + j][row 16*nt + l16]
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(sc[tt][nt][j], a.c, -mref));
-          ps += p;
-          pf[nt][4 * tt + j] = (__bf16)p;
+        for (int nt = 0; nt < NT; ++nt) sc[tt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+          const bf16x8 kf =
+              *reinterpret_cast<const bf16x8*>(kt_lds + TL::off(16 * tt + l16, 4 * c + g4));
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt)
+            sc[tt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[nt][c], sc[tt][nt], 0, 0, 0);
         }
-      lsum[nt] = lsum[nt] * alpha + ps;
+
+      // masks: the cache tail and the tree tiles
+      if (t < nct) {
+        if ((t + 1) * kKeyTile > kvl) {
+#pragma unroll
+          for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const bool vis = t * kKeyTile + 16 * tt + 4 * g4 + j < kvl;
+#pragma unroll
+              for (int nt = 0; nt < NT; ++nt)
+                if (!vis) sc[tt][nt][j] = -INFINITY;
+            }
+        }
+      } else {
+        const int word = t - nct;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const uint32_t bits = anc[node_rel[nt] * ntt + word];
+#pragma unroll
+          for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              if (!((bits >> (16 * tt + 4 * g4 + j)) & 1u)) sc[tt][nt][j] = -INFINITY;
+        }
+      }
+
+      // Online softmax in base 2 with a lazily moved reference: a row's
+      // reference m (log2 units) only moves when its tile maximum exceeds it
+      // by more than kSlack, so rescaling is rare; weights stay below
+      // 2^kSlack, far inside the fp32 and bf16 ranges.
+      bool move = false;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        float v = fmaxf(fmaxf(sc[0][nt][0], sc[0][nt][1]), sc[0][nt][2]);
+        v = fmaxf(fmaxf(v, sc[0][nt][3]), sc[1][nt][0]);
+        v = fmaxf(fmaxf(v, sc[1][nt][1]), sc[1][nt][2]);
+        v = fmaxf(v, sc[1][nt][3]);
+        mx[nt] = wave_max_across_groups(v) * a.c;
+        move |= mx[nt] > m[nt] + kSlack;
+      }
+      if (__any(move)) {
+        pending = true;
+        break;
+      }
+      softmax_pv<D>(sc, m, a.c, vt_lds, ones, o, lacc, g4, l16);
+    }
+    if (!pending) break;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const bool moved = mx[nt] > m[nt] + kSlack;
+      // a row that has not moved keeps its scale (its m may still be -inf)
+      const float alpha = moved ? __builtin_amdgcn_exp2f(m[nt] - mx[nt]) : 1.f;
+      m[nt] = moved ? mx[nt] : m[nt];
+      lacc[nt] *= alpha;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) o[dt][nt] *= alpha;
     }
-
-    // O^T += V^T P^T; the transposing reads give lane (g4, l16) the values
-    // V[key 4*g4 + j (+16)][16*dt + l16], matching the key order of P^T
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      const unsigned char* src = vbuf + (4 * g4 + (l16 >> 2)) * VS + (16 * dt + 4 * (l16 & 3)) * 2;
-      typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(src));
-      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(src + 16 * VS));
-      const bf16x4 lob = __builtin_bit_cast(bf16x4, lo), hib = __builtin_bit_cast(bf16x4, hi);
-      const bf16x8 vf = {lob[0], lob[1], lob[2], lob[3], hib[0], hib[1], hib[2], hib[3]};
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-        o[dt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[nt], o[dt][nt], 0, 0, 0);
-    }
+    softmax_pv<D>(sc, m, a.c, vt_lds, ones, o, lacc, g4, l16);
+    ++i;
   }
 
-  // ---- merge the 4 waves (each saw a disjoint subset of this range's keys)
+  float lsum[NT];
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) lsum[nt] = wave_sum_across_groups(lsum[nt]);
+  for (int nt = 0; nt < NT; ++nt) lsum[nt] = lacc[nt][0];
   const int invalid = has_tree ? *flag : 0;
-  __syncthreads();  // V staging and tree tables are dead from here on
+  const int bg = b * a.Hkv + g;
+
+  // Final values of one 16x16 fragment (dt, ntg) of this workgroup's rows:
+  // either the normalised bf16 output (single chunk) or the chunk partial.
+  auto emit = [&](int dt, int ntg, const f32x4& acc, float mstar, float l) {
+    const int row = ntg * 16 + l16;
+    if (a.S == 1) {
+      const int r = r0 + row;
+      if (r < a.M) {
+        const int node = r / a.G, h = g * a.G + r % a.G;
+        const float inv = invalid ? NAN : 1.f / l;
+        const bf16x4 ov = {(__bf16)(acc[0] * inv), (__bf16)(acc[1] * inv),
+                           (__bf16)(acc[2] * inv), (__bf16)(acc[3] * inv)};
+        *reinterpret_cast<bf16x4*>(a.out + ((size_t)(b * a.N + node) * a.Hq + h) * D + 16 * dt +
+                                   4 * g4) = ov;
+      }
+    } else {
+      const size_t fr = ((size_t)(bg * a.nRB + rb) * a.S + s) * DT * NTG;
+      a.ws_o[(fr + dt * NTG + ntg) * 64 + lane] = acc;
+      if (dt == 0 && g4 == 0)
+        a.ws_ml[((size_t)(bg * a.nRB + rb) * a.S + s) * RB + row] = make_float2(mstar, l);
+    }
+  };
+
+  if (ROWS) {
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) emit(dt, wave * NT + nt, o[dt][nt], m[nt], lsum[nt]);
+    return;
+  }
+
+  // ---- keys mode: merge the 4 waves (disjoint key subsets, same rows)
+  __syncthreads();  // rings and tree tables are dead from here on
   f32x4* obuf = reinterpret_cast<f32x4*>(smem);
   float2* mlbuf = reinterpret_cast<float2*>(smem + (size_t)kWaves * RB * D * 4);
 #pragma unroll
@@ -327,53 +504,36 @@ __global__ __launch_bounds__(256, 1) void attn_main(AttnArgs a) {
     for (int nt = 0; nt < NT; ++nt) mlbuf[wave * RB + nt * 16 + l16] = make_float2(m[nt], lsum[nt]);
   }
   __syncthreads();
-
-  const int bg = b * a.Hkv + g;
   for (int f = wave; f < DT * NT; f += kWaves) {
     const int dt = f / NT, nt = f % NT;
     const int row = nt * 16 + l16;
     float mw[kWaves], mstar = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      mw[w] = mlbuf[w * RB + row].x;
-      mstar = fmaxf(mstar, mw[w]);
+    for (int k = 0; k < kWaves; ++k) {
+      mw[k] = mlbuf[k * RB + row].x;
+      mstar = fmaxf(mstar, mw[k]);
     }
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     float l = 0.f;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      const float e = mw[w] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw[w] - mstar);
-      l += e * mlbuf[w * RB + row].y;
-      acc += e * obuf[((w * DT + dt) * NT + nt) * 64 + lane];
+    for (int k = 0; k < kWaves; ++k) {
+      const float e = mw[k] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw[k] - mstar);
+      l += e * mlbuf[k * RB + row].y;
+      acc += e * obuf[((k * DT + dt) * NT + nt) * 64 + lane];
     }
-    if (a.S == 1) {
-      const int r = r0 + row;
-      if (r < a.M) {
-        const int node = r / a.G, h = g * a.G + r % a.G;
-        const float inv = invalid ? NAN : 1.f / l;
-        bf16x4 ov = {(__bf16)(acc[0] * inv), (__bf16)(acc[1] * inv), (__bf16)(acc[2] * inv),
-                     (__bf16)(acc[3] * inv)};
-        *reinterpret_cast<bf16x4*>(a.out + ((size_t)(b * a.N + node) * a.Hq + h) * D + 16 * dt +
-                                   4 * g4) = ov;
-      }
-    } else {
-      const size_t fr = ((size_t)(bg * a.nRB + rb) * a.S + s) * DT * NT;
-      a.ws_o[(fr + dt * NT + nt) * 64 + lane] = acc;
-      if (dt == 0 && g4 == 0)
-        a.ws_ml[((size_t)(bg * a.nRB + rb) * a.S + s) * RB + row] = make_float2(mstar, l);
-    }
+    emit(dt, nt, acc, mstar, l);
   }
 }
 
-// Merge the S key-range partials of every row: out = sum_s e_s O_s /
-// sum_s e_s l_s with e_s = 2^(m_s - max m).  One wave per 16x16 fragment.
+// Merge the S chunk partials of every row: out = sum_s e_s O_s / sum_s e_s
+// l_s with e_s = 2^(m_s - max m).  One wave per 16x16 fragment.
 template <int D, int RB>
 __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
-  constexpr int NT = RB / 16, DT = D / 16;
+  constexpr int NTG = RB / 16, DT = D / 16;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g4 = lane >> 4, l16 = lane & 15;
-  const int F = blockIdx.x * 4 + wave;       // fragment id, all 4 in one (b,g,rb)
-  const int per_blk = DT * NT;
+  const int F = blockIdx.x * 4 + wave;  // fragment id; all 4 of a block share (b,g,rb)
+  const int per_blk = DT * NTG;
   const int blk = F / per_blk, f = F % per_blk;
   const int rb = blk % a.nRB, bg = blk / a.nRB;
   const int b = bg / a.Hkv, g = bg % a.Hkv;
@@ -383,8 +543,8 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
     bad |= (i == 0) ? (p != -1) : (p < 0 || p >= i);
   }
   bad = __syncthreads_or(bad);
-  const int dt = f / NT, nt = f % NT;
-  const int row = nt * 16 + l16, r = rb * RB + row;
+  const int dt = f / NTG, ntg = f % NTG;
+  const int row = ntg * 16 + l16, r = rb * RB + row;
   if (r >= a.M) return;
   const size_t base = (size_t)(bg * a.nRB + rb) * a.S;
   float mstar = -INFINITY;
@@ -396,23 +556,25 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
     if (ml.x == -INFINITY) continue;
     const float e = __builtin_amdgcn_exp2f(ml.x - mstar);
     l += e * ml.y;
-    acc += e * a.ws_o[((base + s) * DT * NT + dt * NT + nt) * 64 + lane];
+    acc += e * a.ws_o[((base + s) * DT * NTG + dt * NTG + ntg) * 64 + lane];
   }
   const float inv = bad ? NAN : 1.f / l;
   const int node = r / a.G, h = g * a.G + r % a.G;
-  bf16x4 ov = {(__bf16)(acc[0] * inv), (__bf16)(acc[1] * inv), (__bf16)(acc[2] * inv),
-               (__bf16)(acc[3] * inv)};
-  *reinterpret_cast<bf16x4*>(a.out + ((size_t)(b * a.N + node) * a.Hq + h) * D + 16 * dt + 4 * g4) = ov;
+  const bf16x4 ov = {(__bf16)(acc[0] * inv), (__bf16)(acc[1] * inv), (__bf16)(acc[2] * inv),
+                     (__bf16)(acc[3] * inv)};
+  *reinterpret_cast<bf16x4*>(a.out + ((size_t)(b * a.N + node) * a.Hq + h) * D + 16 * dt +
+                             4 * g4) = ov;
 }
 
-template <int D, int RB>
+template <int D, bool ROWS>
 static hipError_t launch_attn_t(const AttnArgs& a, const AttnPlan& p, hipStream_t st) {
-  hipError_t e0 = hipFuncSetAttribute((const void*)attn_main<D, RB>,
-                                      hipFuncAttributeMaxDynamicSharedMemorySize,
-                                      (int)p.lds_bytes);
-  if (e0 != hipSuccess) return e0;
-  hipLaunchKernelGGL((attn_main<D, RB>), dim3(p.grid), dim3(256), p.lds_bytes, st, a);
-  hipError_t e = hipGetLastError();
+  constexpr int RB = ROWS ? kRowsModeRB : kKeysModeRB;
+  hipError_t e = hipFuncSetAttribute((const void*)attn_main<D, ROWS>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)p.lds_bytes);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((attn_main<D, ROWS>), dim3(p.grid), dim3(256), p.lds_bytes, st, a);
+  e = hipGetLastError();
   if (e != hipSuccess || p.S == 1) return e;
   const int frags = a.B * a.Hkv * p.nRB * (D / 16) * (RB / 16);
   hipLaunchKernelGGL((attn_combine<D, RB>), dim3(frags / 4), dim3(256), 0, st, a);
@@ -443,10 +605,12 @@ hipError_t launch_attention(const void* q, const void* kc, const void* vc, const
   a.M = p.M;
   a.nRB = p.nRB;
   a.S = p.S;
+  a.chunk = p.chunk;
   a.nwork = p.nwork;
   a.c = scale * 1.4426950408889634f;
-  if (D == 128) return p.RB == 64 ? launch_attn_t<128, 64>(a, p, st) : launch_attn_t<128, 32>(a, p, st);
-  return p.RB == 64 ? launch_attn_t<64, 64>(a, p, st) : launch_attn_t<64, 32>(a, p, st);
+  if (D == 128)
+    return p.rows_mode ? launch_attn_t<128, true>(a, p, st) : launch_attn_t<128, false>(a, p, st);
+  return p.rows_mode ? launch_attn_t<64, true>(a, p, st) : launch_attn_t<64, false>(a, p, st);
 }
 
 }  // namespace tv

@@ -1,0 +1,58 @@
+// Host-side check of the launch plans (tv_plan.h is plain C++): for each
+// shape on stdin ("B N Hq Hkv D Lmax V"), enumerate every launched
+// workgroup exactly as the kernels decode it and verify that the decoded
+// work items are in range and cover every (b, g, rb, s) once, that the
+// workspace holds the largest index any workgroup writes, and that the
+// dynamic LDS fits the 160 KB of a CDNA4 CU.  Prints "OK ..." or "FAIL ...".
+#include <cstdio>
+#include <vector>
+#include "tv_plan.h"
+
+int main() {
+  int B, N, Hq, Hkv, D, Lmax, V;
+  int bad = 0, cases = 0;
+  while (std::scanf("%d %d %d %d %d %d %d", &B, &N, &Hq, &Hkv, &D, &Lmax, &V) == 7) {
+    ++cases;
+    const tv::AttnPlan p = tv::attn_plan(B, N, Hq, Hkv, D, Lmax);
+    std::vector<int> seen((size_t)p.nwork, 0);
+    const int tiles = tv::cdiv(Lmax, tv::kKeyTile) + tv::cdiv(N, tv::kKeyTile);
+    bool ok = p.grid % tv::kXcds == 0 && p.nwork == B * Hkv * p.nRB * p.S && p.grid >= p.nwork;
+    ok = ok && (long long)p.S * p.chunk >= tiles && (long long)(p.S - 1) * p.chunk < tiles;
+    ok = ok && p.RB == (p.rows_mode ? tv::kRowsModeRB : tv::kKeysModeRB);
+    const int per = p.grid / tv::kXcds;
+    for (int bid = 0; bid < p.grid && ok; ++bid) {
+      int w = (bid % tv::kXcds) * per + bid / tv::kXcds;
+      if (w < 0 || w >= p.grid) ok = false;
+      if (w >= p.nwork) continue;
+      const int s = w % p.S, rb = (w / p.S) % p.nRB, g = (w / p.S / p.nRB) % Hkv;
+      const int b = w / p.S / p.nRB / Hkv;
+      if (b >= B || rb * p.RB >= p.M) ok = false;
+      seen[(size_t)w]++;
+      if (p.S > 1) {
+        const int DT = D / 16, NT = p.RB / 16;
+        const size_t fr = ((size_t)((b * Hkv + g) * p.nRB + rb) * p.S + s) * DT * NT;
+        const size_t last_o = (fr + (size_t)DT * NT - 1) * 64 + 63;
+        const size_t last_ml = ((size_t)((b * Hkv + g) * p.nRB + rb) * p.S + s) * p.RB + p.RB - 1;
+        if ((last_o + 1) * 16 > p.ws_o_bytes || (last_ml + 1) * 8 > p.ws_ml_bytes) ok = false;
+      }
+    }
+    for (int v : seen) ok = ok && v == 1;
+    if (p.lds_bytes > 160 * 1024) ok = false;
+    for (int esize : {2, 4})
+      for (int vec : {1, 16 / esize}) {
+        const tv::AcceptPlan ap = tv::accept_plan(B, N, V, esize, vec);
+        const long long nch = ((long long)V + vec - 1) / vec;
+        if (ap.ws_bytes > tv::accept_ws_bytes(B, N)) ok = false;
+        if (ap.grid != (long long)B * N * ap.nsplit) ok = false;
+        if ((long long)ap.nsplit * ap.chunks_per_split < nch) ok = false;
+        if ((long long)(ap.nsplit - 1) * ap.chunks_per_split >= nch) ok = false;
+        if (ap.nsplit < 1 || ap.nsplit > tv::kAcceptMaxSplit) ok = false;
+      }
+    std::printf("%s B=%d N=%d Hq=%d Hkv=%d D=%d L=%d V=%d S=%d RB=%d nRB=%d grid=%d lds=%zu ws=%zu\n",
+                ok ? "OK" : "FAIL", B, N, Hq, Hkv, D, Lmax, V, p.S, p.RB, p.nRB, p.grid,
+                p.lds_bytes, p.ws_bytes);
+    bad += !ok;
+  }
+  std::printf("%d cases, %d failed\n", cases, bad);
+  return bad ? 1 : 0;
+}

@@ -64,14 +64,15 @@ __device__ __forceinline__ float wave_max_across_groups(float v) {
   return v;
 }
 
-// 16 bytes per lane from global memory straight into LDS: lane i's bytes
-// land at lds_addr + 16 * i (lds_addr is wave-uniform).  Issued as inline assembly so the compiler does
-// not serialise every later LDS read behind it; completion is awaited with
-// explicit vmcnt waits.
-__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+// 16 bytes per lane from global memory straight into LDS: lane i reads
+// sbase + voff (sbase wave-uniform, voff a per-lane byte offset) and its
+// bytes land at lds_addr + 16 * i (lds_addr wave-uniform).  Issued as inline
+// assembly so the compiler does not serialise every later LDS read behind
+// it; completion is awaited with explicit vmcnt waits.
+__device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
                :
-               : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(gptr)
+               : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(sbase)
                : "memory");
 }
 
@@ -99,8 +100,11 @@ __device__ __forceinline__ void wait_vm_dyn(int n) {
 }
 
 // Layout of one 32-key tile in LDS: row-major, D bf16 per row, 16-byte
-// chunks XOR-swizzled by the row so 16 rows read at the same logical chunk
-// hit 16 different bank groups.
+// chunks XOR-swizzled by the row.  The swizzle is chosen so that
+//   * 16 rows read at the same logical chunk (the K operand reads, 16 lanes
+//     per pass) land in 16 different bank groups, and
+//   * the transposing V reads (rows 8k..8k+7, two adjacent chunks each, 32
+//     lanes per pass) cover every bank exactly once.
 template <int D>
 struct TileLayout {
   static constexpr int kRowBytes = 2 * D;
@@ -109,7 +113,8 @@ struct TileLayout {
   static constexpr int kDma = kBytes / 1024;       // 1 KB DMA instructions per tile
   static constexpr int kRowsPerDma = 64 / kCPR;
   __device__ static __forceinline__ int swz(int r) {
-    return D == 128 ? (r & 15) : ((r >> 1) & 7);
+    return D == 128 ? (((r & 7) << 1) | ((r >> 3) & 1))
+                    : ((((r >> 1) & 3) << 1) | ((r >> 3) & 1));
   }
   __device__ static __forceinline__ int off(int r, int chunk) {
     return r * kRowBytes + ((chunk ^ swz(r)) << 4);
@@ -117,51 +122,50 @@ struct TileLayout {
 };
 
 // Where a wave's K/V rows come from: the padded cache of one (sequence, KV
-// head) pair, then its tree K/V.
+// head) pair, then its tree K/V.  Pointers are byte pointers.
 struct TreeSrc {
-  const __bf16* kcache;
-  const __bf16* vcache;
-  const __bf16* ktree;
-  const __bf16* vtree;
-  int krow;   // elements between consecutive keys
-  int kvl;    // valid cache rows
-  int nct;    // cache tiles
-  int i_hi;   // last tree node the row block can see
+  const char* kcache;
+  const char* vcache;
+  const char* ktree;
+  const char* vtree;
+  int row_bytes;  // bytes between consecutive keys
+  int kvl;        // valid cache rows
+  int nct;        // cache tiles
+  int i_hi;       // last tree node the row block can see
 };
 
 // Issue this lane's DMA instructions for tile t into the stage at kdst (K
-// tile, then V tile).  Rows past the valid range are clamped onto a valid
-// row: the mask gives them zero weight, the clamp keeps reads in range.
-template <int D, bool ROWS, int PW>
-__device__ __forceinline__ void issue_tile(const TreeSrc& src, const int (&dma_off)[PW], int wave,
-                                           int lane, int t, uint32_t kdst) {
+// tile, then V tile).  The scalar base is the tile's first row; rows past
+// the valid range are clamped onto a valid row (the mask gives them zero
+// weight, the clamp keeps reads in range).  dma_off is the per-lane byte
+// offset of its chunk within a full tile.
+template <int D, int PW>
+__device__ __forceinline__ void issue_tile(const TreeSrc& src, const uint32_t (&dma_off)[PW],
+                                           int wr, int lane, int t, uint32_t kdst) {
   using TL = TileLayout<D>;
-  if (t < src.nct && (t + 1) * kKeyTile <= src.kvl) {
-    const size_t tofs = (size_t)t * kKeyTile * src.krow;
+  const bool cache = t < src.nct;
+  const int first = cache ? t * kKeyTile : (t - src.nct) * kKeyTile;
+  const size_t tofs = (size_t)first * src.row_bytes;
+  const char* kb = (cache ? src.kcache : src.ktree) + tofs;
+  const char* vb = (cache ? src.vcache : src.vtree) + tofs;
+  if (cache && (t + 1) * kKeyTile <= src.kvl) {
 #pragma unroll
     for (int k = 0; k < PW; ++k) {
-      const int q = ROWS ? wave * PW + k : k;
+      const int q = wr * PW + k;
       const bool isv = q >= TL::kDma;
-      dma16((isv ? src.vcache : src.kcache) + tofs + dma_off[k],
-            kdst + (isv ? TL::kBytes : 0) + (q % TL::kDma) * 1024);
+      dma16(isv ? vb : kb, dma_off[k], kdst + (isv ? TL::kBytes : 0) + (q % TL::kDma) * 1024);
     }
     return;
   }
+  const int last = cache ? src.kvl - 1 : src.i_hi;  // >= first for every existing tile
 #pragma unroll
   for (int k = 0; k < PW; ++k) {
-    const int q = ROWS ? wave * PW + k : k;
+    const int q = wr * PW + k;
     const bool isv = q >= TL::kDma;
     const int r = (q % TL::kDma) * TL::kRowsPerDma + lane / TL::kCPR;
-    const int col = ((lane % TL::kCPR) ^ TL::swz(r)) * 8;
-    const __bf16* p;
-    if (t < src.nct) {
-      const int key = min(t * kKeyTile + r, src.kvl - 1);
-      p = (isv ? src.vcache : src.kcache) + (size_t)key * src.krow;
-    } else {
-      const int u = min((t - src.nct) * kKeyTile + r, src.i_hi);
-      p = (isv ? src.vtree : src.ktree) + (size_t)u * src.krow;
-    }
-    dma16(p + col, kdst + (isv ? TL::kBytes : 0) + (q % TL::kDma) * 1024);
+    const int row = min(first + r, last) - first;
+    const uint32_t off = (uint32_t)(row * src.row_bytes + ((lane % TL::kCPR) ^ TL::swz(r)) * 16);
+    dma16(isv ? vb : kb, off, kdst + (isv ? TL::kBytes : 0) + (q % TL::kDma) * 1024);
   }
 }
 
@@ -203,17 +207,25 @@ __device__ __forceinline__ void softmax_pv(const f32x4 (&sc)[2][NT], const float
   }
 }
 
-template <int D, bool ROWS>
-__global__ __launch_bounds__(256, 1) void attn_main(AttnArgs a) {
+// One workgroup = 8 wave64s (two per SIMD) arranged as WR row groups x WK
+// key groups (WR * WK = 8).  A wave owns 32 rows of its row group; the WR
+// waves of a key group share one LDS ring and walk that group's tiles (every
+// WK-th tile of the chunk) in lock step; WK > 1 groups merge their partial
+// softmax states in LDS at the end.
+template <int D, int WR>
+__global__ __launch_bounds__(kThreads, 1) void attn_main(AttnArgs a) {
   using TL = TileLayout<D>;
-  constexpr int RB = ROWS ? kRowsModeRB : kKeysModeRB;  // rows per workgroup
-  constexpr int NT = 4;                // 16-row tiles per wave (64 rows)
-  constexpr int NTG = RB / 16;         // 16-row tiles per workgroup
-  constexpr int NC = D / 32;           // 32-wide head-dim chunks (QK^T)
-  constexpr int DT = D / 16;           // 16-wide head-dim tiles (PV)
-  constexpr int STAGE = 2 * TL::kBytes;                 // K tile + V tile
-  constexpr int NS = ring_stages(D, ROWS);              // ring depth
-  constexpr int PW = ROWS ? 2 * TL::kDma / kWaves : 2 * TL::kDma;  // DMAs per wave per tile
+  constexpr int WK = kWavesPerWG / WR;  // key groups
+  constexpr int RB = kRowsPerWave * WR; // rows per workgroup
+  constexpr int NT = kRowsPerWave / 16; // 16-row tiles per wave
+  constexpr int NTG = RB / 16;          // 16-row tiles per workgroup
+  constexpr int NC = D / 32;            // 32-wide head-dim chunks (QK^T)
+  constexpr int DT = D / 16;            // 16-wide head-dim tiles (PV)
+  constexpr int STAGE = 2 * TL::kBytes; // K tile + V tile
+  constexpr int NS = ring_stages(D, WK);
+  constexpr int PW = 2 * TL::kDma / WR; // DMAs per wave per tile
+  static_assert(PW >= 1 && PW * WR == 2 * TL::kDma, "DMA split");
+  static_assert(NS >= 1, "ring does not fit");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
   const int per = gridDim.x / kXcds;
@@ -226,7 +238,9 @@ __global__ __launch_bounds__(256, 1) void attn_main(AttnArgs a) {
   const int g = w % a.Hkv;
   const int b = w / a.Hkv;
   if (b >= a.B) return;  // never taken for a consistent plan
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr = wave % WR, wk = wave / WR;
   const int g4 = lane >> 4, l16 = lane & 15;
 
   int kvl = a.kv_len ? a.kv_len[b] : a.Lmax;
@@ -241,10 +255,9 @@ __global__ __launch_bounds__(256, 1) void attn_main(AttnArgs a) {
   const int t1 = min(T, t0 + a.chunk);
   const bool has_tree = t0 < t1 && t1 > nct;
 
-  constexpr int RING = ROWS ? NS * STAGE : kWaves * NS * STAGE;
-  const uint32_t smem_base = (uint32_t)(uintptr_t)smem;
-  const uint32_t ring = smem_base + (ROWS ? 0 : wave * NS * STAGE);
-  const unsigned char* ring_ptr = smem + (ROWS ? 0 : wave * NS * STAGE);
+  constexpr int RING = WK * NS * STAGE;
+  const uint32_t ring = (uint32_t)(uintptr_t)smem + wk * NS * STAGE;
+  const unsigned char* ring_ptr = smem + wk * NS * STAGE;
   uint32_t* anc = reinterpret_cast<uint32_t*>(smem + RING);
   const int anc_nodes = RB / a.G + 2;
   int32_t* par = reinterpret_cast<int32_t*>(anc + anc_nodes * ntt);
@@ -259,28 +272,28 @@ __global__ __launch_bounds__(256, 1) void attn_main(AttnArgs a) {
   // This lane's share of the DMA instructions of one tile: instruction q
   // (q < kDma: K, else V) covers tile rows j*kRowsPerDma.. (j = q % kDma);
   // lane i fetches row j*kRowsPerDma + i/kCPR at the logical chunk that the
-  // swizzle places at physical chunk i % kCPR.  dma_off is that element
-  // offset for a full cache tile starting at key 0.
-  int dma_off[PW];
+  // swizzle places at physical chunk i % kCPR.  dma_off is that byte offset
+  // from the first row of a full tile.
+  uint32_t dma_off[PW];
 #pragma unroll
   for (int k = 0; k < PW; ++k) {
-    const int q = ROWS ? wave * PW + k : k;
+    const int q = wr * PW + k;
     const int r = (q % TL::kDma) * TL::kRowsPerDma + lane / TL::kCPR;
-    dma_off[k] = r * (int)krow + ((lane % TL::kCPR) ^ TL::swz(r)) * 8;
+    dma_off[k] = (uint32_t)(r * (int)krow * 2 + ((lane % TL::kCPR) ^ TL::swz(r)) * 16);
   }
-  const TreeSrc src{kcache, vcache, ktree, vtree, (int)krow, kvl, nct, i_hi};
+  const TreeSrc src{(const char*)kcache, (const char*)vcache, (const char*)ktree,
+                    (const char*)vtree, (int)krow * 2, kvl, nct, i_hi};
 
-  // this wave's tiles: rows mode walks t0..t1-1 in step with the other
-  // waves, keys mode takes every 4th tile
-  const int my_first = ROWS ? t0 : t0 + wave;
-  const int my_step = ROWS ? 1 : kWaves;
-  const int n_my = my_first < t1 ? (t1 - my_first + my_step - 1) / my_step : 0;
+  // iteration i handles tile t0 + wk + WK*i of this wave's key group; all
+  // waves run n_iter iterations so the per-iteration barriers line up
+  const int n_iter = t1 > t0 ? (t1 - t0 + WK - 1) / WK : 0;
+  const int n_mine = t0 + wk < t1 ? (t1 - t0 - wk + WK - 1) / WK : 0;  // valid tiles
 #pragma unroll
   for (int i = 0; i < NS - 1; ++i)
-    if (i < n_my) issue_tile<D, ROWS, PW>(src, dma_off, wave, lane, my_first + i * my_step, ring + i * STAGE);
+    if (i < n_mine) issue_tile<D, PW>(src, dma_off, wr, lane, t0 + wk + WK * i, ring + i * STAGE);
 
   // ---- queries: B operand of S^T = K Q^T, lane holds Q[row l16][8*g4 .. +8]
-  const int wrow0 = r0 + (ROWS ? 64 * wave : 0);
+  const int wrow0 = r0 + kRowsPerWave * wr;
   bf16x8 qf[NT][NC];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
@@ -300,14 +313,14 @@ __global__ __launch_bounds__(256, 1) void attn_main(AttnArgs a) {
   // ---- tree structure: ancestor-or-self bitmask of this block's nodes
   if (has_tree) {
     int bad = 0;
-    for (int i = tid; i < a.N; i += 256) {
+    for (int i = tid; i < a.N; i += kThreads) {
       const int p = a.parent[(size_t)b * a.N + i];
       par[i] = p;
       bad |= (i == 0) ? (p != -1) : (p < 0 || p >= i);
     }
     bad = __syncthreads_or(bad);
     const int nodes = i_hi - i_lo + 1;
-    for (int t = tid; t < nodes; t += 256) {
+    for (int t = tid; t < nodes; t += kThreads) {
       uint32_t* wd = anc + t * ntt;
       for (int k = 0; k < ntt; ++k) wd[k] = 0u;
       int u = i_lo + t;
@@ -346,52 +359,54 @@ __global__ __launch_bounds__(256, 1) void attn_main(AttnArgs a) {
   }
 
   // The tile loop runs without touching O on the vector ALUs, so the O
-  // accumulators stay in accumulation registers; a tile whose maximum moves
-  // a row's reference leaves the inner loop, O and l are rescaled, and the
-  // tile is finished outside.
+  // accumulators never move between register files; a tile whose scores
+  // move a row's reference leaves the inner loop, O and l are rescaled, and
+  // the tile is finished outside.
   constexpr float kSlack = 8.f;
   f32x4 sc[2][NT];
   float mx[NT];
   const unsigned char* vt_lds = ring_ptr + TL::kBytes;
   int i = 0;
-  while (i < n_my) {
+  while (i < n_iter) {
     bool pending = false;
-    for (; i < n_my; ++i) {
-      const int t = my_first + i * my_step;
-      if (ROWS) {
+    for (; i < n_iter; ++i) {
+      const bool mine = i < n_mine;
+      if (WR > 1) {
         // my DMAs of tile i are done once at most min(later tiles, NS-2)
-        // tiles' DMAs are outstanding; the barrier makes everyone's visible
-        // and guarantees every wave has finished reading tile i-1's slot
-        const int later = min(n_my - 1 - i, NS - 2);
-        wait_vm_dyn(later * PW);
+        // tiles' DMAs are outstanding; the barrier makes the whole group's
+        // visible and guarantees the slot of tile i-1 is no longer read
+        if (mine) wait_vm_dyn(min(n_mine - 1 - i, NS - 2) * PW);
         __syncthreads();
-        if (i + NS - 1 < n_my)
-          issue_tile<D, ROWS, PW>(src, dma_off, wave, lane, my_first + (i + NS - 1) * my_step,
-                                  ring + ((i + NS - 1) % NS) * STAGE);
+        if (i + NS - 1 < n_mine)
+          issue_tile<D, PW>(src, dma_off, wr, lane, t0 + wk + WK * (i + NS - 1),
+                            ring + ((i + NS - 1) % NS) * STAGE);
       } else {
-        if (i + NS - 1 < n_my)
-          issue_tile<D, ROWS, PW>(src, dma_off, wave, lane, my_first + (i + NS - 1) * my_step,
-                                  ring + ((i + NS - 1) % NS) * STAGE);
-        const int later = min(n_my - 1 - i, NS - 1);
-        wait_vm_dyn(later * PW);
+        if (i + NS - 1 < n_mine)
+          issue_tile<D, PW>(src, dma_off, wr, lane, t0 + wk + WK * (i + NS - 1),
+                            ring + ((i + NS - 1) % NS) * STAGE);
+        if (mine) wait_vm_dyn(min(n_mine - 1 - i, NS - 1) * PW);
       }
+      if (!mine) continue;
+      const int t = t0 + wk + WK * i;
       const unsigned char* kt_lds = ring_ptr + (i % NS) * STAGE;
       vt_lds = kt_lds + TL::kBytes;
 
       // S^T tile: lane holds S^T[key 16*tt + 4*g4 + j][row 16*nt + l16]
+      bf16x8 kf[2][NC];
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) sc[tt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int c = 0; c < NC; ++c)
+          kf[tt][c] = *reinterpret_cast<const bf16x8*>(kt_lds + TL::off(16 * tt + l16, 4 * c + g4));
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
+      for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-        for (int c = 0; c < NC; ++c) {
-          const bf16x8 kf =
-              *reinterpret_cast<const bf16x8*>(kt_lds + TL::off(16 * tt + l16, 4 * c + g4));
+        for (int tt = 0; tt < 2; ++tt) {
+          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int nt = 0; nt < NT; ++nt)
-            sc[tt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[nt][c], sc[tt][nt], 0, 0, 0);
+          for (int c = 0; c < NC; ++c)
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[tt][c], qf[nt][c], acc, 0, 0, 0);
+          sc[tt][nt] = acc;
         }
 
       // masks: the cache tail and the tree tiles
@@ -421,9 +436,10 @@ __global__ __launch_bounds__(256, 1) void attn_main(AttnArgs a) {
       }
 
       // Online softmax in base 2 with a lazily moved reference: a row's
-      // reference m (log2 units) only moves when its tile maximum exceeds it
-      // by more than kSlack, so rescaling is rare; weights stay below
-      // 2^kSlack, far inside the fp32 and bf16 ranges.
+      // reference m (log2 units) only moves when one of its scores exceeds
+      // it by more than kSlack, so weights stay below 2^kSlack (far inside
+      // the fp32 and bf16 ranges) and rescaling is rare.  Each lane checks
+      // its own scores; only a moving tile pays for exact row maxima.
       bool move = false;
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
@@ -431,7 +447,7 @@ __global__ __launch_bounds__(256, 1) void attn_main(AttnArgs a) {
         v = fmaxf(fmaxf(v, sc[0][nt][3]), sc[1][nt][0]);
         v = fmaxf(fmaxf(v, sc[1][nt][1]), sc[1][nt][2]);
         v = fmaxf(v, sc[1][nt][3]);
-        mx[nt] = wave_max_across_groups(v) * a.c;
+        mx[nt] = v * a.c;
         move |= mx[nt] > m[nt] + kSlack;
       }
       if (__any(move)) {
@@ -443,6 +459,7 @@ __global__ __launch_bounds__(256, 1) void attn_main(AttnArgs a) {
     if (!pending) break;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
+      mx[nt] = wave_max_across_groups(mx[nt]);  // exact row maxima of the tile
       const bool moved = mx[nt] > m[nt] + kSlack;
       // a row that has not moved keeps its scale (its m may still be -inf)
       const float alpha = moved ? __builtin_amdgcn_exp2f(m[nt] - mx[nt]) : 1.f;
@@ -483,45 +500,46 @@ __global__ __launch_bounds__(256, 1) void attn_main(AttnArgs a) {
     }
   };
 
-  if (ROWS) {
+  if (WK == 1) {
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) emit(dt, wave * NT + nt, o[dt][nt], m[nt], lsum[nt]);
+      for (int nt = 0; nt < NT; ++nt) emit(dt, wr * NT + nt, o[dt][nt], m[nt], lsum[nt]);
     return;
   }
 
-  // ---- keys mode: merge the 4 waves (disjoint key subsets, same rows)
+  // ---- merge the WK key groups of each row group (same rows, disjoint keys)
   __syncthreads();  // rings and tree tables are dead from here on
   f32x4* obuf = reinterpret_cast<f32x4*>(smem);
-  float2* mlbuf = reinterpret_cast<float2*>(smem + (size_t)kWaves * RB * D * 4);
+  float2* mlbuf = reinterpret_cast<float2*>(smem + (size_t)kWavesPerWG * kRowsPerWave * D * 4);
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) obuf[((wave * DT + dt) * NT + nt) * 64 + lane] = o[dt][nt];
   if (g4 == 0) {
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) mlbuf[wave * RB + nt * 16 + l16] = make_float2(m[nt], lsum[nt]);
+    for (int nt = 0; nt < NT; ++nt)
+      mlbuf[wave * kRowsPerWave + nt * 16 + l16] = make_float2(m[nt], lsum[nt]);
   }
   __syncthreads();
-  for (int f = wave; f < DT * NT; f += kWaves) {
+  for (int f = wk; f < DT * NT; f += WK) {
     const int dt = f / NT, nt = f % NT;
-    const int row = nt * 16 + l16;
-    float mw[kWaves], mstar = -INFINITY;
+    const int rw = nt * 16 + l16;  // row within the wave's 32
+    float mw[WK], mstar = -INFINITY;
 #pragma unroll
-    for (int k = 0; k < kWaves; ++k) {
-      mw[k] = mlbuf[k * RB + row].x;
+    for (int k = 0; k < WK; ++k) {
+      mw[k] = mlbuf[(k * WR + wr) * kRowsPerWave + rw].x;
       mstar = fmaxf(mstar, mw[k]);
     }
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     float l = 0.f;
 #pragma unroll
-    for (int k = 0; k < kWaves; ++k) {
+    for (int k = 0; k < WK; ++k) {
       const float e = mw[k] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw[k] - mstar);
-      l += e * mlbuf[k * RB + row].y;
-      acc += e * obuf[((k * DT + dt) * NT + nt) * 64 + lane];
+      l += e * mlbuf[(k * WR + wr) * kRowsPerWave + rw].y;
+      acc += e * obuf[(((k * WR + wr) * DT + dt) * NT + nt) * 64 + lane];
     }
-    emit(dt, nt, acc, mstar, l);
+    emit(dt, wr * NT + nt, acc, mstar, l);
   }
 }
 
@@ -566,19 +584,32 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
                              4 * g4) = ov;
 }
 
-template <int D, bool ROWS>
+template <int D, int WR>
 static hipError_t launch_attn_t(const AttnArgs& a, const AttnPlan& p, hipStream_t st) {
-  constexpr int RB = ROWS ? kRowsModeRB : kKeysModeRB;
-  hipError_t e = hipFuncSetAttribute((const void*)attn_main<D, ROWS>,
+  constexpr int RB = kRowsPerWave * WR;
+  hipError_t e = hipFuncSetAttribute((const void*)attn_main<D, WR>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)p.lds_bytes);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attn_main<D, ROWS>), dim3(p.grid), dim3(256), p.lds_bytes, st, a);
+  hipLaunchKernelGGL((attn_main<D, WR>), dim3(p.grid), dim3(kThreads), p.lds_bytes, st, a);
   e = hipGetLastError();
   if (e != hipSuccess || p.S == 1) return e;
   const int frags = a.B * a.Hkv * p.nRB * (D / 16) * (RB / 16);
   hipLaunchKernelGGL((attn_combine<D, RB>), dim3(frags / 4), dim3(256), 0, st, a);
   return hipGetLastError();
+}
+
+template <int D>
+static hipError_t launch_attn_d(const AttnArgs& a, const AttnPlan& p, hipStream_t st) {
+  // arrangements whose ring does not fit in LDS are never planned
+  if constexpr (ring_stages(D, kWavesPerWG / 1) > 0)
+    if (p.WR == 1) return launch_attn_t<D, 1>(a, p, st);
+  switch (p.WR) {
+    case 2: return launch_attn_t<D, 2>(a, p, st);
+    case 4: return launch_attn_t<D, 4>(a, p, st);
+    case 8: return launch_attn_t<D, 8>(a, p, st);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_attention(const void* q, const void* kc, const void* vc, const void* kt,
@@ -608,9 +639,7 @@ hipError_t launch_attention(const void* q, const void* kc, const void* vc, const
   a.chunk = p.chunk;
   a.nwork = p.nwork;
   a.c = scale * 1.4426950408889634f;
-  if (D == 128)
-    return p.rows_mode ? launch_attn_t<128, true>(a, p, st) : launch_attn_t<128, false>(a, p, st);
-  return p.rows_mode ? launch_attn_t<64, true>(a, p, st) : launch_attn_t<64, false>(a, p, st);
+  return D == 128 ? launch_attn_d<128>(a, p, st) : launch_attn_d<64>(a, p, st);
 }
 
 }  // namespace tv

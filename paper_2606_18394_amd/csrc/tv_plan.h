@@ -6,7 +6,6 @@
 
 namespace tv {
 
-constexpr int kWaves = 4;          // waves per attention workgroup
 constexpr int kKeyTile = 32;       // keys one wave consumes per step
 constexpr int kXcds = 8;           // MI355X accelerator complex dies
 constexpr int kMaxNodes = 2048;    // == TV_MAX_NODES
@@ -15,48 +14,56 @@ inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 
 // Attention work decomposition.  Rows of one (sequence, KV head) pair are the
 // N*G (node, query-head-in-group) pairs, row r = node * G + head_in_group.
-// A workgroup takes one block of consecutive rows (64 in keys mode, 256 in
-// rows mode) and one fixed-size chunk of the key tiles (cache tiles first,
-// then tree tiles).
-constexpr int kKeysModeRB = 64;
-constexpr int kRowsModeRB = 256;
+// A workgroup of 8 waves (two per SIMD) takes a block of RB = 32*WR
+// consecutive rows and one fixed-size chunk of the key tiles (cache tiles
+// first, then tree tiles): WR row groups of one 32-row wave each, times
+// WK = 8/WR key groups that split the chunk's tiles between them.
+constexpr int kThreads = 512;
+constexpr int kWavesPerWG = 8;
+constexpr int kRowsPerWave = 32;
 
-// LDS ring depth (stages of one 32-key K tile + V tile)
-constexpr int ring_stages(int D, bool rows_mode) {
-  return rows_mode ? 4 : (D == 128 ? 2 : 4);
+// LDS ring depth per key group (stages of one 32-key K tile + V tile);
+// 0 marks an arrangement that does not fit.
+constexpr int ring_stages(int D, int WK) {
+  return D == 128 ? (WK <= 2 ? 4 : (WK == 4 ? 2 : 0)) : (WK <= 4 ? 4 : 2);
 }
 
 struct AttnPlan {
-  bool rows_mode;
+  int WR;                      // row groups (waves per key group)
   int G, M, RB, nRB, S, chunk;
   int nwork, grid;             // work items, launched workgroups (x8 padded)
   size_t ws_o_bytes, ws_ml_bytes, ws_bytes;
   size_t lds_bytes;            // dynamic LDS of the main kernel
 };
 
-inline size_t attn_lds_bytes(int D, bool rows_mode, int G, int N) {
-  const int RB = rows_mode ? kRowsModeRB : kKeysModeRB;
+inline size_t attn_lds_bytes(int D, int WR, int G, int N) {
+  const int WK = kWavesPerWG / WR, RB = kRowsPerWave * WR;
   const size_t stage = 2 * (size_t)kKeyTile * 2 * D;
-  const size_t ring = (rows_mode ? 1 : kWaves) * (size_t)ring_stages(D, rows_mode) * stage;
+  const size_t ring = (size_t)WK * ring_stages(D, WK) * stage;
   const int words = cdiv(N, 32);
   const int nodes = RB / G + 2;
   const size_t tree = (size_t)nodes * words * 4 + (size_t)N * 4 + 16;
-  const size_t merge = rows_mode ? 0 : (size_t)kWaves * RB * D * 4 + (size_t)kWaves * RB * 8;
+  const size_t merge =
+      WK == 1 ? 0 : (size_t)kWavesPerWG * kRowsPerWave * D * 4 + (size_t)kWavesPerWG * kRowsPerWave * 8;
   const size_t a = ring + tree;
   return a > merge ? a : merge;
 }
 
-inline AttnPlan attn_plan(int B, int N, int Hq, int Hkv, int D, int Lmax) {
+constexpr size_t kMaxLds = 160 * 1024;
+
+// The plan for one arrangement WR: split count and sizes.
+inline AttnPlan attn_plan_wr(int B, int N, int Hq, int Hkv, int D, int Lmax, int WR) {
   AttnPlan p{};
+  p.WR = WR;
   p.G = Hq / Hkv;
   p.M = N * p.G;
-  p.rows_mode = p.M >= 2 * kRowsModeRB;
-  p.RB = p.rows_mode ? kRowsModeRB : kKeysModeRB;
+  p.RB = kRowsPerWave * WR;
   p.nRB = cdiv(p.M, p.RB);
+  const int WK = kWavesPerWG / WR;
   const int tiles = cdiv(Lmax, kKeyTile) + cdiv(N, kKeyTile);
   const long long base = (long long)B * Hkv * p.nRB;
   const long long target = 256;                 // one workgroup per CU
-  const int min_chunk = p.rows_mode ? 4 : 2 * kWaves;
+  const int min_chunk = 2 * WK;                 // >= 2 tiles per key group
   long long S = (target + base - 1) / base;
   const long long max_s = tiles / min_chunk > 1 ? tiles / min_chunk : 1;
   if (S > max_s) S = max_s;
@@ -71,8 +78,41 @@ inline AttnPlan attn_plan(int B, int N, int Hq, int Hkv, int D, int Lmax) {
     p.ws_ml_bytes = (size_t)B * Hkv * p.nRB * p.S * p.RB * 8;
   }
   p.ws_bytes = p.ws_o_bytes + p.ws_ml_bytes;
-  p.lds_bytes = attn_lds_bytes(D, p.rows_mode, p.G, N);
+  p.lds_bytes = attn_lds_bytes(D, WR, p.G, N);
   return p;
+}
+
+// Rough time (arbitrary units) of an arrangement: matrix work on padded
+// rows, K/V traffic from L2 (each row block re-reads the keys), and the
+// split partials written and read back.
+inline double attn_plan_cost(const AttnPlan& p, int B, int Hkv, int D, int Lmax, int N) {
+  const double keys = (double)Lmax + N;
+  const double mfma = (double)B * Hkv * p.nRB * p.RB * keys * 4.0 * D / 2.0e15;
+  const double kv = (double)B * Hkv * keys * D * 4.0;
+  const double l2 = kv * p.nRB / 20.0e12;
+  const double hbm = kv / 6.0e12;
+  const double partial = (double)p.ws_bytes * 2.0 / 5.0e12;
+  double t = mfma > l2 ? mfma : l2;
+  t = t > hbm ? t : hbm;
+  return t + partial;
+}
+
+inline AttnPlan attn_plan(int B, int N, int Hq, int Hkv, int D, int Lmax) {
+  AttnPlan best{};
+  double best_cost = 0;
+  const int candidates[4] = {1, 2, 4, 8};
+  for (int WR : candidates) {
+    const int WK = kWavesPerWG / WR;
+    if (ring_stages(D, WK) == 0) continue;
+    const AttnPlan p = attn_plan_wr(B, N, Hq, Hkv, D, Lmax, WR);
+    if (p.lds_bytes > kMaxLds) continue;
+    const double c = attn_plan_cost(p, B, Hkv, D, Lmax, N);
+    if (best.WR == 0 || c < best_cost) {
+      best = p;
+      best_cost = c;
+    }
+  }
+  return best;
 }
 
 // Acceptance decomposition: a scan kernel runs one workgroup per (node row,

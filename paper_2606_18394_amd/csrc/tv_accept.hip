@@ -5,7 +5,7 @@
 // prediction at its parent and the parent is accepted; the result is the
 // deepest accepted root-to-node path (Sec. 2.4 greedy rule; App. E).
 //
-// Two kernels, no atomics:
+// Two kernels, no global atomics:
 //   scan    one workgroup per (node row, vocabulary split).  256 threads
 //           stream their slice with 16-byte loads, kScanLoadsPerThread of
 //           them in flight per thread, and keep a running first maximum;
@@ -147,6 +147,7 @@ __global__ __launch_bounds__(kScanThreads) void accept_scan(AcceptArgs a) {
 __global__ __launch_bounds__(256) void accept_finish(AcceptArgs a) {
   __shared__ short par[kMaxNodes];
   __shared__ int tgt[kMaxNodes];
+  __shared__ unsigned long long rowkey[kMaxNodes];
   __shared__ unsigned char ok[2][kMaxNodes];
   __shared__ short jmp[2][kMaxNodes];
   __shared__ short dep[2][kMaxNodes];
@@ -154,15 +155,30 @@ __global__ __launch_bounds__(256) void accept_finish(AcceptArgs a) {
   const int tid = threadIdx.x;
   const int b = blockIdx.x;
   const int N = a.N;
+  // the split keys of all rows: independent loads, merged with LDS max
+  for (int i = tid; i < N; i += 256) rowkey[i] = 0ull;
+  __syncthreads();
+  const size_t kbase = (size_t)b * N * a.nsplit;
+  for (int idx = tid; idx < N * a.nsplit; idx += 256)
+    atomicMax(&rowkey[idx / a.nsplit], a.part[kbase + idx]);
   int bad = 0;
-  for (int i = tid; i < N; i += 256) {
-    const size_t r = (size_t)b * N + i;
-    unsigned long long k = 0ull;
-    for (int s = 0; s < a.nsplit; ++s) k = umax64(k, a.part[r * a.nsplit + s]);
-    const int t = (int)(0xFFFFFFFFu - (unsigned int)k);
+  int pv[kMaxNodes / 256], dv[kMaxNodes / 256];
+#pragma unroll
+  for (int k = 0; k < kMaxNodes / 256; ++k) {
+    const int i = tid + 256 * k;
+    pv[k] = i < N ? a.parent[(size_t)b * N + i] : 0;
+    dv[k] = i < N ? a.draft[(size_t)b * N + i] : 0;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < kMaxNodes / 256; ++k) {
+    const int i = tid + 256 * k;
+    if (i >= N) break;
+    const unsigned long long key = rowkey[i];
+    const int t = (int)(0xFFFFFFFFu - (unsigned int)key);
     tgt[i] = t;
-    if (a.tgt_out) a.tgt_out[r] = t;
-    const int p = a.parent[r];
+    if (a.tgt_out) a.tgt_out[(size_t)b * N + i] = t;
+    const int p = pv[k];
     const int badi = (i == 0) ? (p != -1) : (p < 0 || p >= i);
     bad |= badi;
     par[i] = (short)(badi ? 0 : p);
@@ -170,13 +186,16 @@ __global__ __launch_bounds__(256) void accept_finish(AcceptArgs a) {
   if (tid == 0) best_key = 0u;
   bad = __syncthreads_or(bad);
   if (!bad) {
-    for (int i = tid; i < N; i += 256) {
+#pragma unroll
+    for (int k = 0; k < kMaxNodes / 256; ++k) {
+      const int i = tid + 256 * k;
+      if (i >= N) break;
       if (i == 0) {
         ok[0][0] = 1;
         jmp[0][0] = 0;
         dep[0][0] = 0;
       } else {
-        ok[0][i] = a.draft[(size_t)b * N + i] == tgt[par[i]];
+        ok[0][i] = dv[k] == tgt[par[i]];
         jmp[0][i] = par[i];
         dep[0][i] = 1;
       }

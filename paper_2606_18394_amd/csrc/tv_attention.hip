@@ -169,6 +169,37 @@ __device__ __forceinline__ void issue_tile(const TreeSrc& src, const uint32_t (&
   }
 }
 
+// Sets the scores of keys a row cannot see to -inf: cache keys at or past
+// kv_len, and tree keys outside the row's ancestor-or-self set (one 32-bit
+// word of its bitmask per tile).
+template <int NT>
+__device__ __forceinline__ void mask_tile(f32x4 (&sc)[2][NT], int t, int nct, int kvl,
+                                          const uint32_t* anc, const int (&node_rel)[NT], int ntt,
+                                          int g4) {
+  if (t < nct) {
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bool vis = t * kKeyTile + 16 * tt + 4 * g4 + j < kvl;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+          if (!vis) sc[tt][nt][j] = -INFINITY;
+      }
+  } else {
+    const int word = t - nct;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const uint32_t bits = anc[node_rel[nt] * ntt + word];
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (!((bits >> (16 * tt + 4 * g4 + j)) & 1u)) sc[tt][nt][j] = -INFINITY;
+    }
+  }
+}
+
 // Softmax weights of one 32-key tile (base 2, reference m per row) as the
 // bf16 P^T operand, their row sums (ones^T P^T) into lacc, and O^T += V^T
 // P^T with V^T from transposing LDS reads: lane (g4, l16) receives
@@ -207,22 +238,22 @@ __device__ __forceinline__ void softmax_pv(const f32x4 (&sc)[2][NT], const float
   }
 }
 
-// One workgroup = 8 wave64s (two per SIMD) arranged as WR row groups x WK
-// key groups (WR * WK = 8).  A wave owns 32 rows of its row group; the WR
+// A workgroup of WR x WK wave64s: WR row groups x WK key groups.  A wave owns 32 rows of its row group; the WR
 // waves of a key group share one LDS ring and walk that group's tiles (every
 // WK-th tile of the chunk) in lock step; WK > 1 groups merge their partial
 // softmax states in LDS at the end.
-template <int D, int WR>
-__global__ __launch_bounds__(kThreads, 1) void attn_main(AttnArgs a) {
+template <int D, int WR, int WK, int NS>
+__global__ __launch_bounds__(64 * WR * WK) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attn_main(AttnArgs a) {
   using TL = TileLayout<D>;
-  constexpr int WK = kWavesPerWG / WR;  // key groups
+  constexpr int kThreads = 64 * WR * WK;
+  constexpr int kWaves = WR * WK;
   constexpr int RB = kRowsPerWave * WR; // rows per workgroup
   constexpr int NT = kRowsPerWave / 16; // 16-row tiles per wave
   constexpr int NTG = RB / 16;          // 16-row tiles per workgroup
   constexpr int NC = D / 32;            // 32-wide head-dim chunks (QK^T)
   constexpr int DT = D / 16;            // 16-wide head-dim tiles (PV)
   constexpr int STAGE = 2 * TL::kBytes; // K tile + V tile
-  constexpr int NS = ring_stages(D, WK);
   constexpr int PW = 2 * TL::kDma / WR; // DMAs per wave per tile
   static_assert(PW >= 1 && PW * WR == 2 * TL::kDma, "DMA split");
   static_assert(NS >= 1, "ring does not fit");
@@ -253,7 +284,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_main(AttnArgs a) {
   const int T = nct + ntt;
   const int t0 = s * a.chunk;
   const int t1 = min(T, t0 + a.chunk);
-  const bool has_tree = t0 < t1 && t1 > nct;
+  if (t0 >= t1) return;  // empty chunk: the merge reads only chunks with tiles
+  const bool has_tree = t1 > nct;
 
   constexpr int RING = WK * NS * STAGE;
   const uint32_t ring = (uint32_t)(uintptr_t)smem + wk * NS * STAGE;
@@ -358,18 +390,14 @@ __global__ __launch_bounds__(kThreads, 1) void attn_main(AttnArgs a) {
     node_rel[nt] = (r < a.M ? r : a.M - 1) / a.G - i_lo;
   }
 
-  // The tile loop runs without touching O on the vector ALUs, so the O
-  // accumulators never move between register files; a tile whose scores
-  // move a row's reference leaves the inner loop, O and l are rescaled, and
-  // the tile is finished outside.
   constexpr float kSlack = 8.f;
   f32x4 sc[2][NT];
-  float mx[NT];
+  float mx[NT], thr[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) thr[nt] = -INFINITY;  // m = -inf: any visible score moves
   const unsigned char* vt_lds = ring_ptr + TL::kBytes;
-  int i = 0;
-  while (i < n_iter) {
-    bool pending = false;
-    for (; i < n_iter; ++i) {
+  for (int i = 0; i < n_iter; ++i) {
+    {
       const bool mine = i < n_mine;
       if (WR > 1) {
         // my DMAs of tile i are done once at most min(later tiles, NS-2)
@@ -409,37 +437,16 @@ __global__ __launch_bounds__(kThreads, 1) void attn_main(AttnArgs a) {
           sc[tt][nt] = acc;
         }
 
-      // masks: the cache tail and the tree tiles
-      if (t < nct) {
-        if ((t + 1) * kKeyTile > kvl) {
-#pragma unroll
-          for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const bool vis = t * kKeyTile + 16 * tt + 4 * g4 + j < kvl;
-#pragma unroll
-              for (int nt = 0; nt < NT; ++nt)
-                if (!vis) sc[tt][nt][j] = -INFINITY;
-            }
-        }
-      } else {
-        const int word = t - nct;
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const uint32_t bits = anc[node_rel[nt] * ntt + word];
-#pragma unroll
-          for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-              if (!((bits >> (16 * tt + 4 * g4 + j)) & 1u)) sc[tt][nt][j] = -INFINITY;
-        }
-      }
+      // masks: the cache tail and the tree tiles (full cache tiles skip this)
+      if (t >= nct || (t + 1) * kKeyTile > kvl)
+        mask_tile<NT>(sc, t, nct, kvl, anc, node_rel, ntt, g4);
 
       // Online softmax in base 2 with a lazily moved reference: a row's
       // reference m (log2 units) only moves when one of its scores exceeds
       // it by more than kSlack, so weights stay below 2^kSlack (far inside
-      // the fp32 and bf16 ranges) and rescaling is rare.  Each lane checks
-      // its own scores; only a moving tile pays for exact row maxima.
+      // the fp32 and bf16 ranges) and rescaling is rare.  Each lane compares
+      // its own raw scores with thr = (m + kSlack) / c; only a moving tile
+      // pays for exact row maxima.
       bool move = false;
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
@@ -447,29 +454,27 @@ __global__ __launch_bounds__(kThreads, 1) void attn_main(AttnArgs a) {
         v = fmaxf(fmaxf(v, sc[0][nt][3]), sc[1][nt][0]);
         v = fmaxf(fmaxf(v, sc[1][nt][1]), sc[1][nt][2]);
         v = fmaxf(v, sc[1][nt][3]);
-        mx[nt] = v * a.c;
-        move |= mx[nt] > m[nt] + kSlack;
+        mx[nt] = v;
+        move |= v > thr[nt];
       }
       if (__any(move)) {
-        pending = true;
-        break;
+        // rare: exact row maxima of the tile, move the references that
+        // need it and rescale their O and l (a row that has not moved keeps
+        // its scale; its m may still be -inf)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          mx[nt] = wave_max_across_groups(mx[nt]) * a.c;
+          const bool moved = mx[nt] > m[nt] + kSlack;
+          const float alpha = moved ? __builtin_amdgcn_exp2f(m[nt] - mx[nt]) : 1.f;
+          m[nt] = moved ? mx[nt] : m[nt];
+          thr[nt] = (m[nt] + kSlack) / a.c;
+          lacc[nt] *= alpha;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) o[dt][nt] *= alpha;
+        }
       }
       softmax_pv<D>(sc, m, a.c, vt_lds, ones, o, lacc, g4, l16);
     }
-    if (!pending) break;
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      mx[nt] = wave_max_across_groups(mx[nt]);  // exact row maxima of the tile
-      const bool moved = mx[nt] > m[nt] + kSlack;
-      // a row that has not moved keeps its scale (its m may still be -inf)
-      const float alpha = moved ? __builtin_amdgcn_exp2f(m[nt] - mx[nt]) : 1.f;
-      m[nt] = moved ? mx[nt] : m[nt];
-      lacc[nt] *= alpha;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) o[dt][nt] *= alpha;
-    }
-    softmax_pv<D>(sc, m, a.c, vt_lds, ones, o, lacc, g4, l16);
-    ++i;
   }
 
   float lsum[NT];
@@ -511,7 +516,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_main(AttnArgs a) {
   // ---- merge the WK key groups of each row group (same rows, disjoint keys)
   __syncthreads();  // rings and tree tables are dead from here on
   f32x4* obuf = reinterpret_cast<f32x4*>(smem);
-  float2* mlbuf = reinterpret_cast<float2*>(smem + (size_t)kWavesPerWG * kRowsPerWave * D * 4);
+  float2* mlbuf = reinterpret_cast<float2*>(smem + (size_t)kWaves * kRowsPerWave * D * 4);
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -543,11 +548,13 @@ __global__ __launch_bounds__(kThreads, 1) void attn_main(AttnArgs a) {
   }
 }
 
-// Merge the S chunk partials of every row: out = sum_s e_s O_s / sum_s e_s
-// l_s with e_s = 2^(m_s - max m).  One wave per 16x16 fragment.
+// Merge the chunk partials of every row: out = sum_s e_s O_s / sum_s e_s
+// l_s with e_s = 2^(m_s - max m).  Only chunks that hold tiles of this row
+// block were written.  One wave per 16x16 fragment; loads are issued in
+// groups of 8 so their latencies overlap.
 template <int D, int RB>
 __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
-  constexpr int NTG = RB / 16, DT = D / 16;
+  constexpr int NTG = RB / 16, DT = D / 16, U = 8;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g4 = lane >> 4, l16 = lane & 15;
   const int F = blockIdx.x * 4 + wave;  // fragment id; all 4 of a block share (b,g,rb)
@@ -564,51 +571,80 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
   const int dt = f / NTG, ntg = f % NTG;
   const int row = ntg * 16 + l16, r = rb * RB + row;
   if (r >= a.M) return;
+  // chunks of this row block that hold tiles (the same count the main
+  // kernel derives from kv_len and the block's last node)
+  int kvl = a.kv_len ? a.kv_len[b] : a.Lmax;
+  kvl = kvl < 0 ? 0 : (kvl > a.Lmax ? a.Lmax : kvl);
+  const int i_hi = (min(rb * RB + RB, a.M) - 1) / a.G;
+  const int T = (kvl + kKeyTile - 1) / kKeyTile + i_hi / kKeyTile + 1;
+  const int nval = min(a.S, (T + a.chunk - 1) / a.chunk);
   const size_t base = (size_t)(bg * a.nRB + rb) * a.S;
   float mstar = -INFINITY;
-  for (int s = 0; s < a.S; ++s) mstar = fmaxf(mstar, a.ws_ml[(base + s) * RB + row].x);
+  for (int s0 = 0; s0 < nval; s0 += U) {
+    float2 ml[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (s0 + u < nval) ml[u] = a.ws_ml[(base + s0 + u) * RB + row];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (s0 + u < nval) mstar = fmaxf(mstar, ml[u].x);
+  }
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   float l = 0.f;
-  for (int s = 0; s < a.S; ++s) {
-    const float2 ml = a.ws_ml[(base + s) * RB + row];
-    if (ml.x == -INFINITY) continue;
-    const float e = __builtin_amdgcn_exp2f(ml.x - mstar);
-    l += e * ml.y;
-    acc += e * a.ws_o[((base + s) * DT * NTG + dt * NTG + ntg) * 64 + lane];
+  for (int s0 = 0; s0 < nval; s0 += U) {
+    float2 ml[U];
+    f32x4 ov[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (s0 + u < nval) {
+        ml[u] = a.ws_ml[(base + s0 + u) * RB + row];
+        ov[u] = a.ws_o[((base + s0 + u) * DT * NTG + dt * NTG + ntg) * 64 + lane];
+      }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (s0 + u < nval && ml[u].x != -INFINITY) {
+        const float e = __builtin_amdgcn_exp2f(ml[u].x - mstar);
+        l += e * ml[u].y;
+        acc += e * ov[u];
+      }
   }
   const float inv = bad ? NAN : 1.f / l;
   const int node = r / a.G, h = g * a.G + r % a.G;
-  const bf16x4 ov = {(__bf16)(acc[0] * inv), (__bf16)(acc[1] * inv), (__bf16)(acc[2] * inv),
+  const bf16x4 o4 = {(__bf16)(acc[0] * inv), (__bf16)(acc[1] * inv), (__bf16)(acc[2] * inv),
                      (__bf16)(acc[3] * inv)};
   *reinterpret_cast<bf16x4*>(a.out + ((size_t)(b * a.N + node) * a.Hq + h) * D + 16 * dt +
-                             4 * g4) = ov;
+                             4 * g4) = o4;
 }
 
-template <int D, int WR>
+template <int D, int ARR>
 static hipError_t launch_attn_t(const AttnArgs& a, const AttnPlan& p, hipStream_t st) {
-  constexpr int RB = kRowsPerWave * WR;
-  hipError_t e = hipFuncSetAttribute((const void*)attn_main<D, WR>,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     (int)p.lds_bytes);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attn_main<D, WR>), dim3(p.grid), dim3(kThreads), p.lds_bytes, st, a);
-  e = hipGetLastError();
-  if (e != hipSuccess || p.S == 1) return e;
-  const int frags = a.B * a.Hkv * p.nRB * (D / 16) * (RB / 16);
-  hipLaunchKernelGGL((attn_combine<D, RB>), dim3(frags / 4), dim3(256), 0, st, a);
-  return hipGetLastError();
+  constexpr Arrangement ar = kArrangements[ARR];
+  constexpr int NS = arr_stages(ar, D);
+  if constexpr (NS == 0) {
+    return hipErrorInvalidValue;  // never planned: the ring does not fit
+  } else {
+    constexpr int RB = kRowsPerWave * ar.WR;
+    hipError_t e = hipFuncSetAttribute((const void*)attn_main<D, ar.WR, ar.WK, NS>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)p.lds_bytes);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((attn_main<D, ar.WR, ar.WK, NS>), dim3(p.grid), dim3(64 * ar.WR * ar.WK),
+                       p.lds_bytes, st, a);
+    e = hipGetLastError();
+    if (e != hipSuccess || p.S == 1) return e;
+    const int frags = a.B * a.Hkv * p.nRB * (D / 16) * (RB / 16);
+    hipLaunchKernelGGL((attn_combine<D, RB>), dim3(frags / 4), dim3(256), 0, st, a);
+    return hipGetLastError();
+  }
 }
 
-template <int D>
+template <int D, int K = 0>
 static hipError_t launch_attn_d(const AttnArgs& a, const AttnPlan& p, hipStream_t st) {
-  // arrangements whose ring does not fit in LDS are never planned
-  if constexpr (ring_stages(D, kWavesPerWG / 1) > 0)
-    if (p.WR == 1) return launch_attn_t<D, 1>(a, p, st);
-  switch (p.WR) {
-    case 2: return launch_attn_t<D, 2>(a, p, st);
-    case 4: return launch_attn_t<D, 4>(a, p, st);
-    case 8: return launch_attn_t<D, 8>(a, p, st);
-    default: return hipErrorInvalidValue;
+  if constexpr (K < kNumArrangements) {
+    if (p.arr == K) return launch_attn_t<D, K>(a, p, st);
+    return launch_attn_d<D, K + 1>(a, p, st);
+  } else {
+    return hipErrorInvalidValue;
   }
 }
 

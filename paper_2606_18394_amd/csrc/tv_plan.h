@@ -14,59 +14,73 @@ inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 
 // Attention work decomposition.  Rows of one (sequence, KV head) pair are the
 // N*G (node, query-head-in-group) pairs, row r = node * G + head_in_group.
-// A workgroup of 8 waves (two per SIMD) takes a block of RB = 32*WR
-// consecutive rows and one fixed-size chunk of the key tiles (cache tiles
-// first, then tree tiles): WR row groups of one 32-row wave each, times
-// WK = 8/WR key groups that split the chunk's tiles between them.
-constexpr int kThreads = 512;
-constexpr int kWavesPerWG = 8;
+// A workgroup takes a block of RB = 32*WR consecutive rows and one
+// fixed-size chunk of the key tiles (cache tiles first, then tree tiles).
+// Its WR*WK waves form WR row groups (32 rows per wave) times WK key groups
+// that split the chunk's tiles between them; each key group streams its
+// tiles through an LDS ring of NS stages.  Arrangements are sized so that a
+// CU holds 8 waves (two per SIMD), from one or more workgroups.
 constexpr int kRowsPerWave = 32;
+constexpr int kWavesPerCU = 8;
+constexpr size_t kMaxLds = 160 * 1024;
 
-// LDS ring depth per key group (stages of one 32-key K tile + V tile);
-// 0 marks an arrangement that does not fit.
-constexpr int ring_stages(int D, int WK) {
-  return D == 128 ? (WK <= 2 ? 4 : (WK == 4 ? 2 : 0)) : (WK <= 4 ? 4 : 2);
-}
+struct Arrangement {
+  int WR, WK, NS128, NS64;
+};
+// WR x WK waves; ring stages for D = 128 and D = 64 (16 KB / 8 KB stages)
+constexpr Arrangement kArrangements[] = {
+    {8, 1, 4, 4}, {4, 2, 4, 4}, {2, 4, 2, 4}, {1, 8, 0, 2},
+    {4, 1, 4, 4}, {2, 2, 2, 4}, {2, 1, 2, 4},
+};
+constexpr int kNumArrangements = sizeof(kArrangements) / sizeof(kArrangements[0]);
+
+constexpr int arr_stages(const Arrangement& a, int D) { return D == 128 ? a.NS128 : a.NS64; }
 
 struct AttnPlan {
-  int WR;                      // row groups (waves per key group)
+  int arr;                     // index into kArrangements
+  int WR, WK, NS, threads, wg_per_cu;
   int G, M, RB, nRB, S, chunk;
   int nwork, grid;             // work items, launched workgroups (x8 padded)
   size_t ws_o_bytes, ws_ml_bytes, ws_bytes;
   size_t lds_bytes;            // dynamic LDS of the main kernel
 };
 
-inline size_t attn_lds_bytes(int D, int WR, int G, int N) {
-  const int WK = kWavesPerWG / WR, RB = kRowsPerWave * WR;
+inline size_t attn_lds_bytes(int D, int WR, int WK, int NS, int G, int N) {
+  const int RB = kRowsPerWave * WR;
   const size_t stage = 2 * (size_t)kKeyTile * 2 * D;
-  const size_t ring = (size_t)WK * ring_stages(D, WK) * stage;
+  const size_t ring = (size_t)WK * NS * stage;
   const int words = cdiv(N, 32);
   const int nodes = RB / G + 2;
   const size_t tree = (size_t)nodes * words * 4 + (size_t)N * 4 + 16;
-  const size_t merge =
-      WK == 1 ? 0 : (size_t)kWavesPerWG * kRowsPerWave * D * 4 + (size_t)kWavesPerWG * kRowsPerWave * 8;
+  const size_t waves = (size_t)WR * WK;
+  const size_t merge = WK == 1 ? 0 : waves * kRowsPerWave * D * 4 + waves * kRowsPerWave * 8;
   const size_t a = ring + tree;
   return a > merge ? a : merge;
 }
 
-constexpr size_t kMaxLds = 160 * 1024;
-
-// The plan for one arrangement WR: split count and sizes.
-inline AttnPlan attn_plan_wr(int B, int N, int Hq, int Hkv, int D, int Lmax, int WR) {
+// The plan for one arrangement: split count and sizes (grid sized to fill
+// every CU with its workgroups-per-CU).
+inline AttnPlan attn_plan_arr(int B, int N, int Hq, int Hkv, int D, int Lmax, int arr) {
+  const Arrangement& ar = kArrangements[arr];
   AttnPlan p{};
-  p.WR = WR;
+  p.arr = arr;
+  p.WR = ar.WR;
+  p.WK = ar.WK;
+  p.NS = arr_stages(ar, D);
+  p.threads = 64 * ar.WR * ar.WK;
+  p.wg_per_cu = kWavesPerCU / (ar.WR * ar.WK);
   p.G = Hq / Hkv;
   p.M = N * p.G;
-  p.RB = kRowsPerWave * WR;
+  p.RB = kRowsPerWave * ar.WR;
   p.nRB = cdiv(p.M, p.RB);
-  const int WK = kWavesPerWG / WR;
   const int tiles = cdiv(Lmax, kKeyTile) + cdiv(N, kKeyTile);
   const long long base = (long long)B * Hkv * p.nRB;
-  const long long target = 256;                 // one workgroup per CU
-  const int min_chunk = 2 * WK;                 // >= 2 tiles per key group
+  const long long target = 256LL * p.wg_per_cu;  // every CU full
+  const int min_chunk = 2 * ar.WK;               // >= 2 tiles per key group
   long long S = (target + base - 1) / base;
   const long long max_s = tiles / min_chunk > 1 ? tiles / min_chunk : 1;
   if (S > max_s) S = max_s;
+  if (B > 1 && S < 4 && max_s >= 4) S = 4;        // ragged batches: balance long sequences
   if (S < 1) S = 1;
   p.chunk = cdiv(tiles, S);
   p.S = cdiv(tiles, p.chunk);
@@ -78,16 +92,23 @@ inline AttnPlan attn_plan_wr(int B, int N, int Hq, int Hkv, int D, int Lmax, int
     p.ws_ml_bytes = (size_t)B * Hkv * p.nRB * p.S * p.RB * 8;
   }
   p.ws_bytes = p.ws_o_bytes + p.ws_ml_bytes;
-  p.lds_bytes = attn_lds_bytes(D, WR, p.G, N);
+  p.lds_bytes = p.NS > 0 ? attn_lds_bytes(D, ar.WR, ar.WK, p.NS, p.G, N) : kMaxLds + 1;
   return p;
 }
 
-// Rough time (arbitrary units) of an arrangement: matrix work on padded
-// rows, K/V traffic from L2 (each row block re-reads the keys), and the
-// split partials written and read back.
+inline bool attn_plan_fits(const AttnPlan& p) {
+  return p.NS > 0 && p.lds_bytes * p.wg_per_cu <= kMaxLds;
+}
+
+// Rough time of an arrangement: matrix work on padded rows, K/V traffic
+// from L2 (each row block re-reads the keys), HBM, the split partials
+// written and read back, and a penalty when the two waves of a SIMD belong
+// to one workgroup (its per-tile barriers keep them in phase, so their
+// matrix and vector work overlap poorly).
 inline double attn_plan_cost(const AttnPlan& p, int B, int Hkv, int D, int Lmax, int N) {
   const double keys = (double)Lmax + N;
-  const double mfma = (double)B * Hkv * p.nRB * p.RB * keys * 4.0 * D / 2.0e15;
+  double mfma = (double)B * Hkv * p.nRB * p.RB * keys * 4.0 * D / 2.0e15;
+  if (p.wg_per_cu == 1 && p.WR > 1) mfma *= 1.3;
   const double kv = (double)B * Hkv * keys * D * 4.0;
   const double l2 = kv * p.nRB / 20.0e12;
   const double hbm = kv / 6.0e12;
@@ -100,16 +121,15 @@ inline double attn_plan_cost(const AttnPlan& p, int B, int Hkv, int D, int Lmax,
 inline AttnPlan attn_plan(int B, int N, int Hq, int Hkv, int D, int Lmax) {
   AttnPlan best{};
   double best_cost = 0;
-  const int candidates[4] = {1, 2, 4, 8};
-  for (int WR : candidates) {
-    const int WK = kWavesPerWG / WR;
-    if (ring_stages(D, WK) == 0) continue;
-    const AttnPlan p = attn_plan_wr(B, N, Hq, Hkv, D, Lmax, WR);
-    if (p.lds_bytes > kMaxLds) continue;
+  bool have = false;
+  for (int k = 0; k < kNumArrangements; ++k) {
+    const AttnPlan p = attn_plan_arr(B, N, Hq, Hkv, D, Lmax, k);
+    if (!attn_plan_fits(p)) continue;
     const double c = attn_plan_cost(p, B, Hkv, D, Lmax, N);
-    if (best.WR == 0 || c < best_cost) {
+    if (!have || c < best_cost) {
       best = p;
       best_cost = c;
+      have = true;
     }
   }
   return best;

@@ -18,7 +18,7 @@ int main() {
     const int tiles = tv::cdiv(Lmax, tv::kKeyTile) + tv::cdiv(N, tv::kKeyTile);
     bool ok = p.grid % tv::kXcds == 0 && p.nwork == B * Hkv * p.nRB * p.S && p.grid >= p.nwork;
     ok = ok && (long long)p.S * p.chunk >= tiles && (long long)(p.S - 1) * p.chunk < tiles;
-    ok = ok && p.WR >= 1 && p.RB == tv::kRowsPerWave * p.WR && tv::ring_stages(D, tv::kWavesPerWG / p.WR) > 0;
+    ok = ok && p.WR >= 1 && p.RB == tv::kRowsPerWave * p.WR && tv::attn_plan_fits(p);
     const int per = p.grid / tv::kXcds;
     for (int bid = 0; bid < p.grid && ok; ++bid) {
       int w = (bid % tv::kXcds) * per + bid / tv::kXcds;

@@ -258,7 +258,7 @@ def main():
 
     tokens = w.B * w.N
     line = {
-        "metric": "tree-verify us/step & tree-tokens/s; % of HBM/MFMA roofline at 1 MI355X",
+        "metric": "tree-verify \u00b5s/step & tree-tokens/s; % of HBM/MFMA roofline at 1 MI355X",
         "value": tokens / (ms_step * 1e-3),
         "unit": "tree-tokens/s",
         "n_gpus": 1,

@@ -155,13 +155,7 @@ __global__ __launch_bounds__(256) void accept_finish(AcceptArgs a) {
   const int tid = threadIdx.x;
   const int b = blockIdx.x;
   const int N = a.N;
-  // the split keys of all rows: independent loads, merged with LDS max
-  for (int i = tid; i < N; i += 256) rowkey[i] = 0ull;
-  __syncthreads();
-  const size_t kbase = (size_t)b * N * a.nsplit;
-  for (int idx = tid; idx < N * a.nsplit; idx += 256)
-    atomicMax(&rowkey[idx / a.nsplit], a.part[kbase + idx]);
-  int bad = 0;
+  // parents and drafts of this thread's nodes: loads issued first
   int pv[kMaxNodes / 256], dv[kMaxNodes / 256];
 #pragma unroll
   for (int k = 0; k < kMaxNodes / 256; ++k) {
@@ -169,6 +163,27 @@ __global__ __launch_bounds__(256) void accept_finish(AcceptArgs a) {
     pv[k] = i < N ? a.parent[(size_t)b * N + i] : 0;
     dv[k] = i < N ? a.draft[(size_t)b * N + i] : 0;
   }
+  // the split keys of all rows, merged with LDS max; loads go out in
+  // batches of kFinishLoads so their latencies overlap
+  constexpr int kFinishLoads = 8;
+  for (int i = tid; i < N; i += 256) rowkey[i] = 0ull;
+  __syncthreads();
+  const size_t kbase = (size_t)b * N * a.nsplit;
+  const int nkeys = N * a.nsplit;
+  for (int idx0 = 0; idx0 < nkeys; idx0 += 256 * kFinishLoads) {
+    unsigned long long kv[kFinishLoads];
+#pragma unroll
+    for (int u = 0; u < kFinishLoads; ++u) {
+      const int idx = idx0 + 256 * u + tid;
+      kv[u] = idx < nkeys ? a.part[kbase + idx] : 0ull;
+    }
+#pragma unroll
+    for (int u = 0; u < kFinishLoads; ++u) {
+      const int idx = idx0 + 256 * u + tid;
+      if (idx < nkeys) atomicMax(&rowkey[idx / a.nsplit], kv[u]);
+    }
+  }
+  int bad = 0;
   __syncthreads();
 #pragma unroll
   for (int k = 0; k < kMaxNodes / 256; ++k) {

@@ -12,23 +12,26 @@
 // 32-key tiles: ceil(kv_len/32) cache tiles, then the tree tiles up to the
 // last node of the row block (a node never sees a later node because
 // parents precede children).  The tiles are cut into S contiguous chunks of
-// a fixed size (split-KV).  One workgroup = 4 wave64s takes one row block
-// and one chunk, in one of two arrangements:
-//   * keys mode (64-row blocks, for short trees): every wave owns all 64
-//     rows and every 4th tile, streams its tiles through a private LDS ring,
-//     and the 4 waves merge their partial softmax states in LDS at the end;
-//   * rows mode (256-row blocks, for large trees or GQA groups): every wave
-//     owns 64 rows and all 4 waves consume one shared LDS ring, so each K/V
-//     byte fetched serves 256 rows.
-// K and V tiles move HBM -> LDS with global_load_lds_dwordx4 (no register
-// staging), rows XOR-swizzled in 16-byte chunks so the reads below are free
-// of bank conflicts.  Per 32-key tile a wave computes S^T = K Q^T with
-// v_mfma_f32_16x16x32_bf16 (keys on the M side, its 64 rows on the N side),
+// a fixed size (split-KV).  A workgroup takes one block of 32*WR rows and
+// one chunk with WR x WK wave64s: WR row groups of 32 rows, and WK key
+// groups that share out the chunk's tiles, each streaming its tiles through
+// an LDS ring of NS stages; key groups merge their softmax states in LDS at
+// the end.  The host plan (tv_plan.h) picks WR, WK, NS and S per shape so
+// that every CU holds 8 waves (two per SIMD).
+//
+// Per tile.  K and V move HBM -> LDS with global_load_lds_dwordx4 (no
+// register staging), rows XOR-swizzled in 16-byte chunks so the reads below
+// are free of bank conflicts.  A wave computes S^T = K Q^T with
+// v_mfma_f32_16x16x32_bf16 (keys on the M side, its 32 rows on the N side),
 // runs an fp32 base-2 online softmax on the accumulators with a lazily moved
 // reference maximum, and accumulates O^T += V^T P^T: P^T comes straight from
 // the S^T accumulators (the 32 keys are ordered so the B operand needs no
-// data movement) and V^T from ds_read_b64_tr_b16 transposing reads.  With
-// S > 1 a second kernel merges the chunks' (max, sum, O) partials.
+// data movement) and V^T from ds_read_b64_tr_b16 transposing reads.
+//
+// Split-KV merge (S > 1).  Every chunk stores its (max, sum, O) partial.
+// When one workgroup can merge a row block in one batch of loads, the
+// chunk that finishes last does it inside this kernel (arrival counters in
+// the workspace); otherwise a second kernel merges all row blocks.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -54,9 +57,54 @@ struct AttnArgs {
   __bf16* out;
   f32x4* ws_o;
   float2* ws_ml;
+  unsigned int* arrived;  // per row block: chunks that have stored partials
+  int* tree_bad;          // per row block: invalid parent array seen
   int B, N, Hq, Hkv, Lmax, G, M, nRB, S, chunk, nwork;
+  int fused;  // split-KV merge inside the main kernel (else a second kernel)
   float c;  // scale * log2(e): scores live in base-2 exponent units
 };
+
+// Four output values, or four NaN when the sequence's tree is invalid (the
+// NaN is written as a bit pattern: the kernels assume no NaN arithmetic).
+__device__ __forceinline__ void store_out4(__bf16* p, const f32x4& acc, float inv, bool nan) {
+  const bf16x4 v = {(__bf16)(acc[0] * inv), (__bf16)(acc[1] * inv), (__bf16)(acc[2] * inv),
+                    (__bf16)(acc[3] * inv)};
+  i16x4 bits = __builtin_bit_cast(i16x4, v);
+  if (nan) bits = i16x4{0x7FC0, 0x7FC0, 0x7FC0, 0x7FC0};
+  *reinterpret_cast<i16x4*>(p) = bits;
+}
+
+// Split-KV partials cross workgroups (and XCDs) through device-scope
+// accesses: the sc1 bit makes a store complete only once it is visible at
+// device scope and a load read at that level, which is how the compiler
+// lowers relaxed agent-scope atomic loads and stores; these are their
+// 8- and 16-byte forms.  Publishing then needs only vmcnt(0) before the
+// arrival counter, where a release fence would write back the whole L2,
+// and the merging workgroup needs no L2 invalidate (which would evict the
+// keys that other workgroups are still reading).
+__device__ __forceinline__ void store_dev(f32x4* p, f32x4 v) {
+  asm volatile("global_store_dwordx4 %0, %1, off sc1" ::"v"(p), "v"(v) : "memory");
+}
+__device__ __forceinline__ void store_dev(float2* p, float2 v) {
+  asm volatile("global_store_dwordx2 %0, %1, off sc1" ::"v"(p), "v"(v) : "memory");
+}
+__device__ __forceinline__ f32x4 load_dev(const f32x4* p) {
+  f32x4 v;
+  asm volatile("global_load_dwordx4 %0, %1, off sc1" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+__device__ __forceinline__ float2 load_dev(const float2* p) {
+  float2 v;
+  asm volatile("global_load_dwordx2 %0, %1, off sc1" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+// Waits for every outstanding vector memory access; `loaded` values of
+// load_dev are tied to the wait so no use is scheduled before it.
+__device__ __forceinline__ void wait_all_vm() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+template <class T>
+__device__ __forceinline__ void loaded(T& v) {
+  asm volatile("" : "+v"(v));
+}
 
 __device__ __forceinline__ float wave_max_across_groups(float v) {
   v = fmaxf(v, __shfl_xor(v, 16));
@@ -235,6 +283,75 @@ __device__ __forceinline__ void softmax_pv(const f32x4 (&sc)[2][NT], const float
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
       o[dt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[nt], o[dt][nt], 0, 0, 0);
+  }
+}
+
+// Merge of the chunk partials of one row block, run by the workgroup whose
+// chunk arrived last: out = sum_s e_s O_s / sum_s e_s l_s, e_s = 2^(m_s - m*),
+// folded in online over s in batches of loads.  Wave w takes one 16-row
+// tile and every WPN-th 16-column tile of it (or several row tiles when the
+// block has more row tiles than the workgroup has waves), so each lane
+// reads its rows' (m, l) once.
+template <int D, int RB, int kWaves>
+__device__ __forceinline__ void merge_chunks(const AttnArgs& a, size_t part0, int nval, int b,
+                                             int g, int r0, bool bad, int wave, int lane) {
+  constexpr int DT = D / 16, NTG = RB / 16;
+  constexpr bool kSplitCols = kWaves >= NTG;
+  constexpr int WPN = kSplitCols ? kWaves / NTG : 1;  // waves per row tile
+  constexpr int NPW = kSplitCols ? 1 : NTG / kWaves;  // row tiles per wave
+  constexpr int DPW = DT / WPN;                       // column tiles per wave
+  constexpr int UB = 32 / DPW;                        // chunks per batch of loads
+  static_assert(DT % WPN == 0 && NTG % (kSplitCols ? 1 : kWaves) == 0, "merge split");
+  const int g4 = lane >> 4, l16 = lane & 15;
+#pragma unroll
+  for (int k = 0; k < NPW; ++k) {
+    const int ntg = kSplitCols ? wave % NTG : wave + k * kWaves;
+    const int dt0 = kSplitCols ? wave / NTG : 0;
+    const int row = ntg * 16 + l16;
+    float m = -INFINITY, l = 0.f;
+    f32x4 acc[DPW];
+#pragma unroll
+    for (int j = 0; j < DPW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < nval; s0 += UB) {
+      float2 ml[UB];
+      f32x4 ov[UB][DPW];
+#pragma unroll
+      for (int u = 0; u < UB; ++u)
+        if (s0 + u < nval) {
+          const size_t ps = part0 + s0 + u;
+          ml[u] = load_dev(&a.ws_ml[ps * RB + row]);
+#pragma unroll
+          for (int j = 0; j < DPW; ++j)
+            ov[u][j] = load_dev(&a.ws_o[(ps * DT * NTG + (dt0 + j * WPN) * NTG + ntg) * 64 + lane]);
+        }
+      wait_all_vm();
+#pragma unroll
+      for (int u = 0; u < UB; ++u)
+        if (s0 + u < nval) {
+          loaded(ml[u]);
+#pragma unroll
+          for (int j = 0; j < DPW; ++j) loaded(ov[u][j]);
+        }
+#pragma unroll
+      for (int u = 0; u < UB; ++u)
+        if (s0 + u < nval && ml[u].x != -INFINITY) {
+          const float mn = fmaxf(m, ml[u].x);
+          const float ea = __builtin_amdgcn_exp2f(m - mn);  // 0 while m = -inf
+          const float eb = __builtin_amdgcn_exp2f(ml[u].x - mn);
+          l = l * ea + eb * ml[u].y;
+#pragma unroll
+          for (int j = 0; j < DPW; ++j) acc[j] = acc[j] * ea + eb * ov[u][j];
+          m = mn;
+        }
+    }
+    const int r = r0 + row;
+    if (r < a.M) {
+      const int node = r / a.G, h = g * a.G + r % a.G;
+      __bf16* op = a.out + ((size_t)(b * a.N + node) * a.Hq + h) * D + 4 * g4;
+      const float inv = 1.f / l;
+#pragma unroll
+      for (int j = 0; j < DPW; ++j) store_out4(op + 16 * (dt0 + j * WPN), acc[j], inv, bad);
+    }
   }
 }
 
@@ -482,6 +599,8 @@ void attn_main(AttnArgs a) {
   for (int nt = 0; nt < NT; ++nt) lsum[nt] = lacc[nt][0];
   const int invalid = has_tree ? *flag : 0;
   const int bg = b * a.Hkv + g;
+  const size_t grp = (size_t)bg * a.nRB + rb;  // row block id
+  const size_t part0 = grp * a.S;              // its first chunk partial
 
   // Final values of one 16x16 fragment (dt, ntg) of this workgroup's rows:
   // either the normalised bf16 output (single chunk) or the chunk partial.
@@ -491,17 +610,19 @@ void attn_main(AttnArgs a) {
       const int r = r0 + row;
       if (r < a.M) {
         const int node = r / a.G, h = g * a.G + r % a.G;
-        const float inv = invalid ? NAN : 1.f / l;
-        const bf16x4 ov = {(__bf16)(acc[0] * inv), (__bf16)(acc[1] * inv),
-                           (__bf16)(acc[2] * inv), (__bf16)(acc[3] * inv)};
-        *reinterpret_cast<bf16x4*>(a.out + ((size_t)(b * a.N + node) * a.Hq + h) * D + 16 * dt +
-                                   4 * g4) = ov;
+        store_out4(a.out + ((size_t)(b * a.N + node) * a.Hq + h) * D + 16 * dt + 4 * g4, acc,
+                   1.f / l, invalid != 0);
       }
     } else {
-      const size_t fr = ((size_t)(bg * a.nRB + rb) * a.S + s) * DT * NTG;
-      a.ws_o[(fr + dt * NTG + ntg) * 64 + lane] = acc;
-      if (dt == 0 && g4 == 0)
-        a.ws_ml[((size_t)(bg * a.nRB + rb) * a.S + s) * RB + row] = make_float2(mstar, l);
+      f32x4* po = &a.ws_o[((part0 + s) * DT * NTG + dt * NTG + ntg) * 64 + lane];
+      float2* pml = &a.ws_ml[(part0 + s) * RB + row];
+      if (a.fused) {  // read by another workgroup of this kernel
+        store_dev(po, acc);
+        if (dt == 0 && g4 == 0) store_dev(pml, make_float2(mstar, l));
+      } else {        // read by the merge kernel
+        *po = acc;
+        if (dt == 0 && g4 == 0) *pml = make_float2(mstar, l);
+      }
     }
   };
 
@@ -510,46 +631,69 @@ void attn_main(AttnArgs a) {
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) emit(dt, wr * NT + nt, o[dt][nt], m[nt], lsum[nt]);
-    return;
+  } else {
+    // ---- merge the WK key groups of each row group (same rows, disjoint keys)
+    __syncthreads();  // rings and tree tables are dead from here on
+    f32x4* obuf = reinterpret_cast<f32x4*>(smem);
+    float2* mlbuf = reinterpret_cast<float2*>(smem + (size_t)kWaves * kRowsPerWave * D * 4);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) obuf[((wave * DT + dt) * NT + nt) * 64 + lane] = o[dt][nt];
+    if (g4 == 0) {
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+        mlbuf[wave * kRowsPerWave + nt * 16 + l16] = make_float2(m[nt], lsum[nt]);
+    }
+    __syncthreads();
+    for (int f = wk; f < DT * NT; f += WK) {
+      const int dt = f / NT, nt = f % NT;
+      const int rw = nt * 16 + l16;  // row within the wave's 32
+      float mw[WK], mstar = -INFINITY;
+#pragma unroll
+      for (int k = 0; k < WK; ++k) {
+        mw[k] = mlbuf[(k * WR + wr) * kRowsPerWave + rw].x;
+        mstar = fmaxf(mstar, mw[k]);
+      }
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      float l = 0.f;
+#pragma unroll
+      for (int k = 0; k < WK; ++k) {
+        const float e = mw[k] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw[k] - mstar);
+        l += e * mlbuf[(k * WR + wr) * kRowsPerWave + rw].y;
+        acc += e * obuf[(((k * WR + wr) * DT + dt) * NT + nt) * 64 + lane];
+      }
+      emit(dt, wr * NT + nt, acc, mstar, l);
+    }
   }
+  if (a.S == 1 || !a.fused) return;
 
-  // ---- merge the WK key groups of each row group (same rows, disjoint keys)
-  __syncthreads();  // rings and tree tables are dead from here on
-  f32x4* obuf = reinterpret_cast<f32x4*>(smem);
-  float2* mlbuf = reinterpret_cast<float2*>(smem + (size_t)kWaves * kRowsPerWave * D * 4);
-#pragma unroll
-  for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) obuf[((wave * DT + dt) * NT + nt) * 64 + lane] = o[dt][nt];
-  if (g4 == 0) {
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-      mlbuf[wave * kRowsPerWave + nt * 16 + l16] = make_float2(m[nt], lsum[nt]);
+  // ---- fused split-KV merge: the chunk that arrives last merges its row
+  // block.  Every workgroup publishes its partial (device-scope stores,
+  // completed before the count), then counts itself in; the one that
+  // completes the count merges and resets the counter for the next call.
+  // Only chunks that hold tiles take part: nval of them.
+  const int nval = min(a.S, (T + a.chunk - 1) / a.chunk);
+  __shared__ int s_last;
+  if (has_tree && tid == 0)  // every row block has a chunk with tree tiles
+    __hip_atomic_store(a.tree_bad + grp, invalid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  wait_all_vm();
+  __syncthreads();
+  if (tid == 0) {
+    const unsigned int before =
+        __hip_atomic_fetch_add(a.arrived + grp, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const bool last = before + 1 == (unsigned int)nval;
+    if (last) __hip_atomic_store(a.arrived + grp, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = last;
   }
   __syncthreads();
-  for (int f = wk; f < DT * NT; f += WK) {
-    const int dt = f / NT, nt = f % NT;
-    const int rw = nt * 16 + l16;  // row within the wave's 32
-    float mw[WK], mstar = -INFINITY;
-#pragma unroll
-    for (int k = 0; k < WK; ++k) {
-      mw[k] = mlbuf[(k * WR + wr) * kRowsPerWave + rw].x;
-      mstar = fmaxf(mstar, mw[k]);
-    }
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    float l = 0.f;
-#pragma unroll
-    for (int k = 0; k < WK; ++k) {
-      const float e = mw[k] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw[k] - mstar);
-      l += e * mlbuf[(k * WR + wr) * kRowsPerWave + rw].y;
-      acc += e * obuf[(((k * WR + wr) * DT + dt) * NT + nt) * 64 + lane];
-    }
-    emit(dt, wr * NT + nt, acc, mstar, l);
-  }
+  if (!s_last) return;
+  const bool bad = __hip_atomic_load(a.tree_bad + grp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
+  merge_chunks<D, RB, kWaves>(a, part0, nval, b, g, r0, bad, wave, lane);
 }
 
-// Merge the chunk partials of every row: out = sum_s e_s O_s / sum_s e_s
-// l_s with e_s = 2^(m_s - max m).  Only chunks that hold tiles of this row
+// Second kernel of the split-KV plans whose merge is too large for one
+// workgroup: out = sum_s e_s O_s / sum_s e_s l_s with e_s = 2^(m_s - max m).  Only chunks that hold tiles of this row
 // block were written.  One wave per 16x16 fragment; loads are issued in
 // groups of 8 so their latencies overlap.
 template <int D, int RB>
@@ -578,7 +722,7 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
   const int i_hi = (min(rb * RB + RB, a.M) - 1) / a.G;
   const int T = (kvl + kKeyTile - 1) / kKeyTile + i_hi / kKeyTile + 1;
   const int nval = min(a.S, (T + a.chunk - 1) / a.chunk);
-  const size_t base = (size_t)(bg * a.nRB + rb) * a.S;
+  const size_t base = (size_t)(bg * a.nRB + rb) * a.S;  // first chunk partial
   float mstar = -INFINITY;
   for (int s0 = 0; s0 < nval; s0 += U) {
     float2 ml[U];
@@ -608,12 +752,9 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
         acc += e * ov[u];
       }
   }
-  const float inv = bad ? NAN : 1.f / l;
   const int node = r / a.G, h = g * a.G + r % a.G;
-  const bf16x4 o4 = {(__bf16)(acc[0] * inv), (__bf16)(acc[1] * inv), (__bf16)(acc[2] * inv),
-                     (__bf16)(acc[3] * inv)};
-  *reinterpret_cast<bf16x4*>(a.out + ((size_t)(b * a.N + node) * a.Hq + h) * D + 16 * dt +
-                             4 * g4) = o4;
+  store_out4(a.out + ((size_t)(b * a.N + node) * a.Hq + h) * D + 16 * dt + 4 * g4, acc, 1.f / l,
+             bad != 0);
 }
 
 template <int D, int ARR>
@@ -623,7 +764,6 @@ static hipError_t launch_attn_t(const AttnArgs& a, const AttnPlan& p, hipStream_
   if constexpr (NS == 0) {
     return hipErrorInvalidValue;  // never planned: the ring does not fit
   } else {
-    constexpr int RB = kRowsPerWave * ar.WR;
     hipError_t e = hipFuncSetAttribute((const void*)attn_main<D, ar.WR, ar.WK, NS>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)p.lds_bytes);
@@ -631,7 +771,8 @@ static hipError_t launch_attn_t(const AttnArgs& a, const AttnPlan& p, hipStream_
     hipLaunchKernelGGL((attn_main<D, ar.WR, ar.WK, NS>), dim3(p.grid), dim3(64 * ar.WR * ar.WK),
                        p.lds_bytes, st, a);
     e = hipGetLastError();
-    if (e != hipSuccess || p.S == 1) return e;
+    if (e != hipSuccess || p.S == 1 || p.fused) return e;
+    constexpr int RB = kRowsPerWave * ar.WR;
     const int frags = a.B * a.Hkv * p.nRB * (D / 16) * (RB / 16);
     hipLaunchKernelGGL((attn_combine<D, RB>), dim3(frags / 4), dim3(256), 0, st, a);
     return hipGetLastError();
@@ -661,8 +802,10 @@ hipError_t launch_attention(const void* q, const void* kc, const void* vc, const
   a.parent = parent;
   a.kv_len = kv_len;
   a.out = (__bf16*)out;
-  a.ws_o = (f32x4*)ws;
-  a.ws_ml = (float2*)((char*)ws + p.ws_o_bytes);
+  a.arrived = (unsigned int*)ws;
+  a.tree_bad = (int*)ws + kSyncGroups;
+  a.ws_o = (f32x4*)((char*)ws + p.ws_sync_bytes);
+  a.ws_ml = (float2*)((char*)ws + p.ws_sync_bytes + p.ws_o_bytes);
   a.B = B;
   a.N = N;
   a.Hq = Hq;
@@ -674,6 +817,7 @@ hipError_t launch_attention(const void* q, const void* kc, const void* vc, const
   a.S = p.S;
   a.chunk = p.chunk;
   a.nwork = p.nwork;
+  a.fused = p.fused;
   a.c = scale * 1.4426950408889634f;
   return D == 128 ? launch_attn_d<128>(a, p, st) : launch_attn_d<64>(a, p, st);
 }

@@ -21,6 +21,14 @@ inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 // tiles through an LDS ring of NS stages.  Arrangements are sized so that a
 // CU holds 8 waves (two per SIMD), from one or more workgroups.
 constexpr int kRowsPerWave = 32;
+// Split-KV plans keep per-row-block sync words (arrival counter, tree flag)
+// in a fixed region at the start of the workspace, the same place for every
+// shape, so that one zero-filled workspace can serve calls of any sizes: a
+// call's partials never overlap another call's counters, and each call
+// leaves its counters at zero.  Plans with more row blocks do not split.
+constexpr int kSyncGroups = 4096;
+constexpr size_t kSyncBytes = (size_t)kSyncGroups * 8;
+constexpr int kFusedMergeBytes = 512;
 constexpr int kWavesPerCU = 8;
 constexpr size_t kMaxLds = 160 * 1024;
 
@@ -41,7 +49,8 @@ struct AttnPlan {
   int WR, WK, NS, threads, wg_per_cu;
   int G, M, RB, nRB, S, chunk;
   int nwork, grid;             // work items, launched workgroups (x8 padded)
-  size_t ws_o_bytes, ws_ml_bytes, ws_bytes;
+  int fused;                   // S > 1: merge in the main kernel's last chunk
+  size_t ws_o_bytes, ws_ml_bytes, ws_sync_bytes, ws_bytes;
   size_t lds_bytes;            // dynamic LDS of the main kernel
 };
 
@@ -81,17 +90,24 @@ inline AttnPlan attn_plan_arr(int B, int N, int Hq, int Hkv, int D, int Lmax, in
   const long long max_s = tiles / min_chunk > 1 ? tiles / min_chunk : 1;
   if (S > max_s) S = max_s;
   if (B > 1 && S < 4 && max_s >= 4) S = 4;        // ragged batches: balance long sequences
-  if (S < 1) S = 1;
+  if (S < 1 || base > kSyncGroups) S = 1;
   p.chunk = cdiv(tiles, S);
   p.S = cdiv(tiles, p.chunk);
   p.nwork = (int)(base * p.S);
   p.grid = cdiv(p.nwork, kXcds) * kXcds;
   const int DT = D / 16, NTG = p.RB / 16;
   if (p.S > 1) {
+    // sync region (counters, then tree flags), chunk partials: O fragments,
+    // then (m, l) per row
+    p.ws_sync_bytes = kSyncBytes;
     p.ws_o_bytes = (size_t)B * Hkv * p.nRB * p.S * DT * NTG * 64 * 16;
     p.ws_ml_bytes = (size_t)B * Hkv * p.nRB * p.S * p.RB * 8;
   }
-  p.ws_bytes = p.ws_o_bytes + p.ws_ml_bytes;
+  p.ws_bytes = p.ws_sync_bytes + p.ws_o_bytes + p.ws_ml_bytes;
+  // The last chunk of a row block merges all of them when that takes one
+  // batch of loads per lane (<= kFusedMergeBytes per thread); larger merges
+  // go to a second kernel that spreads them over the whole GPU.
+  p.fused = p.S > 1 && (size_t)p.S * p.RB * D * 4 <= (size_t)kFusedMergeBytes * p.threads;
   p.lds_bytes = p.NS > 0 ? attn_lds_bytes(D, ar.WR, ar.WK, p.NS, p.G, N) : kMaxLds + 1;
   return p;
 }

@@ -30,7 +30,7 @@ def host_logits_f64(inp: dict) -> np.ndarray:
     return oracle.decode_bf16(inp["logits"])
 
 
-def gpu_attention(inp: dict, scale=None, kv_len=True, canary: int = 0):
+def gpu_attention(inp: dict, scale=None, kv_len=True, canary: int = 0, workspace=None):
     """Runs the HIP attention; returns (out fp32 numpy [B,N,Hq,D], canary_ok)."""
     from paper_2606_18394_amd import tree_verify_attention
     B, N, Hq, D = inp["q"].shape
@@ -40,7 +40,8 @@ def gpu_attention(inp: dict, scale=None, kv_len=True, canary: int = 0):
     tree_verify_attention(dev_bf16(inp["q"]), dev_bf16(inp["k_cache"]),
                           dev_bf16(inp["v_cache"]), dev_bf16(inp["k_tree"]),
                           dev_bf16(inp["v_tree"]), dev_i32(inp["parent"]), out,
-                          kv_len=dev_i32(inp["kv_len"]) if kv_len else None, scale=scale)
+                          kv_len=dev_i32(inp["kv_len"]) if kv_len else None, scale=scale,
+                          workspace_tensor=workspace)
     torch.cuda.synchronize()
     ok = True
     if canary:

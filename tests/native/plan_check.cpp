@@ -37,6 +37,34 @@ int main() {
       }
     }
     for (int v : seen) ok = ok && v == 1;
+    if (p.S > 1) {
+      // arrival counter + tree flag per row block; the workspace sections add up
+      const size_t groups = (size_t)B * Hkv * p.nRB;
+      if (groups > (size_t)tv::kSyncGroups || p.ws_sync_bytes != tv::kSyncBytes) ok = false;
+      if (p.ws_bytes != p.ws_o_bytes + p.ws_ml_bytes + p.ws_sync_bytes) ok = false;
+      // for any kv_len, the chunks that hold tiles are exactly the first
+      // nval = min(S, ceil(T / chunk)) and one of them holds tree tiles
+      for (int kvl : {0, 1, Lmax / 2, Lmax}) {
+        if (kvl < 0 || kvl > Lmax) continue;
+        const int nct = tv::cdiv(kvl, tv::kKeyTile);
+        for (int rb = 0; rb < p.nRB; ++rb) {
+          const int rows = p.M - rb * p.RB < p.RB ? p.M - rb * p.RB : p.RB;
+          const int i_hi = (rb * p.RB + rows - 1) / p.G;
+          const int T = nct + i_hi / tv::kKeyTile + 1;
+          const int nval = p.S < tv::cdiv(T, p.chunk) ? p.S : tv::cdiv(T, p.chunk);
+          int nonempty = 0, tree = 0;
+          for (int s = 0; s < p.S; ++s) {
+            const int t0 = s * p.chunk, t1 = t0 + p.chunk < T ? t0 + p.chunk : T;
+            if (t0 < t1) {
+              ++nonempty;
+              tree += t1 > nct;
+              if (s >= nval) ok = false;
+            }
+          }
+          if (nonempty != nval || tree < 1 || nval < 1) ok = false;
+        }
+      }
+    }
     if (p.lds_bytes > 160 * 1024) ok = false;
     for (int esize : {2, 4})
       for (int vec : {1, 16 / esize}) {

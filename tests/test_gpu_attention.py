@@ -171,3 +171,29 @@ def test_invalid_tree_rows_are_nan():
         ref = oracle_attention({k: (v[:1] if isinstance(v, np.ndarray) and v.ndim and
                                     v.shape[0] == B else v) for k, v in inp.items()})
         assert np.abs(got[:1] - ref).max() <= TOL
+
+
+def test_workspace_reuse_across_shapes():
+    """One zero-filled workspace serves calls of any sizes in any order
+    (split-KV counters live at a fixed place and are left at zero): every
+    result is bit-identical to the result with a fresh workspace."""
+    from paper_2606_18394_amd.binding import load_library
+    lib = load_library()
+    ws_need = lambda w: lib.tv_tree_verify_attention_workspace(w.B, w.N, w.Hq, w.Hkv, w.D, w.L)
+    W = synth.WORKLOADS
+    cases = [synth.with_shape(W["long_ctx"], L=8192, N=64, depth=8),
+             W["tiny"], W["qwen3_8b"],
+             synth.with_shape(W["batched_30b_a3b"], B=4, L=4096),
+             synth.with_shape(W["big_tree_32b"], L=2048, N=256)]
+    size = max(ws_need(w) for w in cases)
+    shared = torch.zeros(size, dtype=torch.uint8, device="cuda")
+    inps = [synth.draw(w, with_logits=False) for w in cases]
+    for rnd in range(2):
+        for w, inp in zip(cases, inps):
+            print(f"reuse round {rnd}: {w.name} B={w.B} N={w.N} L={w.L} ws={ws_need(w)}", flush=True)
+            got, _ = gpu_attention(inp, workspace=shared)
+            fresh = torch.zeros(max(256, ws_need(w)), dtype=torch.uint8, device="cuda")
+            ref, _ = gpu_attention(inp, workspace=fresh)
+            assert np.array_equal(got, ref), w.name
+            # counters back at zero, tree flags 0 for a valid tree
+            assert not fresh[:32768].any(), "sync words left non-zero"

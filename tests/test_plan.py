@@ -24,6 +24,8 @@ def shapes():
                 for D in [64, 128]:
                     for L in [0, 1, 64, 1000, 32768]:
                         out.append((B, N, Hq, Hkv, D, L, 151936 if N < 100 else 1001))
+    # more row blocks than the split-KV sync region holds: no split
+    out += [(64, 512, 64, 8, 128, 1000, 1001), (512, 64, 32, 8, 128, 32768, 1001)]
     return out
 
 

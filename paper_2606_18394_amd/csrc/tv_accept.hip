@@ -5,20 +5,24 @@
 // prediction at its parent and the parent is accepted; the result is the
 // deepest accepted root-to-node path (Sec. 2.4 greedy rule; App. E).
 //
-// Two kernels, no global atomics:
-//   scan    one workgroup per (node row, vocabulary split).  256 threads
-//           stream their slice with 16-byte loads, kScanLoadsPerThread of
-//           them in flight per thread, and keep a running first maximum;
-//           the workgroup reduces it with wave64 shuffles on the 64-bit key
-//             key = order-preserving(value) << 32 | (0xFFFFFFFF - index)
-//           whose maximum is the largest value at its lowest index (-0.0 is
-//           folded into +0.0 first, so equal values compare equal), and
-//           stores the key in the workspace.
-//   finish  one workgroup per sequence: merges the split keys into the
-//           per-node argmax, validates the tree, computes acceptance for all
-//           nodes at once by pointer jumping over the parent links
-//           (O(log depth) rounds), picks the deepest accepted node (lowest
-//           index on ties) and writes the path.
+// Scan: one workgroup per (node row, vocabulary split).  256 threads stream
+// the slice with 16-byte loads, kScanLoadsPerThread of them in flight per
+// thread, and keep a running first maximum; the workgroup reduces it with
+// wave64 shuffles on the 64-bit key
+//     key = order-preserving(value) << 32 | (0xFFFFFFFF - index)
+// whose maximum is the largest value at its lowest index (-0.0 is folded
+// into +0.0 first, so equal values compare equal).
+//
+// Acceptance of a sequence (one workgroup): validate the parent array,
+// compute acceptance for all nodes at once by pointer jumping over the
+// parent links (O(log depth) rounds), pick the deepest accepted node (lowest
+// index on ties) and write the path.
+//
+// Two kernels: the scan stores one key per (row, split); one workgroup per
+// sequence merges its rows' keys in LDS and runs the acceptance.  (A single
+// kernel whose last split and last row carry on through arrival counters
+// was measured slower: its chain of dependent device-scope round trips
+// outlasts the kernel boundary it saves.)
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -33,7 +37,7 @@ struct AcceptArgs {
   int32_t* accept_len;
   int32_t* path;
   int32_t* tgt_out;
-  unsigned long long* part;
+  unsigned long long* part;  // split keys [rows, nsplit]
   int B, N, V, Dmax, nsplit;
   long long cps;  // chunks per split
 };
@@ -43,6 +47,10 @@ __device__ __forceinline__ unsigned long long make_key(float v, unsigned int idx
   if (u == 0x80000000u) u = 0u;                       // -0.0 -> +0.0
   u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);     // monotone in value
   return ((unsigned long long)u << 32) | (unsigned long long)(0xFFFFFFFFu - idx);
+}
+
+__device__ __forceinline__ int key_index(unsigned long long key) {
+  return (int)(0xFFFFFFFFu - (unsigned int)key);
 }
 
 __device__ __forceinline__ unsigned long long umax64(unsigned long long x, unsigned long long y) {
@@ -88,13 +96,12 @@ __device__ __forceinline__ void see_chunk(Best& best, const uint4& w, unsigned i
   }
 }
 
+// The key of one (row, split) slice, returned to every thread.
 template <bool F32, bool VEC>
-__global__ __launch_bounds__(kScanThreads) void accept_scan(AcceptArgs a) {
+__device__ __forceinline__ unsigned long long scan_slice(const AcceptArgs& a, int row, int split) {
   constexpr int E = VEC ? (F32 ? 4 : 8) : 1;  // elements per chunk
   constexpr int L = kScanLoadsPerThread;
   const int tid = threadIdx.x;
-  const int row = blockIdx.x / a.nsplit;       // b * N + i
-  const int split = blockIdx.x % a.nsplit;
   const long long nchunks = ((long long)a.V + E - 1) / E;
   const long long c0 = (long long)split * a.cps;
   const long long c1 = c0 + a.cps < nchunks ? c0 + a.cps : nchunks;
@@ -136,67 +143,59 @@ __global__ __launch_bounds__(kScanThreads) void accept_scan(AcceptArgs a) {
   key = wave_max_u64(key);
   if ((tid & 63) == 0) red[tid >> 6] = key;
   __syncthreads();
-  if (tid == 0) {
-    key = red[0];
+  key = red[0];
 #pragma unroll
-    for (int k = 1; k < kScanThreads / 64; ++k) key = umax64(key, red[k]);
-    a.part[(size_t)row * a.nsplit + split] = key;
+  for (int k = 1; k < kScanThreads / 64; ++k) key = umax64(key, red[k]);
+  return key;
+}
+
+// Per-node LDS arrays of one sequence's acceptance (accept_lds_bytes).
+struct SeqLds {
+  int* tgt;
+  short *jmp0, *jmp1, *dep0, *dep1, *par;
+  unsigned char *ok0, *ok1;
+};
+
+__device__ __forceinline__ SeqLds seq_lds(unsigned char* base, int N) {
+  SeqLds l;
+  l.tgt = reinterpret_cast<int*>(base);
+  l.jmp0 = reinterpret_cast<short*>(base + 4 * (size_t)N);
+  l.jmp1 = l.jmp0 + N;
+  l.dep0 = l.jmp1 + N;
+  l.dep1 = l.dep0 + N;
+  l.par = l.dep1 + N;
+  l.ok0 = reinterpret_cast<unsigned char*>(l.par + N);
+  l.ok1 = l.ok0 + N;
+  return l;
+}
+
+__device__ __forceinline__ void load_nodes(const AcceptArgs& a, int b, int (&pv)[kMaxNodes / 256],
+                                           int (&dv)[kMaxNodes / 256]) {
+#pragma unroll
+  for (int k = 0; k < kMaxNodes / 256; ++k) {
+    const int i = threadIdx.x + 256 * k;
+    pv[k] = i < a.N ? a.parent[(size_t)b * a.N + i] : 0;
+    dv[k] = i < a.N ? a.draft[(size_t)b * a.N + i] : 0;
   }
 }
 
-__global__ __launch_bounds__(256) void accept_finish(AcceptArgs a) {
-  __shared__ short par[kMaxNodes];
-  __shared__ int tgt[kMaxNodes];
-  __shared__ unsigned long long rowkey[kMaxNodes];
-  __shared__ unsigned char ok[2][kMaxNodes];
-  __shared__ short jmp[2][kMaxNodes];
-  __shared__ short dep[2][kMaxNodes];
+// Acceptance of sequence b once l.tgt holds every node's prediction; pv and
+// dv hold parent and draft token of nodes tid + 256 k.  All 256 threads.
+__device__ __forceinline__ void accept_sequence(const AcceptArgs& a, int b, const SeqLds& l,
+                                                const int (&pv)[kMaxNodes / 256],
+                                                const int (&dv)[kMaxNodes / 256]) {
   __shared__ unsigned int best_key;
   const int tid = threadIdx.x;
-  const int b = blockIdx.x;
   const int N = a.N;
-  // parents and drafts of this thread's nodes: loads issued first
-  int pv[kMaxNodes / 256], dv[kMaxNodes / 256];
-#pragma unroll
-  for (int k = 0; k < kMaxNodes / 256; ++k) {
-    const int i = tid + 256 * k;
-    pv[k] = i < N ? a.parent[(size_t)b * N + i] : 0;
-    dv[k] = i < N ? a.draft[(size_t)b * N + i] : 0;
-  }
-  // the split keys of all rows, merged with LDS max; loads go out in
-  // batches of kFinishLoads so their latencies overlap
-  constexpr int kFinishLoads = 8;
-  for (int i = tid; i < N; i += 256) rowkey[i] = 0ull;
-  __syncthreads();
-  const size_t kbase = (size_t)b * N * a.nsplit;
-  const int nkeys = N * a.nsplit;
-  for (int idx0 = 0; idx0 < nkeys; idx0 += 256 * kFinishLoads) {
-    unsigned long long kv[kFinishLoads];
-#pragma unroll
-    for (int u = 0; u < kFinishLoads; ++u) {
-      const int idx = idx0 + 256 * u + tid;
-      kv[u] = idx < nkeys ? a.part[kbase + idx] : 0ull;
-    }
-#pragma unroll
-    for (int u = 0; u < kFinishLoads; ++u) {
-      const int idx = idx0 + 256 * u + tid;
-      if (idx < nkeys) atomicMax(&rowkey[idx / a.nsplit], kv[u]);
-    }
-  }
   int bad = 0;
-  __syncthreads();
 #pragma unroll
   for (int k = 0; k < kMaxNodes / 256; ++k) {
     const int i = tid + 256 * k;
     if (i >= N) break;
-    const unsigned long long key = rowkey[i];
-    const int t = (int)(0xFFFFFFFFu - (unsigned int)key);
-    tgt[i] = t;
-    if (a.tgt_out) a.tgt_out[(size_t)b * N + i] = t;
     const int p = pv[k];
     const int badi = (i == 0) ? (p != -1) : (p < 0 || p >= i);
     bad |= badi;
-    par[i] = (short)(badi ? 0 : p);
+    l.par[i] = (short)(badi ? 0 : p);
   }
   if (tid == 0) best_key = 0u;
   bad = __syncthreads_or(bad);
@@ -205,36 +204,41 @@ __global__ __launch_bounds__(256) void accept_finish(AcceptArgs a) {
     for (int k = 0; k < kMaxNodes / 256; ++k) {
       const int i = tid + 256 * k;
       if (i >= N) break;
-      if (i == 0) {
-        ok[0][0] = 1;
-        jmp[0][0] = 0;
-        dep[0][0] = 0;
-      } else {
-        ok[0][i] = dv[k] == tgt[par[i]];
-        jmp[0][i] = par[i];
-        dep[0][i] = 1;
-      }
+      // the root (par = -1) jumps to itself
+      const int p = i == 0 ? 0 : l.par[i];
+      l.ok0[i] = i == 0 ? 1 : dv[k] == l.tgt[p];
+      l.jmp0[i] = (short)p;
+      l.dep0[i] = i == 0 ? 0 : 1;
     }
     __syncthreads();
     // pointer jumping: afterwards jmp = root, dep = depth and ok = every
-    // node on the root path matches the prediction at its parent
-    int cur = 0, more;
+    // node on the root path matches the prediction at its parent.  Jumps
+    // double each round, so ceil(log2(kMaxNodes)) = 11 rounds reach the
+    // root from any node; the round cap only bounds the loop.
+    int cur = 0, more, rounds = 0;
     do {
-      const int nxt = cur ^ 1;
+      const short* jc = cur ? l.jmp1 : l.jmp0;
+      const short* dc = cur ? l.dep1 : l.dep0;
+      const unsigned char* oc = cur ? l.ok1 : l.ok0;
+      short* jn = cur ? l.jmp0 : l.jmp1;
+      short* dn = cur ? l.dep0 : l.dep1;
+      unsigned char* on = cur ? l.ok0 : l.ok1;
       more = 0;
       for (int i = tid; i < N; i += 256) {
-        const int j = jmp[cur][i];
-        ok[nxt][i] = ok[cur][i] & ok[cur][j];
-        dep[nxt][i] = dep[cur][i] + dep[cur][j];
-        jmp[nxt][i] = jmp[cur][j];
-        more |= jmp[nxt][i] != 0;
+        const int j = jc[i];
+        on[i] = oc[i] & oc[j];
+        dn[i] = dc[i] + dc[j];
+        jn[i] = jc[j];
+        more |= jc[j] != 0;
       }
-      cur = nxt;
-    } while (__syncthreads_or(more));
+      cur ^= 1;
+    } while (__syncthreads_or(more) && ++rounds < 16);
+    const short* dc = cur ? l.dep1 : l.dep0;
+    const unsigned char* oc = cur ? l.ok1 : l.ok0;
     unsigned int mk = 0u;
     for (int i = tid; i < N; i += 256)
-      if (ok[cur][i]) {
-        const unsigned int k = ((unsigned int)dep[cur][i] << 16) | (0xFFFFu - (unsigned int)i);
+      if (oc[i]) {
+        const unsigned int k = ((unsigned int)dc[i] << 16) | (0xFFFFu - (unsigned int)i);
         mk = mk > k ? mk : k;
       }
     atomicMax(&best_key, mk);  // LDS atomic, one per thread
@@ -251,11 +255,60 @@ __global__ __launch_bounds__(256) void accept_finish(AcceptArgs a) {
       int u = (int)(0xFFFFu - (bk & 0xFFFFu));
       for (int k = depth; k >= 0; --k) {
         pth[k] = u;
-        u = par[u];
+        u = l.par[u];
       }
     }
     a.accept_len[b] = len;
   }
+}
+
+// First kernel: the key of every (row, split).
+template <bool F32, bool VEC>
+__global__ __launch_bounds__(kScanThreads) void accept_scan(AcceptArgs a) {
+  const int row = blockIdx.x / a.nsplit;
+  const int split = blockIdx.x % a.nsplit;
+  const unsigned long long key = scan_slice<F32, VEC>(a, row, split);
+  if (threadIdx.x == 0) a.part[(size_t)row * a.nsplit + split] = key;
+}
+
+// Second kernel: one workgroup per sequence merges the split keys of its
+// rows (LDS max) and runs the acceptance.
+__global__ __launch_bounds__(256) void accept_finish(AcceptArgs a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+  const int tid = threadIdx.x;
+  const int b = blockIdx.x;
+  const int N = a.N;
+  int pv[kMaxNodes / 256], dv[kMaxNodes / 256];
+  load_nodes(a, b, pv, dv);
+  unsigned long long* rowkey = reinterpret_cast<unsigned long long*>(lds + accept_lds_bytes(N));
+  for (int i = tid; i < N; i += 256) rowkey[i] = 0ull;
+  __syncthreads();
+  // loads go out in batches of kFinishLoads so their latencies overlap
+  constexpr int kFinishLoads = 8;
+  const size_t kbase = (size_t)b * N * a.nsplit;
+  const int nkeys = N * a.nsplit;
+  for (int idx0 = 0; idx0 < nkeys; idx0 += 256 * kFinishLoads) {
+    unsigned long long kv[kFinishLoads];
+#pragma unroll
+    for (int u = 0; u < kFinishLoads; ++u) {
+      const int idx = idx0 + 256 * u + tid;
+      kv[u] = idx < nkeys ? a.part[kbase + idx] : 0ull;
+    }
+#pragma unroll
+    for (int u = 0; u < kFinishLoads; ++u) {
+      const int idx = idx0 + 256 * u + tid;
+      if (idx < nkeys) atomicMax(&rowkey[idx / a.nsplit], kv[u]);
+    }
+  }
+  __syncthreads();
+  const SeqLds l = seq_lds(lds, N);
+  for (int i = tid; i < N; i += 256) {
+    const int t = key_index(rowkey[i]);
+    l.tgt[i] = t;
+    if (a.tgt_out) a.tgt_out[(size_t)b * N + i] = t;
+  }
+  __syncthreads();
+  accept_sequence(a, b, l, pv, dv);
 }
 
 hipError_t launch_accept(const void* logits, int f32, const int32_t* draft, const int32_t* parent,
@@ -289,7 +342,8 @@ hipError_t launch_accept(const void* logits, int f32, const int32_t* draft, cons
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(accept_finish, dim3(B), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(accept_finish, dim3(B), dim3(256), accept_lds_bytes(N) + (size_t)N * 8, st,
+                     a);
   return hipGetLastError();
 }
 

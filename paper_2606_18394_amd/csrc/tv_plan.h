@@ -152,7 +152,7 @@ inline AttnPlan attn_plan(int B, int N, int Hq, int Hkv, int D, int Lmax) {
 }
 
 // Acceptance decomposition: a scan kernel runs one workgroup per (node row,
-// vocabulary split) and writes one 64-bit key per pair; a finish kernel runs
+// vocabulary split) and stores one 64-bit key per pair; a second kernel runs
 // one workgroup per sequence.  Splits give the scan >= ~2048 workgroups but
 // each thread gets at least one full round of kScanLoadsPerThread loads.
 constexpr int kAcceptMaxSplit = 16;
@@ -194,5 +194,11 @@ inline size_t accept_ws_bytes(int B, int N) {
   const long long rows = (long long)B * N;
   return (size_t)(rows * accept_split_cap(rows) * 8);
 }
+
+// LDS of the acceptance of one sequence of N nodes: per node the target
+// argmax (int), jump pointers and depths (2 x 2 short, double-buffered),
+// parent (short) and acceptance flags (2 bytes); the finish kernel adds the
+// merged 64-bit key per node.
+constexpr size_t accept_lds_bytes(int N) { return (size_t)N * 16 + 16; }
 
 }  // namespace tv

@@ -75,6 +75,8 @@ int main() {
         if ((long long)ap.nsplit * ap.chunks_per_split < nch) ok = false;
         if ((long long)(ap.nsplit - 1) * ap.chunks_per_split >= nch) ok = false;
         if (ap.nsplit < 1 || ap.nsplit > tv::kAcceptMaxSplit) ok = false;
+        if (ap.ws_bytes != (size_t)B * N * ap.nsplit * 8) ok = false;
+        if (tv::accept_lds_bytes(N) + (size_t)N * 8 > 64 * 1024) ok = false;
       }
     std::printf("%s B=%d N=%d Hq=%d Hkv=%d D=%d L=%d V=%d S=%d RB=%d nRB=%d grid=%d lds=%zu ws=%zu\n",
                 ok ? "OK" : "FAIL", B, N, Hq, Hkv, D, Lmax, V, p.S, p.RB, p.nRB, p.grid,

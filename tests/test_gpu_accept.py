@@ -119,3 +119,12 @@ def test_workspace_reuse_across_shapes():
                         (40, 7, 5, "f32"), (16, 64, 3000, "bf16")]:
         inp = _small(rng, B, N, V, dt)
         _compare(inp, oracle_draft_tokens(inp), 6)
+
+
+@pytest.mark.parametrize("B", [8, 9])
+def test_row_count_plans(B):
+    """Many sequences of the largest tree: the per-sequence workgroups
+    each merge 2048 rows of split keys."""
+    rng = np.random.default_rng(20 + B)
+    inp = _small(rng, B, 2048, 48, "bf16", depth=14, width=4)
+    _compare(inp, oracle_draft_tokens(inp), 16)

@@ -89,6 +89,7 @@ def test_fuzz_parity(case):
         nodes = _sample_nodes(trees[0], 64, rng)
         ref = oracle_attention(inp, nodes=nodes)
         err = np.abs(got[:, nodes] - ref).max()
+    print(f"fuzz case {case}: max abs err {err:.3e}", flush=True)
     assert err <= TOL, err
 
 

@@ -41,7 +41,24 @@ def parse():
     ap.add_argument("--replicas", type=int, default=0, help="0 = enough to exceed 2x the LLC")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    ap.add_argument("--copy-only", action="store_true",
+                    help="only run 10 plain device copies of 256 MiB (calibrates the HBM "
+                         "traffic counters: each copy reads and writes exactly 256 MiB)")
     return ap.parse_args()
+
+
+COPY_BYTES = 256 << 20
+
+
+def copy_only():
+    import torch
+    dev = torch.device("cuda:0")
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(10):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": COPY_BYTES, "copies": 10}), flush=True)
 
 
 def depths(parent_row):
@@ -124,6 +141,9 @@ def cpu_baseline(inp, w, draft, budget_s):
 
 def main():
     args = parse()
+    if args.copy_only:
+        copy_only()
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the tree-"
               f"verification path is built and timed for a single MI355X", file=sys.stderr)
@@ -244,12 +264,12 @@ def main():
             roof = {"bound": "mfma", "achieved": attn_flops / t / 1e12,
                     "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
         roof["kernel"] = "tree_verify_attention"
-        roof["traffic"] = measured_traffic("attention", w.name)
+        roof["traffic"] = measured_traffic("attn_main", w.name)
     else:
         t = ms_acc * 1e-3
         roof = {"bound": "hbm", "achieved": acc_bytes / t / 1e9, "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "kernel": "tree_accept",
-                "traffic": measured_traffic("accept", w.name)}
+                "traffic": measured_traffic("accept_scan", w.name)}
     roof["frac"] = roof["achieved"] / roof["peak"]
 
     cpu = None

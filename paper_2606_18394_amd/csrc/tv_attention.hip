@@ -217,48 +217,111 @@ __device__ __forceinline__ void issue_tile(const TreeSrc& src, const uint32_t (&
   }
 }
 
-// Sets the scores of keys a row cannot see to -inf: cache keys at or past
-// kv_len, and tree keys outside the row's ancestor-or-self set (one 32-bit
-// word of its bitmask per tile).
+// Where a tile's scores need masking: the cache tail and the tree tiles.
+struct MaskInfo {
+  int t, nct, kvl, ntt, g4;
+  const uint32_t* anc;
+};
+
+constexpr float kSlack = 8.f;  // log2 units a row's reference may lag its maximum
+
+// Steps of one 32-key tile for a wave's 32 rows (two 16-row tiles nt).
+//
+// scores: S^T = K Q^T on the matrix cores; lane (g4, l16) holds
+//   S^T[key 16*tt + 4*g4 + j][row 16*nt + l16].
+template <int D, int NT>
+__device__ __forceinline__ void tile_scores(const unsigned char* kt_lds, const bf16x8 (&qf)[NT][D / 32],
+                                            f32x4 (&sc)[2][NT], int g4, int l16) {
+  using TL = TileLayout<D>;
+  constexpr int NC = D / 32;
+  bf16x8 kf[2][NC];
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+    for (int cc = 0; cc < NC; ++cc)
+      kf[tt][cc] = *reinterpret_cast<const bf16x8*>(kt_lds + TL::off(16 * tt + l16, 4 * cc + g4));
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int cc = 0; cc < NC; ++cc)
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[tt][cc], qf[nt][cc], acc, 0, 0, 0);
+      sc[tt][nt] = acc;
+    }
+}
+
+// mask: -inf for cache keys at or past kv_len and for tree keys outside
+// the row's ancestor-or-self set (one 32-bit word of its bitmask per tile).
 template <int NT>
-__device__ __forceinline__ void mask_tile(f32x4 (&sc)[2][NT], int t, int nct, int kvl,
-                                          const uint32_t* anc, const int (&node_rel)[NT], int ntt,
-                                          int g4) {
-  if (t < nct) {
+__device__ __forceinline__ void tile_mask(f32x4 (&sc)[2][NT], const MaskInfo& mk,
+                                          const int (&node_rel)[NT]) {
+  if (mk.t < mk.nct) {
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const bool vis = t * kKeyTile + 16 * tt + 4 * g4 + j < kvl;
+        const bool vis = mk.t * kKeyTile + 16 * tt + 4 * mk.g4 + j < mk.kvl;
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt)
           if (!vis) sc[tt][nt][j] = -INFINITY;
       }
   } else {
-    const int word = t - nct;
+    const int word = mk.t - mk.nct;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const uint32_t bits = anc[node_rel[nt] * ntt + word];
+      const uint32_t bits = mk.anc[node_rel[nt] * mk.ntt + word];
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          if (!((bits >> (16 * tt + 4 * g4 + j)) & 1u)) sc[tt][nt][j] = -INFINITY;
+          if (!((bits >> (16 * tt + 4 * mk.g4 + j)) & 1u)) sc[tt][nt][j] = -INFINITY;
     }
   }
 }
 
-// Softmax weights of one 32-key tile (base 2, reference m per row) as the
-// bf16 P^T operand, their row sums (ones^T P^T) into lacc, and O^T += V^T
-// P^T with V^T from transposing LDS reads: lane (g4, l16) receives
-// V[key 4*g4 + j (+16)][16*dt + l16], the key order of the P^T operand.
-template <int D, int NT>
-__device__ __forceinline__ void softmax_pv(const f32x4 (&sc)[2][NT], const float (&m)[NT], float c,
-                                           const unsigned char* vt_lds, const bf16x8& ones,
-                                           f32x4 (&o)[D / 16][NT], f32x4 (&lacc)[NT], int g4,
-                                           int l16) {
-  using TL = TileLayout<D>;
-  bf16x8 pf[NT];
+// reference: online softmax in base 2 with a lazily moved reference.  A
+//   row's reference m (log2 units) only moves when one of its scores
+//   exceeds it by more than kSlack, so weights stay below 2^kSlack (far
+//   inside the fp32 and bf16 ranges) and rescaling is rare.  Each lane
+//   compares its raw scores with thr = (m + kSlack) / c; only a moving tile
+//   pays for exact row maxima, and rows that move rescale O and l.
+template <int DT, int NT>
+__device__ __forceinline__ void tile_reference(const f32x4 (&sc)[2][NT], float (&m)[NT],
+                                               float (&thr)[NT], f32x4 (&o)[DT][NT],
+                                               f32x4 (&lacc)[NT], float c, float inv_c) {
+  float mx[NT];
+  bool move = false;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    float v = fmaxf(fmaxf(sc[0][nt][0], sc[0][nt][1]), sc[0][nt][2]);
+    v = fmaxf(fmaxf(v, sc[0][nt][3]), sc[1][nt][0]);
+    v = fmaxf(fmaxf(v, sc[1][nt][1]), sc[1][nt][2]);
+    v = fmaxf(v, sc[1][nt][3]);
+    mx[nt] = v;
+    move |= v > thr[nt];
+  }
+  if (__any(move)) {
+    // rare: a row that has not moved keeps its scale; its m may still be -inf
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      mx[nt] = wave_max_across_groups(mx[nt]) * c;
+      const bool moved = mx[nt] > m[nt] + kSlack;
+      const float alpha = moved ? __builtin_amdgcn_exp2f(m[nt] - mx[nt]) : 1.f;
+      m[nt] = moved ? mx[nt] : m[nt];
+      thr[nt] = (m[nt] + kSlack) * inv_c;
+      lacc[nt] *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) o[dt][nt] *= alpha;
+    }
+  }
+}
+
+// weights: the bf16 P^T operand, exactly as it lies in the accumulators.
+template <int NT>
+__device__ __forceinline__ void tile_weights(const f32x4 (&sc)[2][NT], const float (&m)[NT], float c,
+                                             bf16x8 (&pf)[NT]) {
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const float mref = fmaxf(m[nt], -3.0e38f);  // rows with nothing visible yet: weights 0
@@ -267,8 +330,20 @@ __device__ __forceinline__ void softmax_pv(const f32x4 (&sc)[2][NT], const float
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         pf[nt][4 * tt + j] = (__bf16)__builtin_amdgcn_exp2f(fmaf(sc[tt][nt][j], c, -mref));
-    lacc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[nt], lacc[nt], 0, 0, 0);
   }
+}
+
+// values: row sums ones^T P^T into lacc (same rounded weights as the
+//   numerator) and O^T += V^T P^T with V^T from transposing LDS reads: lane
+//   (g4, l16) receives V[key 4*g4 + j (+16)][16*dt + l16], the key order of P^T.
+template <int D, int NT>
+__device__ __forceinline__ void tile_values(const unsigned char* vt_lds, const bf16x8 (&pf)[NT],
+                                            const bf16x8& ones, f32x4 (&o)[D / 16][NT],
+                                            f32x4 (&lacc)[NT], int g4, int l16) {
+  using TL = TileLayout<D>;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+    lacc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[nt], lacc[nt], 0, 0, 0);
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt) {
     const int rr = 4 * g4 + (l16 >> 2);
@@ -284,6 +359,22 @@ __device__ __forceinline__ void softmax_pv(const f32x4 (&sc)[2][NT], const float
     for (int nt = 0; nt < NT; ++nt)
       o[dt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[nt], o[dt][nt], 0, 0, 0);
   }
+}
+
+// The whole tile in order (the loop form without lookahead).
+template <int D, int NT, bool kMasked>
+__device__ __forceinline__ void attend_tile(const unsigned char* kt_lds, const bf16x8 (&qf)[NT][D / 32],
+                                            f32x4 (&o)[D / 16][NT], f32x4 (&lacc)[NT],
+                                            float (&m)[NT], float (&thr)[NT], const bf16x8& ones,
+                                            float c, float inv_c, const MaskInfo& mk,
+                                            const int (&node_rel)[NT], int g4, int l16) {
+  f32x4 sc[2][NT];
+  tile_scores<D, NT>(kt_lds, qf, sc, g4, l16);
+  if (kMasked) tile_mask<NT>(sc, mk, node_rel);
+  tile_reference<D / 16, NT>(sc, m, thr, o, lacc, c, inv_c);
+  bf16x8 pf[NT];
+  tile_weights<NT>(sc, m, c, pf);
+  tile_values<D, NT>(kt_lds + TileLayout<D>::kBytes, pf, ones, o, lacc, g4, l16);
 }
 
 // Merge of the chunk partials of one row block, run by the workgroup whose
@@ -507,91 +598,50 @@ void attn_main(AttnArgs a) {
     node_rel[nt] = (r < a.M ? r : a.M - 1) / a.G - i_lo;
   }
 
-  constexpr float kSlack = 8.f;
-  f32x4 sc[2][NT];
-  float mx[NT], thr[NT];
+  float thr[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) thr[nt] = -INFINITY;  // m = -inf: any visible score moves
-  const unsigned char* vt_lds = ring_ptr + TL::kBytes;
-  for (int i = 0; i < n_iter; ++i) {
-    {
-      const bool mine = i < n_mine;
-      if (WR > 1) {
-        // my DMAs of tile i are done once at most min(later tiles, NS-2)
-        // tiles' DMAs are outstanding; the barrier makes the whole group's
-        // visible and guarantees the slot of tile i-1 is no longer read
-        if (mine) wait_vm_dyn(min(n_mine - 1 - i, NS - 2) * PW);
-        __syncthreads();
-        if (i + NS - 1 < n_mine)
-          issue_tile<D, PW>(src, dma_off, wr, lane, t0 + wk + WK * (i + NS - 1),
-                            ring + ((i + NS - 1) % NS) * STAGE);
-      } else {
-        if (i + NS - 1 < n_mine)
-          issue_tile<D, PW>(src, dma_off, wr, lane, t0 + wk + WK * (i + NS - 1),
-                            ring + ((i + NS - 1) % NS) * STAGE);
-        if (mine) wait_vm_dyn(min(n_mine - 1 - i, NS - 1) * PW);
-      }
-      if (!mine) continue;
-      const int t = t0 + wk + WK * i;
-      const unsigned char* kt_lds = ring_ptr + (i % NS) * STAGE;
-      vt_lds = kt_lds + TL::kBytes;
-
-      // S^T tile: lane holds S^T[key 16*tt + 4*g4 + j][row 16*nt + l16]
-      bf16x8 kf[2][NC];
-#pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-        for (int c = 0; c < NC; ++c)
-          kf[tt][c] = *reinterpret_cast<const bf16x8*>(kt_lds + TL::off(16 * tt + l16, 4 * c + g4));
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-        for (int tt = 0; tt < 2; ++tt) {
-          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int c = 0; c < NC; ++c)
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[tt][c], qf[nt][c], acc, 0, 0, 0);
-          sc[tt][nt] = acc;
-        }
-
-      // masks: the cache tail and the tree tiles (full cache tiles skip this)
-      if (t >= nct || (t + 1) * kKeyTile > kvl)
-        mask_tile<NT>(sc, t, nct, kvl, anc, node_rel, ntt, g4);
-
-      // Online softmax in base 2 with a lazily moved reference: a row's
-      // reference m (log2 units) only moves when one of its scores exceeds
-      // it by more than kSlack, so weights stay below 2^kSlack (far inside
-      // the fp32 and bf16 ranges) and rescaling is rare.  Each lane compares
-      // its own raw scores with thr = (m + kSlack) / c; only a moving tile
-      // pays for exact row maxima.
-      bool move = false;
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        float v = fmaxf(fmaxf(sc[0][nt][0], sc[0][nt][1]), sc[0][nt][2]);
-        v = fmaxf(fmaxf(v, sc[0][nt][3]), sc[1][nt][0]);
-        v = fmaxf(fmaxf(v, sc[1][nt][1]), sc[1][nt][2]);
-        v = fmaxf(v, sc[1][nt][3]);
-        mx[nt] = v;
-        move |= v > thr[nt];
-      }
-      if (__any(move)) {
-        // rare: exact row maxima of the tile, move the references that
-        // need it and rescale their O and l (a row that has not moved keeps
-        // its scale; its m may still be -inf)
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          mx[nt] = wave_max_across_groups(mx[nt]) * a.c;
-          const bool moved = mx[nt] > m[nt] + kSlack;
-          const float alpha = moved ? __builtin_amdgcn_exp2f(m[nt] - mx[nt]) : 1.f;
-          m[nt] = moved ? mx[nt] : m[nt];
-          thr[nt] = (m[nt] + kSlack) / a.c;
-          lacc[nt] *= alpha;
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) o[dt][nt] *= alpha;
-        }
-      }
-      softmax_pv<D>(sc, m, a.c, vt_lds, ones, o, lacc, g4, l16);
+  const float inv_c = 1.f / a.c;
+  bf16x8 ones_v = ones;
+  asm volatile("" : "+v"(ones_v));  // keep it in registers, not rebuilt every tile
+  // Ring step of iteration i: wait for this key group's tile i and refill
+  // the ring.  With WR > 1 my DMAs of tile i are done once at most
+  // min(later tiles, NS-2) tiles' DMAs are outstanding; the barrier makes
+  // the whole group's visible and guarantees the slot of tile i-1 is no
+  // longer read.
+  auto ring_step = [&](int i) {
+    const bool mine = i < n_mine;
+    if (WR > 1) {
+      if (mine) wait_vm_dyn(min(n_mine - 1 - i, NS - 2) * PW);
+      __syncthreads();
+      if (i + NS - 1 < n_mine)
+        issue_tile<D, PW>(src, dma_off, wr, lane, t0 + wk + WK * (i + NS - 1),
+                          ring + ((i + NS - 1) % NS) * STAGE);
+    } else {
+      if (i + NS - 1 < n_mine)
+        issue_tile<D, PW>(src, dma_off, wr, lane, t0 + wk + WK * (i + NS - 1),
+                          ring + ((i + NS - 1) % NS) * STAGE);
+      if (mine) wait_vm_dyn(min(n_mine - 1 - i, NS - 1) * PW);
     }
+  };
+  // Full cache tiles first, without masking; the tiles that need a mask
+  // (the cache tail, then the tree tiles) all come after them.
+  int i = 0;
+  for (; i < n_iter; ++i) {
+    ring_step(i);
+    const int t = t0 + wk + WK * i;
+    if (i >= n_mine || t >= nct || (t + 1) * kKeyTile > kvl) break;
+    const MaskInfo mk{t, nct, kvl, ntt, g4, anc};
+    attend_tile<D, NT, false>(ring_ptr + (i % NS) * STAGE, qf, o, lacc, m, thr, ones_v, a.c, inv_c,
+                              mk, node_rel, g4, l16);
+  }
+  for (bool stepped = true; i < n_iter; ++i, stepped = false) {
+    if (!stepped) ring_step(i);
+    if (i >= n_mine) continue;
+    const int t = t0 + wk + WK * i;
+    const MaskInfo mk{t, nct, kvl, ntt, g4, anc};
+    attend_tile<D, NT, true>(ring_ptr + (i % NS) * STAGE, qf, o, lacc, m, thr, ones_v, a.c, inv_c,
+                             mk, node_rel, g4, l16);
   }
 
   float lsum[NT];

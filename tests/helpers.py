@@ -64,7 +64,7 @@ def oracle_draft_tokens(inp: dict) -> np.ndarray:
     return synth.draft_tokens(inp["parent"], tgt, inp["match"], inp["rand_tok"])
 
 
-def gpu_accept(inp: dict, draft: np.ndarray, Dmax: int, canary: int = 0):
+def gpu_accept(inp: dict, draft: np.ndarray, Dmax: int, canary: int = 0, workspace=None):
     from paper_2606_18394_amd import tree_accept
     B, N = inp["parent"].shape
     lbuf = torch.full((B + 2 * canary,), -77, dtype=torch.int32, device="cuda")
@@ -74,7 +74,7 @@ def gpu_accept(inp: dict, draft: np.ndarray, Dmax: int, canary: int = 0):
     path = pbuf[canary:canary + B * Dmax].view(B, Dmax)
     tgt = tbuf[canary:canary + B * N].view(B, N)
     tree_accept(dev_logits(inp), dev_i32(draft), dev_i32(inp["parent"]), Dmax,
-                accept_len=ln, path=path, tgt_argmax=tgt)
+                accept_len=ln, path=path, tgt_argmax=tgt, workspace_tensor=workspace)
     torch.cuda.synchronize()
     ok = True
     if canary:

@@ -10,8 +10,8 @@ from helpers import gpu_accept, host_logits_f64, oracle_draft_tokens
 pytestmark = pytest.mark.gpu
 
 
-def _compare(inp, draft, Dmax, canary=0):
-    ln, path, tgt, ok = gpu_accept(inp, draft, Dmax, canary=canary)
+def _compare(inp, draft, Dmax, canary=0, workspace=None):
+    ln, path, tgt, ok = gpu_accept(inp, draft, Dmax, canary=canary, workspace=workspace)
     rl, rp, rt = oracle.tree_accept(host_logits_f64(inp), draft, inp["parent"], Dmax)
     np.testing.assert_array_equal(tgt, rt)
     np.testing.assert_array_equal(ln, rl)
@@ -112,13 +112,20 @@ def test_max_nodes_chain():
 
 
 def test_workspace_reuse_across_shapes():
-    """One workspace serves calls of different shapes back to back: every
-    call leaves it zeroed again."""
+    """One workspace serves calls of different shapes back to back, with
+    exact results every time."""
+    import torch
+    from paper_2606_18394_amd.binding import load_library
+    lib = load_library()
     rng = np.random.default_rng(8)
-    for B, N, V, dt in [(16, 64, 3000, "bf16"), (300, 1, 777, "f32"), (2, 500, 9000, "bf16"),
-                        (40, 7, 5, "f32"), (16, 64, 3000, "bf16")]:
+    shapes = [(16, 64, 3000, "bf16"), (300, 1, 777, "f32"), (2, 500, 9000, "bf16"),
+              (40, 7, 5, "f32"), (100, 3, 50, "bf16"), (16, 64, 3000, "bf16")]
+    size = max(lib.tv_tree_accept_workspace(B, N, V) for B, N, V, _ in shapes)
+    ws = torch.zeros(size, dtype=torch.uint8, device="cuda")
+    for B, N, V, dt in shapes:
         inp = _small(rng, B, N, V, dt)
-        _compare(inp, oracle_draft_tokens(inp), 6)
+        print(f"accept reuse B={B} N={N} V={V} {dt}", flush=True)
+        _compare(inp, oracle_draft_tokens(inp), 6, workspace=ws)
 
 
 @pytest.mark.parametrize("B", [8, 9])

@@ -10,15 +10,19 @@ Contents
                      attention equations).
   tree_accept     -- per-node target argmax and greedy deepest-path
                      acceptance (Sec. 2.4 greedy rule; App. E).
-  brute           -- pure-Python loop versions of both for tiny inputs, used
-                     only to pin the two functions above.
+  draft_topw,     -- budgeted tree drafting: top-W candidates per draft depth
+  build_tree         and best-first expansion by accumulated draft
+                     log-probability (Sec. 2.4 parallel tree drafting; Alg. 1).
+  brute           -- pure-Python loop versions for tiny inputs, used only to
+                     pin the functions above.
 
-Parity is pinned for both functions (brute force, closed forms, invariants
+Parity is pinned for every function (brute force, closed forms, invariants
 and library special cases in the tests).
 """
 from .tree_attention import (decode_bf16, tree_structure, full_mask,
                              tree_attention)
 from .tree_accept import target_argmax, tree_accept
+from .tree_build import draft_topw, build_tree
 
 __all__ = ["decode_bf16", "tree_structure", "full_mask", "tree_attention",
-           "target_argmax", "tree_accept"]
+           "target_argmax", "tree_accept", "draft_topw", "build_tree"]

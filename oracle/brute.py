@@ -6,11 +6,16 @@ Independent constructions used to pin the oracle:
     the softmax use Python floats and math.exp, no numpy;
   * acceptance: every root-to-node path is enumerated explicitly and checked
     token by token against a loop argmax; the best path is chosen by
-    (length, then lowest end node).
+    (length, then lowest end node);
+  * top-W: Python sort on (value, index) and an exactly summed log-sum-exp;
+  * tree building: the full W-ary tree is enumerated and its nodes visited in
+    descending score order, with no priority queue.
 """
 from __future__ import annotations
 
 import math
+
+import numpy as np
 
 
 def _valid_tree(par):
@@ -100,3 +105,56 @@ def accept(logits, draft_tok, parent, Dmax):
             lens.append(len(best))
             paths.append(best + [-1] * (Dmax - len(best)))
     return lens, paths, tgts
+
+
+def topw(logits_row, W):
+    """Pure-Python top-W of one row: tokens by (value desc, index asc) and
+    their log-probabilities from an exactly summed log-sum-exp."""
+    xs = [float(x) for x in logits_row]
+    m = max(xs)
+    lse = m + math.log(math.fsum(math.exp(x - m) for x in xs))
+    order = sorted(range(len(xs)), key=lambda i: (-xs[i], i))[:W]
+    return order, [xs[i] - lse for i in order]
+
+
+def tree_in_score_order(tok, logp, budget):
+    """The tree of best-first expansion without a priority queue, for one
+    sequence whose accumulated scores are all distinct and whose
+    log-probabilities are negative.
+
+    Every node of the full W-ary tree of depth Nd has a fixed score (float32
+    accumulation along its path).  Because a child scores below its parent,
+    best-first pops nodes in plain descending score order; each popped node
+    above the maximum depth appends its W children in candidate order until
+    the budget is reached.  Returns (parent, token, depth, score) lists.
+    """
+    Nd, W = len(tok), len(tok[0])
+    f32 = np.float32
+    # all nodes of the full tree, keyed by their path of candidate ranks
+    full = {(): f32(0.0)}
+    frontier = [()]
+    for d in range(Nd):
+        nxt = []
+        for p in frontier:
+            for k in range(W):
+                full[p + (k,)] = f32(full[p] + f32(logp[d][k]))
+                nxt.append(p + (k,))
+        frontier = nxt
+    order = sorted((p for p in full if len(p) < Nd), key=lambda p: -float(full[p]))
+    index = {(): 0}
+    parent, token, depth, score = [-1], [-1], [0], [f32(0.0)]
+    for p in order:
+        if len(parent) == budget:
+            break
+        if p not in index:      # not added: the budget ran out before it
+            break
+        for k in range(W):
+            if len(parent) == budget:
+                break
+            c = p + (k,)
+            index[c] = len(parent)
+            parent.append(index[p])
+            token.append(int(tok[len(p)][k]))
+            depth.append(len(c))
+            score.append(full[c])
+    return parent, token, depth, score

@@ -150,7 +150,7 @@ def main():
         sys.exit(2)
 
     import torch
-    from paper_2606_18394_amd import synth, tree_accept, tree_verify_attention
+    from paper_2606_18394_amd import build_tree, draft_topw, synth, tree_accept, tree_verify_attention
     from paper_2606_18394_amd.binding import load_library
 
     load_library()
@@ -203,6 +203,22 @@ def main():
         attn(r)
         accept(r)
 
+    # Tree drafting (the step that builds the verified trees): top-W of the
+    # draft logits per draft depth, then the best-first tree; timed apart,
+    # it is not part of the verification step.
+    Wd = synth.draft_width(w)
+    dl = synth.draft_logits(w)
+    dlog0 = torch.from_numpy(dl).to(dev) if w.logits_dtype == "f32" else bf(dl)
+    dlogs = [dlog0] + [dlog0.clone() for _ in range(R - 1)]
+    dtok = torch.empty(w.B, w.depth, Wd, dtype=torch.int32, device=dev)
+    dlp = torch.empty(w.B, w.depth, Wd, dtype=torch.float32, device=dev)
+
+    def topw(r):
+        draft_topw(dlogs[r], Wd, tok=dtok, logp=dlp)
+
+    def build(r):
+        build_tree(dtok, dlp, w.N)
+
     # Launches are recorded once into HIP graphs (one graph runs the R
     # replicas in turn, R more graphs run one replica each) so the timed
     # region measures the GPU, not Python's launch overhead.
@@ -222,7 +238,11 @@ def main():
         return g
 
     graphs = {}
-    for name, fn in [("step", step), ("attn", attn), ("accept", accept)]:
+    for s in range(2):
+        topw(s % R)
+        build(s % R)
+    for name, fn in [("step", step), ("attn", attn), ("accept", accept), ("topw", topw),
+                     ("build", build)]:
         graphs[name] = (capture(fn, range(R)), [capture(fn, [r]) for r in range(R)])
     torch.cuda.synchronize()
     print(f"[bench] {w.name}: {R} replicas of {per_rep / 2**20:.1f} MiB; warmup done, "
@@ -246,6 +266,8 @@ def main():
     ms_step = timed("step", args.steps)
     ms_attn = timed("attn", args.steps)
     ms_acc = timed("accept", args.steps)
+    ms_topw = timed("topw", args.steps)
+    ms_build = timed("build", args.steps)
     print(f"[bench] step {ms_step * 1e3:.2f} us, attention {ms_attn * 1e3:.2f} us, "
           f"accept {ms_acc * 1e3:.2f} us", file=sys.stderr, flush=True)
 
@@ -300,7 +322,9 @@ def main():
                    "attention_flops": attn_flops, "accept_bytes": acc_bytes,
                    "attention_GBps": attn_bytes / (ms_attn * 1e-3) / 1e9,
                    "attention_TFLOPs": attn_flops / (ms_attn * 1e-3) / 1e12,
-                   "accept_GBps": acc_bytes / (ms_acc * 1e-3) / 1e9},
+                   "accept_GBps": acc_bytes / (ms_acc * 1e-3) / 1e9,
+                   "draft_topw_us": ms_topw * 1e3, "build_tree_us": ms_build * 1e3,
+                   "draft": {"depth": w.depth, "width": Wd, "budget": w.N}},
     }
     print(json.dumps(line), flush=True)
 

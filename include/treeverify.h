@@ -137,6 +137,61 @@ int tv_tree_accept(const void* logits, int logits_dtype,
                    int32_t* tgt_argmax, void* workspace,
                    size_t workspace_bytes, hipStream_t stream);
 
+/* ---- Budgeted tree drafting (the step before verification) ------------ */
+
+/* Largest branching width W and draft depth the drafting calls accept. */
+#define TV_MAX_WIDTH 16
+#define TV_MAX_DRAFT_DEPTH 64
+
+/* Workspace bytes tv_draft_topw needs for these sizes (0 when invalid). */
+size_t tv_draft_topw_workspace(int B, int Nd, int V);
+
+/*
+ * Candidate children per draft depth (Sec. 2.4, parallel tree drafting: one
+ * draft-head pass gives logits for every draft depth, of which the top-W
+ * tokens and their log-probabilities are extracted; App. E uses k = W).
+ *
+ *   logits [B, Nd, V] bf16 or fp32  draft logits, row (b, d) for depth d+1
+ *   tok    [B, Nd, W] int32  out: the W largest logits of each row, in
+ *                            decreasing order, equal values by lower index
+ *   logp   [B, Nd, W] fp32   out: their log-probabilities, logit minus the
+ *                            row's log-sum-exp (computed in fp32)
+ *
+ * Requirements: 1 <= W <= min(V, TV_MAX_WIDTH), 1 <= Nd <= TV_MAX_DRAFT_DEPTH,
+ * B >= 1; logits finite.
+ */
+int tv_draft_topw(const void* logits, int logits_dtype, int B, int Nd, int V, int W,
+                  int32_t* tok, float* logp, void* workspace, size_t workspace_bytes,
+                  hipStream_t stream);
+
+/*
+ * Best-first tree construction under a node budget (Alg. 1 with the
+ * accumulated draft log-probability score of Sec. 2.4).
+ *
+ * Node 0 is the root (depth 0, score 0, token root_tok[b], or -1 when
+ * root_tok is NULL).  Repeatedly the open node of highest score (equal
+ * scores: lower node index) is taken; unless it is at depth Nd it gets up
+ * to W children, child k of a depth-d node carrying tok[b, d, k] and score
+ * fp32(score + logp[b, d, k]), numbered in creation order, until the tree
+ * holds `budget` nodes or no open node is left.
+ *
+ *   tok, logp [B, Nd, W]   candidates as produced by tv_draft_topw
+ *   root_tok  [B] int32    or NULL
+ *   parent    [B, budget] int32  out: parent index, -1 for the root
+ *   token     [B, budget] int32  out
+ *   depth     [B, budget] int32  out
+ *   score     [B, budget] fp32   out, or NULL
+ *   n_nodes   [B] int32          out: nodes built (<= budget)
+ * Slots at or beyond n_nodes[b] hold parent = token = depth = -1 and score
+ * -inf.  The parent/token arrays of a sequence with n_nodes[b] = budget are
+ * directly the parent and draft_tok inputs of the verification calls.
+ * Requirements: 1 <= budget <= TV_MAX_NODES, 1 <= W <= TV_MAX_WIDTH,
+ * 1 <= Nd <= TV_MAX_DRAFT_DEPTH, B >= 1; logp finite.  No workspace.
+ */
+int tv_build_tree(const int32_t* tok, const float* logp, const int32_t* root_tok, int B,
+                  int Nd, int W, int budget, int32_t* parent, int32_t* token, int32_t* depth,
+                  float* score, int32_t* n_nodes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

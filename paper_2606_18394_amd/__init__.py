@@ -6,7 +6,7 @@ Importing the package loads nothing; the first call loads libtreeverify.so
 and raises if it is missing.
 """
 
-__all__ = ["tree_verify_attention", "tree_accept", "load_library"]
+__all__ = ["tree_verify_attention", "tree_accept", "draft_topw", "build_tree", "load_library"]
 
 
 def tree_verify_attention(*args, **kwargs):
@@ -16,6 +16,16 @@ def tree_verify_attention(*args, **kwargs):
 
 def tree_accept(*args, **kwargs):
     from .binding import tree_accept as f
+    return f(*args, **kwargs)
+
+
+def draft_topw(*args, **kwargs):
+    from .binding import draft_topw as f
+    return f(*args, **kwargs)
+
+
+def build_tree(*args, **kwargs):
+    from .binding import build_tree as f
     return f(*args, **kwargs)
 
 

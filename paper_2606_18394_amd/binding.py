@@ -52,6 +52,12 @@ def load_library() -> ctypes.CDLL:
         lib.tv_tree_accept.restype = ci
         lib.tv_tree_accept.argtypes = (
             [vp, ci, i32p, i32p] + [ci] * 4 + [i32p, i32p, i32p, vp, sz, vp])
+        lib.tv_draft_topw_workspace.restype = sz
+        lib.tv_draft_topw_workspace.argtypes = [ci] * 3
+        lib.tv_draft_topw.restype = ci
+        lib.tv_draft_topw.argtypes = [vp] + [ci] * 5 + [i32p, vp, vp, sz, vp]
+        lib.tv_build_tree.restype = ci
+        lib.tv_build_tree.argtypes = [i32p, vp, i32p] + [ci] * 4 + [i32p, i32p, i32p, vp, i32p, vp]
         _lib = lib
         return lib
 
@@ -162,3 +168,56 @@ def tree_accept(logits, draft_tok, parent, Dmax, accept_len=None, path=None,
         _ptr(accept_len), _ptr(path), _ptr(tgt_argmax), _ptr(ws), ws.numel(),
         ctypes.c_void_p(stream)))
     return accept_len, path, tgt_argmax
+
+
+def draft_topw(logits, W, tok=None, logp=None, workspace_tensor=None):
+    """(tok [B,Nd,W] int32, logp [B,Nd,W] fp32): the W largest draft logits
+    of every draft depth and their log-probabilities.  logits [B,Nd,V]
+    bfloat16 or float32."""
+    lib = load_library()
+    B, Nd, V = logits.shape
+    dev = logits.device
+    if logits.dtype == torch.bfloat16:
+        dt = TV_BF16
+    elif logits.dtype == torch.float32:
+        dt = TV_F32
+    else:
+        raise TypeError("logits must be bfloat16 or float32")
+    _need(logits, "logits", logits.dtype, device=dev)
+    if tok is None:
+        tok = torch.empty(B, Nd, W, dtype=torch.int32, device=dev)
+    if logp is None:
+        logp = torch.empty(B, Nd, W, dtype=torch.float32, device=dev)
+    _need(tok, "tok", torch.int32, (B, Nd, W), dev)
+    _need(logp, "logp", torch.float32, (B, Nd, W), dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    need = lib.tv_draft_topw_workspace(B, Nd, V)
+    if need == 0:
+        _check(-2)
+    ws = workspace_tensor if workspace_tensor is not None else workspace("topw", need, dev, stream)
+    _check(lib.tv_draft_topw(_ptr(logits), dt, B, Nd, V, int(W), _ptr(tok), _ptr(logp),
+                             _ptr(ws), ws.numel(), ctypes.c_void_p(stream)))
+    return tok, logp
+
+
+def build_tree(tok, logp, budget, root_tok=None, with_score=True):
+    """Best-first tree under a node budget from per-depth candidates
+    (tok [B,Nd,W] int32, logp [B,Nd,W] fp32).  Returns (parent, token,
+    depth, score or None, n_nodes); parent/token/depth are [B, budget]."""
+    lib = load_library()
+    B, Nd, W = tok.shape
+    dev = tok.device
+    _need(tok, "tok", torch.int32, (B, Nd, W), dev)
+    _need(logp, "logp", torch.float32, (B, Nd, W), dev)
+    if root_tok is not None:
+        _need(root_tok, "root_tok", torch.int32, (B,), dev)
+    parent = torch.empty(B, budget, dtype=torch.int32, device=dev)
+    token = torch.empty(B, budget, dtype=torch.int32, device=dev)
+    depth = torch.empty(B, budget, dtype=torch.int32, device=dev)
+    score = torch.empty(B, budget, dtype=torch.float32, device=dev) if with_score else None
+    n_nodes = torch.empty(B, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    _check(lib.tv_build_tree(_ptr(tok), _ptr(logp), _ptr(root_tok), B, Nd, W, int(budget),
+                             _ptr(parent), _ptr(token), _ptr(depth), _ptr(score), _ptr(n_nodes),
+                             ctypes.c_void_p(stream)))
+    return parent, token, depth, score, n_nodes

@@ -16,7 +16,14 @@ hipError_t launch_attention(const void* q, const void* kc, const void* vc, const
 hipError_t launch_accept(const void* logits, int f32, const int32_t* draft, const int32_t* parent,
                          int B, int N, int V, int Dmax, int32_t* accept_len, int32_t* path,
                          int32_t* tgt_out, void* ws, hipStream_t st);
+hipError_t launch_topw(const void* logits, int f32, int B, int Nd, int V, int W, int32_t* tok,
+                       float* logp, void* ws, hipStream_t st);
+hipError_t launch_build_tree(const int32_t* tok, const float* logp, const int32_t* root_tok, int B,
+                             int Nd, int W, int budget, int32_t* parent, int32_t* token,
+                             int32_t* depth, float* score, int32_t* n_nodes, hipStream_t st);
 }  // namespace tv
+
+static_assert(TV_MAX_WIDTH == tv::kTopwMax, "width limit mismatch");
 
 static bool misaligned(const void* p) { return ((uintptr_t)p & 15u) != 0; }
 
@@ -34,6 +41,13 @@ static int check_accept_sizes(int B, int N, int V, int Dmax) {
   if (B < 1 || N < 1 || V < 1 || Dmax < 1) return TV_ERR_SHAPE;
   if (N > TV_MAX_NODES) return TV_ERR_UNSUPPORTED;
   if ((long long)B * N > (1ll << 24)) return TV_ERR_UNSUPPORTED;
+  return TV_OK;
+}
+
+static int check_draft_sizes(int B, int Nd, int W) {
+  if (B < 1 || Nd < 1 || W < 1) return TV_ERR_SHAPE;
+  if (W > TV_MAX_WIDTH || Nd > TV_MAX_DRAFT_DEPTH) return TV_ERR_UNSUPPORTED;
+  if ((long long)B * Nd > (1ll << 24)) return TV_ERR_UNSUPPORTED;
   return TV_OK;
 }
 
@@ -99,6 +113,39 @@ int tv_tree_accept(const void* logits, int logits_dtype, const int32_t* draft_to
   if (misaligned(workspace)) return TV_ERR_ALIGN;
   hipError_t e = tv::launch_accept(logits, logits_dtype == TV_F32, draft_tok, parent, B, N, V,
                                    Dmax, accept_len, path, tgt_argmax, workspace, stream);
+  return e == hipSuccess ? TV_OK : TV_ERR_LAUNCH;
+}
+
+size_t tv_draft_topw_workspace(int B, int Nd, int V) {
+  if (check_draft_sizes(B, Nd, 1) != TV_OK || V < 1) return 0;
+  return tv::topw_ws_bytes(B, Nd);
+}
+
+int tv_draft_topw(const void* logits, int logits_dtype, int B, int Nd, int V, int W,
+                  int32_t* tok, float* logp, void* workspace, size_t workspace_bytes,
+                  hipStream_t stream) {
+  int rc = check_draft_sizes(B, Nd, W);
+  if (rc != TV_OK) return rc;
+  if (V < 1 || W > V) return TV_ERR_SHAPE;
+  if (logits_dtype != TV_BF16 && logits_dtype != TV_F32) return TV_ERR_DTYPE;
+  if (!logits || !tok || !logp) return TV_ERR_NULL;
+  if (!workspace || workspace_bytes < tv::topw_ws_bytes(B, Nd)) return TV_ERR_WORKSPACE;
+  if (misaligned(workspace)) return TV_ERR_ALIGN;
+  hipError_t e = tv::launch_topw(logits, logits_dtype == TV_F32, B, Nd, V, W, tok, logp,
+                                 workspace, stream);
+  return e == hipSuccess ? TV_OK : TV_ERR_LAUNCH;
+}
+
+int tv_build_tree(const int32_t* tok, const float* logp, const int32_t* root_tok, int B,
+                  int Nd, int W, int budget, int32_t* parent, int32_t* token, int32_t* depth,
+                  float* score, int32_t* n_nodes, hipStream_t stream) {
+  int rc = check_draft_sizes(B, Nd, W);
+  if (rc != TV_OK) return rc;
+  if (budget < 1) return TV_ERR_SHAPE;
+  if (budget > TV_MAX_NODES) return TV_ERR_UNSUPPORTED;
+  if (!tok || !logp || !parent || !token || !depth || !n_nodes) return TV_ERR_NULL;
+  hipError_t e = tv::launch_build_tree(tok, logp, root_tok, B, Nd, W, budget, parent, token,
+                                       depth, score, n_nodes, stream);
   return e == hipSuccess ? TV_OK : TV_ERR_LAUNCH;
 }
 

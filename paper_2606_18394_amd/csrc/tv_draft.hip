@@ -1,0 +1,453 @@
+// Budgeted tree drafting for CDNA4 (gfx950): the step that produces the
+// trees the verification kernels consume (Sec. 2.4, parallel tree drafting;
+// Alg. 1; App. E).
+//
+// topw: candidate children per draft depth.  One draft-head pass gives a
+//   logit row per draft depth; its W largest entries (equal values: lower
+//   token id) and their log-probabilities (logit minus the row's
+//   log-sum-exp) are the children offered to every node one depth above.
+//   Scan: one workgroup per (row, vocabulary split) streams its slice with
+//   16-byte loads, keeps a running (max, sum of exponentials) per thread,
+//   updated once per batch of loads, and a sorted top-W list in registers;
+//   the workgroup merges the lists by W rounds of (value, lower index)
+//   argmax.  Finish: one wave per row merges the splits.
+//
+// build: best-first expansion under a node budget, one wave per sequence.
+//   Node i lives in LDS and is owned by lane i % 64, which caches the best
+//   open node it owns; a pop is a wave argmax of (score, lower index) over
+//   those caches, the winning node's owner rescans its slots, and the up to
+//   W children go to W consecutive lanes.  Scores are fp32 sums
+//   parent + log-probability, the comparisons that decide the tree.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "tv_plan.h"
+
+namespace tv {
+
+// ---------------------------------------------------------------- topw
+
+struct TopwArgs {
+  const void* logits;
+  int32_t* tok;
+  float* logp;
+  unsigned char* part;  // per (row, split): m, s, then kTopwMax (value, index)
+  int rows, V, W, nsplit;
+  long long cps;        // chunks per split
+};
+
+struct TopwPart {
+  float m, s;
+  float v[kTopwMax];
+  int i[kTopwMax];
+};
+
+// Sorted list of the K best (value, index) pairs seen, decreasing, K a
+// compile-time length >= W (a list cut at a runtime W would be indexed
+// dynamically and live in scratch memory).  Insertion is a branch-free
+// bubble pass.  Within a thread, elements arrive in increasing index order,
+// so an equal value never displaces an earlier entry (strict comparison).
+template <int K>
+struct TopList {
+  float v[K];
+  int i[K];
+  __device__ __forceinline__ void init() {
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      v[k] = -INFINITY;
+      i[k] = 0x7FFFFFFF;
+    }
+  }
+  __device__ __forceinline__ float thr() const { return v[K - 1]; }
+  __device__ __forceinline__ void insert(float x, int idx) {
+    float cv = x;
+    int ci = idx;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const bool sw = cv > v[k];
+      const float nv = sw ? cv : v[k];
+      const int ni = sw ? ci : i[k];
+      cv = sw ? v[k] : cv;
+      ci = sw ? i[k] : ci;
+      v[k] = nv;
+      i[k] = ni;
+    }
+  }
+  // drop the head (it was taken by the merge)
+  __device__ __forceinline__ void pop() {
+#pragma unroll
+    for (int k = 0; k < K - 1; ++k) {
+      v[k] = v[k + 1];
+      i[k] = i[k + 1];
+    }
+    v[K - 1] = -INFINITY;
+    i[K - 1] = 0x7FFFFFFF;
+  }
+};
+
+__device__ __forceinline__ bool better(float a, int ia, float b, int ib) {
+  return a > b || (a == b && ia < ib);
+}
+
+// Wave-wide best (value, index), with a payload that travels with it;
+// every lane receives the result.  Within each row of 16 lanes: DPP
+// exchanges with lane ^ 1 and lane ^ 2 (quad permutes), then mirrored lanes
+// of each half-row and of the row, after which all 16 lanes hold the row's
+// best; the four rows are then read out as scalars.  (Cross-lane shuffles
+// would go through the LDS crossbar, one round trip per step.)
+template <int CTRL>
+__device__ __forceinline__ int dpp(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ void dpp_best_step(float& v, int& i, int& p) {
+  const float ov = __int_as_float(dpp<CTRL>(__float_as_int(v)));
+  const int oi = dpp<CTRL>(i), op = dpp<CTRL>(p);
+  if (better(ov, oi, v, i)) {
+    v = ov;
+    i = oi;
+    p = op;
+  }
+}
+__device__ __forceinline__ void wave_best(float& v, int& i, int& p) {
+  dpp_best_step<0xB1>(v, i, p);   // quad_perm(1,0,3,2): lane ^ 1
+  dpp_best_step<0x4E>(v, i, p);   // quad_perm(2,3,0,1): lane ^ 2
+  dpp_best_step<0x141>(v, i, p);  // row_half_mirror: quads of each half-row
+  dpp_best_step<0x140>(v, i, p);  // row_mirror: the two halves of the row
+  float gv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  int gi = __builtin_amdgcn_readlane(i, 0), gp = __builtin_amdgcn_readlane(p, 0);
+#pragma unroll
+  for (int r = 16; r < 64; r += 16) {
+    const float rv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), r));
+    const int ri = __builtin_amdgcn_readlane(i, r), rp = __builtin_amdgcn_readlane(p, r);
+    if (better(rv, ri, gv, gi)) {
+      gv = rv;
+      gi = ri;
+      gp = rp;
+    }
+  }
+  v = gv;
+  i = gi;
+  p = gp;
+}
+__device__ __forceinline__ void wave_best(float& v, int& i) {
+  int p = 0;
+  wave_best(v, i, p);
+}
+
+// (m, s) with s = sum exp(x - m): merge of two such states
+__device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2) {
+  const float mn = fmaxf(m, m2);
+  if (mn == -INFINITY) return;
+  s = s * __expf(m - mn) + s2 * __expf(m2 - mn);
+  m = mn;
+}
+
+template <bool F32, bool VEC, int K>
+__global__ __launch_bounds__(kScanThreads) void topw_scan(TopwArgs a) {
+  constexpr int E = VEC ? (F32 ? 4 : 8) : 1;  // elements per chunk
+  constexpr int L = kScanLoadsPerThread;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int row = blockIdx.x / a.nsplit;
+  const int split = blockIdx.x % a.nsplit;
+  const long long nchunks = ((long long)a.V + E - 1) / E;
+  const long long c0 = (long long)split * a.cps;
+  const long long c1 = c0 + a.cps < nchunks ? c0 + a.cps : nchunks;
+  const int W = a.W;
+
+  TopList<K> top;
+  top.init();
+  float m = -INFINITY, s = 0.f;
+  const char* rowp = (const char*)a.logits + (size_t)row * a.V * (F32 ? 4 : 2);
+  for (long long c = c0 + tid; c < c1; c += (long long)L * kScanThreads) {
+    float x[L][E];
+#pragma unroll
+    for (int u = 0; u < L; ++u) {
+      const long long cu = c + (long long)u * kScanThreads;
+#pragma unroll
+      for (int e = 0; e < E; ++e) x[u][e] = -INFINITY;
+      if (cu < c1) {
+        if (VEC) {
+          const uint4 w = reinterpret_cast<const uint4*>(rowp)[cu];
+          const unsigned int ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            if (F32) {
+              x[u][k] = __uint_as_float(ws[k]);
+            } else {
+              x[u][2 * k] = __uint_as_float(ws[k] << 16);
+              x[u][2 * k + 1] = __uint_as_float(ws[k] & 0xFFFF0000u);
+            }
+          }
+        } else if (F32) {
+          x[u][0] = reinterpret_cast<const float*>(rowp)[cu];
+        } else {
+          x[u][0] = __uint_as_float(
+              (unsigned int)reinterpret_cast<const unsigned short*>(rowp)[cu] << 16);
+        }
+      }
+    }
+    float bm = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < L; ++u)
+#pragma unroll
+      for (int e = 0; e < E; ++e) bm = fmaxf(bm, x[u][e]);
+    const float mn = fmaxf(m, bm);
+    float bs = 0.f;
+#pragma unroll
+    for (int u = 0; u < L; ++u)
+#pragma unroll
+      for (int e = 0; e < E; ++e) bs += __expf(x[u][e] - mn);  // exp(-inf) = 0 for padding
+    s = (m == -INFINITY ? 0.f : s * __expf(m - mn)) + bs;
+    m = mn;
+    // padding (-inf) never passes the threshold
+    if (bm > top.thr()) {
+#pragma unroll
+      for (int u = 0; u < L; ++u) {
+        const long long cu = c + (long long)u * kScanThreads;
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+          if (x[u][e] > top.thr()) top.insert(x[u][e], (int)(cu * E + e));
+      }
+    }
+  }
+
+  // workgroup: (m, s) by shuffles and LDS, the top-W by W rounds of argmax
+  __shared__ float red_m[kScanThreads / 64], red_s[kScanThreads / 64];
+  __shared__ float win_v[kScanThreads / 64];
+  __shared__ int win_i[kScanThreads / 64];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) lse_merge(m, s, __shfl_xor(m, o), __shfl_xor(s, o));
+  if (lane == 0) {
+    red_m[wave] = m;
+    red_s[wave] = s;
+  }
+  TopwPart* out = reinterpret_cast<TopwPart*>(a.part + ((size_t)row * a.nsplit + split) * kTopwPartBytes);
+  for (int k = 0; k < W; ++k) {
+    float bv = top.v[0];
+    int bi = top.i[0];
+    wave_best(bv, bi);
+    if (lane == 0) {
+      win_v[wave] = bv;
+      win_i[wave] = bi;
+    }
+    __syncthreads();
+    float gv = win_v[0];
+    int gi = win_i[0];
+#pragma unroll
+    for (int w = 1; w < kScanThreads / 64; ++w)
+      if (better(win_v[w], win_i[w], gv, gi)) {
+        gv = win_v[w];
+        gi = win_i[w];
+      }
+    if (top.i[0] == gi && gi != 0x7FFFFFFF) top.pop();  // indices are unique: one owner
+    if (tid == 0) {
+      out->v[k] = gv;
+      out->i[k] = gi;
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    float gm = red_m[0], gs = red_s[0];
+#pragma unroll
+    for (int w = 1; w < kScanThreads / 64; ++w) lse_merge(gm, gs, red_m[w], red_s[w]);
+    out->m = gm;
+    out->s = gs;
+  }
+}
+
+// One wave per row: lane j < nsplit holds split j's sorted list.
+__global__ __launch_bounds__(64) void topw_finish(TopwArgs a) {
+  const int row = blockIdx.x, lane = threadIdx.x;
+  const int W = a.W;
+  float m = -INFINITY, s = 0.f;
+  TopList<kTopwMax> top;
+  top.init();
+  if (lane < a.nsplit) {
+    const TopwPart* p =
+        reinterpret_cast<const TopwPart*>(a.part + ((size_t)row * a.nsplit + lane) * kTopwPartBytes);
+    m = p->m;
+    s = p->s;
+#pragma unroll
+    for (int k = 0; k < kTopwMax; ++k)
+      if (k < W) {
+        top.v[k] = p->v[k];
+        top.i[k] = p->i[k];
+      }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) lse_merge(m, s, __shfl_xor(m, o), __shfl_xor(s, o));
+  const float lse = m + logf(s);
+  for (int k = 0; k < W; ++k) {
+    float bv = top.v[0];
+    int bi = top.i[0];
+    wave_best(bv, bi);
+    if (top.i[0] == bi) top.pop();
+    if (lane == 0) {
+      a.tok[(size_t)row * W + k] = bi;
+      a.logp[(size_t)row * W + k] = bv - lse;
+    }
+  }
+}
+
+template <int K>
+static void launch_topw_scan_k(bool f32, bool vec, dim3 g, dim3 t, hipStream_t st,
+                               const TopwArgs& a) {
+  if (f32) {
+    if (vec) hipLaunchKernelGGL((topw_scan<true, true, K>), g, t, 0, st, a);
+    else hipLaunchKernelGGL((topw_scan<true, false, K>), g, t, 0, st, a);
+  } else {
+    if (vec) hipLaunchKernelGGL((topw_scan<false, true, K>), g, t, 0, st, a);
+    else hipLaunchKernelGGL((topw_scan<false, false, K>), g, t, 0, st, a);
+  }
+}
+
+static void launch_topw_scan(bool f32, bool vec, int K, dim3 g, dim3 t, hipStream_t st,
+                             const TopwArgs& a) {
+  if (K == 4) launch_topw_scan_k<4>(f32, vec, g, t, st, a);
+  else if (K == 8) launch_topw_scan_k<8>(f32, vec, g, t, st, a);
+  else launch_topw_scan_k<kTopwMax>(f32, vec, g, t, st, a);
+}
+
+hipError_t launch_topw(const void* logits, int f32, int B, int Nd, int V, int W, int32_t* tok,
+                       float* logp, void* ws, hipStream_t st) {
+  const int esize = f32 ? 4 : 2;
+  const bool vec = ((uintptr_t)logits % 16 == 0) && ((size_t)V * esize % 16 == 0);
+  const TopwPlan p = topw_plan(B, Nd, V, vec ? 16 / esize : 1);
+  TopwArgs a;
+  a.logits = logits;
+  a.tok = tok;
+  a.logp = logp;
+  a.part = (unsigned char*)ws;
+  a.rows = B * Nd;
+  a.V = V;
+  a.W = W;
+  a.nsplit = p.nsplit;
+  a.cps = p.chunks_per_split;
+  const dim3 g(p.grid), t(kScanThreads);
+  const int K = W <= 4 ? 4 : (W <= 8 ? 8 : 16);
+  launch_topw_scan(f32 != 0, vec, K, g, t, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(topw_finish, dim3(a.rows), dim3(64), 0, st, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- build
+
+struct BuildArgs {
+  const int32_t* tok;
+  const float* logp;
+  const int32_t* root_tok;
+  int32_t* parent;
+  int32_t* token;
+  int32_t* depth;
+  float* score;
+  int32_t* n_nodes;
+  int Nd, W, budget;
+};
+
+constexpr int kMaxDraftDepth = 64;  // == TV_MAX_DRAFT_DEPTH
+
+__global__ __launch_bounds__(64) void build_tree(BuildArgs a) {
+  __shared__ float cand_lp[kMaxDraftDepth * kTopwMax];
+  __shared__ int cand_tok[kMaxDraftDepth * kTopwMax];
+  __shared__ float sc[kMaxNodes];
+  __shared__ int tk[kMaxNodes];
+  __shared__ short par[kMaxNodes];
+  __shared__ unsigned char dep[kMaxNodes];
+  __shared__ unsigned char open[kMaxNodes];
+  const int b = blockIdx.x, lane = threadIdx.x;
+  const int Nd = a.Nd, W = a.W, budget = a.budget;
+  const size_t cbase = (size_t)b * Nd * W;
+  for (int k = lane; k < Nd * W; k += 64) {
+    cand_lp[k] = a.logp[cbase + k];
+    cand_tok[k] = a.tok[cbase + k];
+  }
+  if (lane == 0) {
+    sc[0] = 0.f;
+    tk[0] = a.root_tok ? a.root_tok[b] : -1;
+    par[0] = -1;
+    dep[0] = 0;
+    open[0] = 1;  // Nd >= 1
+  }
+  __syncthreads();
+  // The loop runs in one wave: LDS accesses of a wave execute in order, so
+  // a lane reads what another lane wrote in an earlier pop; the outputs go
+  // to global memory once at the end.
+  float bs = lane == 0 ? 0.f : -INFINITY;  // this lane's best open node,
+  int bi = lane == 0 ? 0 : 0x7FFFFFFF;     // its index and depth
+  int bd = 0;                              // (lane 0 owns the root)
+  int n = 1;
+  // each pop of an open node adds at least one node, so budget - 1 pops end it
+  for (int it = 0; it < budget && n < budget; ++it) {
+    float gs = bs;
+    int gi = bi, gd = bd;
+    wave_best(gs, gi, gd);
+    if (gi == 0x7FFFFFFF) break;  // nothing open
+    const int v = gi;
+    const int d = gd;
+    if (lane == (v & 63)) {  // the owner closes v and finds its next best
+      open[v] = 0;
+      bs = -INFINITY;
+      bi = 0x7FFFFFFF;
+      for (int i = lane; i < n; i += 64)
+        if (open[i] && better(sc[i], i, bs, bi)) {
+          bs = sc[i];
+          bi = i;
+          bd = dep[i];
+        }
+    }
+    const int nk = min(W, budget - n);
+    const int k = (lane - (n & 63)) & 63;  // this lane's child, if k < nk
+    if (k < nk) {
+      const int c = n + k;
+      const float s = gs + cand_lp[d * W + k];
+      const bool op = d + 1 < Nd;
+      sc[c] = s;
+      tk[c] = cand_tok[d * W + k];
+      par[c] = (short)v;
+      dep[c] = (unsigned char)(d + 1);
+      open[c] = op;
+      if (op && better(s, c, bs, bi)) {
+        bs = s;
+        bi = c;
+        bd = d + 1;
+      }
+    }
+    n += nk;
+    asm volatile("" ::: "memory");
+  }
+  __syncthreads();
+  const size_t obase = (size_t)b * budget;
+  for (int i = lane; i < budget; i += 64) {
+    const bool used = i < n;
+    a.parent[obase + i] = used ? (int)par[i] : -1;
+    a.token[obase + i] = used ? tk[i] : -1;
+    a.depth[obase + i] = used ? (int)dep[i] : -1;
+    if (a.score) a.score[obase + i] = used ? sc[i] : -INFINITY;
+  }
+  if (lane == 0) a.n_nodes[b] = n;
+}
+
+hipError_t launch_build_tree(const int32_t* tok, const float* logp, const int32_t* root_tok, int B,
+                             int Nd, int W, int budget, int32_t* parent, int32_t* token,
+                             int32_t* depth, float* score, int32_t* n_nodes, hipStream_t st) {
+  BuildArgs a;
+  a.tok = tok;
+  a.logp = logp;
+  a.root_tok = root_tok;
+  a.parent = parent;
+  a.token = token;
+  a.depth = depth;
+  a.score = score;
+  a.n_nodes = n_nodes;
+  a.Nd = Nd;
+  a.W = W;
+  a.budget = budget;
+  hipLaunchKernelGGL(build_tree, dim3(B), dim3(64), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace tv

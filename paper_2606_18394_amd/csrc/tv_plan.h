@@ -195,6 +195,41 @@ inline size_t accept_ws_bytes(int B, int N) {
   return (size_t)(rows * accept_split_cap(rows) * 8);
 }
 
+// Draft top-W (tree drafting's candidates): one workgroup per (draft-depth
+// row, vocabulary split) reduces its slice to a running log-sum-exp state
+// and its W best (value, token) pairs; a second kernel merges the splits of
+// each row.  Splits as in the acceptance scan.
+constexpr int kTopwMax = 16;             // largest branching width W
+constexpr size_t kTopwPartBytes = 8 + 8 * kTopwMax;
+
+struct TopwPlan {
+  int nsplit;
+  long long chunks_per_split;
+  int grid;
+  size_t ws_bytes;
+};
+
+inline TopwPlan topw_plan(int B, int Nd, int V, int vec_elems) {
+  TopwPlan p{};
+  const long long rows = (long long)B * Nd;
+  const long long chunks = (V + vec_elems - 1) / vec_elems;
+  long long ns = accept_split_cap(rows);
+  const long long per_round = (long long)kScanThreads * kScanLoadsPerThread;
+  const long long by_size = (chunks + per_round - 1) / per_round;
+  if (ns > by_size) ns = by_size;
+  if (ns < 1) ns = 1;
+  p.chunks_per_split = (chunks + ns - 1) / ns;
+  p.nsplit = (int)((chunks + p.chunks_per_split - 1) / p.chunks_per_split);
+  p.grid = (int)(rows * p.nsplit);
+  p.ws_bytes = (size_t)rows * p.nsplit * kTopwPartBytes;
+  return p;
+}
+
+inline size_t topw_ws_bytes(int B, int Nd) {
+  const long long rows = (long long)B * Nd;
+  return (size_t)(rows * accept_split_cap(rows)) * kTopwPartBytes;
+}
+
 // LDS of the acceptance of one sequence of N nodes: per node the target
 // argmax (int), jump pointers and depths (2 x 2 short, double-buffered),
 // parent (short) and acceptance flags (2 bytes); the finish kernel adds the

@@ -210,5 +210,20 @@ def draft_tokens(parent: np.ndarray, tgt: np.ndarray, match: np.ndarray,
     return out
 
 
+def draft_width(w: Workload) -> int:
+    """Branching width W of the workload's tree drafting: its branching cap,
+    4 where the tree is uncapped."""
+    return w.branching if w.branching else 4
+
+
+def draft_logits(w: Workload, seed: Optional[int] = None) -> np.ndarray:
+    """Draft-head logits [B, depth, V] (one row per draft depth) for the
+    workload's tree drafting, drawn like its target logits (same std and
+    dtype: bf16 bit patterns, or float32) from a stream of their own."""
+    rng = np.random.default_rng(1000 + (w.seed if seed is None else seed))
+    x = (rng.standard_normal((w.B, w.depth, w.V), dtype=np.float32) * np.float32(w.logit_std))
+    return x if w.logits_dtype == "f32" else bf16_bits(x)
+
+
 def with_shape(w: Workload, **kw) -> Workload:
     return replace(w, **kw)

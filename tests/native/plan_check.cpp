@@ -77,6 +77,15 @@ int main() {
         if (ap.nsplit < 1 || ap.nsplit > tv::kAcceptMaxSplit) ok = false;
         if (ap.ws_bytes != (size_t)B * N * ap.nsplit * 8) ok = false;
         if (tv::accept_lds_bytes(N) + (size_t)N * 8 > 64 * 1024) ok = false;
+        // draft top-W over Nd = min(N, 64) depth rows: every chunk in one
+        // split, the workspace within its bound
+        const int Nd = N < 64 ? N : 64;
+        const tv::TopwPlan tp = tv::topw_plan(B, Nd, V, vec);
+        if (tp.grid != (long long)B * Nd * tp.nsplit) ok = false;
+        if ((long long)tp.nsplit * tp.chunks_per_split < nch) ok = false;
+        if ((long long)(tp.nsplit - 1) * tp.chunks_per_split >= nch) ok = false;
+        if (tp.nsplit < 1 || tp.nsplit > tv::kAcceptMaxSplit) ok = false;
+        if (tp.ws_bytes > tv::topw_ws_bytes(B, Nd)) ok = false;
       }
     std::printf("%s B=%d N=%d Hq=%d Hkv=%d D=%d L=%d V=%d S=%d RB=%d nRB=%d grid=%d lds=%zu ws=%zu\n",
                 ok ? "OK" : "FAIL", B, N, Hq, Hkv, D, Lmax, V, p.S, p.RB, p.nRB, p.grid,

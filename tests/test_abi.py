@@ -27,7 +27,8 @@ def _declared():
 def test_header_declares_the_api():
     names = _declared()
     for n in ["tv_tree_verify_attention", "tv_tree_accept", "tv_tree_verify_attention_workspace",
-              "tv_tree_accept_workspace", "tv_status_string", "tv_version"]:
+              "tv_tree_accept_workspace", "tv_status_string", "tv_version",
+              "tv_draft_topw", "tv_draft_topw_workspace", "tv_build_tree"]:
         assert n in names
 
 
@@ -56,6 +57,9 @@ def test_workspace_queries():
     assert lib.tv_tree_accept_workspace(1, 64, 151936) > 0
     assert lib.tv_tree_accept_workspace(1, 0, 10) == 0
     assert lib.tv_tree_accept_workspace(1, 4096, 10) == 0
+    assert lib.tv_draft_topw_workspace(1, 8, 151936) > 0
+    assert lib.tv_draft_topw_workspace(1, 65, 10) == 0     # draft depth above the limit
+    assert lib.tv_draft_topw_workspace(1, 8, 0) == 0
 
 
 FAKE = 0x100000  # 16-byte aligned non-null address; never dereferenced
@@ -120,3 +124,41 @@ def test_binding_refuses_cpu_tensors():
     with pytest.raises(ValueError):
         tree_accept(torch.zeros(1, 2, 8), torch.zeros(1, 2, dtype=torch.int32),
                     torch.tensor([[-1, 0]], dtype=torch.int32), 2)
+
+
+def _topw(lib, **kw):
+    a = dict(logits=FAKE, dt=0, B=1, Nd=8, V=151936, W=4, tok=FAKE, logp=FAKE, ws=FAKE,
+             wsb=1 << 40)
+    a.update(kw)
+    return lib.tv_draft_topw(a["logits"], a["dt"], a["B"], a["Nd"], a["V"], a["W"], a["tok"],
+                             a["logp"], a["ws"], a["wsb"], None)
+
+
+def _build(lib, **kw):
+    a = dict(tok=FAKE, logp=FAKE, root=None, B=1, Nd=8, W=4, budget=64, parent=FAKE,
+             token=FAKE, depth=FAKE, score=None, n=FAKE)
+    a.update(kw)
+    return lib.tv_build_tree(a["tok"], a["logp"], a["root"], a["B"], a["Nd"], a["W"],
+                             a["budget"], a["parent"], a["token"], a["depth"], a["score"],
+                             a["n"], None)
+
+
+def test_drafting_host_errors():
+    lib = _lib()
+    assert _topw(lib, logits=None) == -1
+    assert _topw(lib, logp=None) == -1
+    assert _topw(lib, dt=5) == -3
+    assert _topw(lib, W=0) == -2
+    assert _topw(lib, V=3, W=4) == -2          # fewer tokens than candidates
+    assert _topw(lib, W=17) == -4
+    assert _topw(lib, Nd=65) == -4
+    assert _topw(lib, ws=None) == -5
+    assert _topw(lib, wsb=8) == -5
+    assert _topw(lib, ws=FAKE + 4) == -7
+    assert _build(lib, tok=None) == -1
+    assert _build(lib, n=None) == -1
+    assert _build(lib, budget=0) == -2
+    assert _build(lib, B=0) == -2
+    assert _build(lib, budget=2049) == -4
+    assert _build(lib, W=17) == -4
+    assert _build(lib, Nd=65) == -4

@@ -1,0 +1,152 @@
+"""GPU parity of budgeted tree drafting against the oracle (through the C
+ABI): top-W tokens bit-exact and log-probabilities within LOGP_TOL; trees
+(parent, token, depth, fp32 score, node count) bit-exact from the same
+candidates."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_18394_amd import synth
+from helpers import dev_bf16, dev_i32
+
+pytestmark = pytest.mark.gpu
+
+# log-probability tolerance: the kernel's log-sum-exp sums up to V ~ 1.5e5
+# fp32 terms (per-thread partial sums of a few hundred, then a tree), each
+# exp accurate to a few ulp: relative error of the sum ~1e-6, i.e. ~1e-6
+# absolute in its log; logits are exact, so 1e-4 leaves a wide margin.
+LOGP_TOL = 1e-4
+
+
+def _dev_logits(x, dtype):
+    import torch
+    if dtype == "f32":
+        return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).cuda()
+    return dev_bf16(x)
+
+
+def _host_logits(x, dtype):
+    return x.astype(np.float64) if dtype == "f32" else oracle.decode_bf16(x)
+
+
+def _gpu_topw(x, dtype, W):
+    import torch
+    from paper_2606_18394_amd import draft_topw
+    tok, lp = draft_topw(_dev_logits(x, dtype), W)
+    torch.cuda.synchronize()
+    return tok.cpu().numpy(), lp.cpu().numpy()
+
+
+TOPW_CASES = [
+    # (B, Nd, V, W, dtype, kind)
+    (1, 8, 151936, 4, "bf16", "normal"),
+    (1, 16, 151936, 7, "bf16", "normal"),
+    (2, 3, 1000, 16, "f32", "normal"),
+    (1, 4, 17, 16, "f32", "normal"),          # tiny vocabulary, not a multiple of 8
+    (3, 5, 4099, 5, "bf16", "normal"),         # scalar (unaligned row) path
+    (2, 6, 5000, 8, "bf16", "ties"),           # many equal values: lower index first
+    (1, 2, 300, 16, "f32", "ties"),
+    (4, 64, 2048, 2, "bf16", "normal"),        # deepest draft
+    (1, 1, 1, 1, "f32", "normal"),
+]
+
+
+@pytest.mark.parametrize("case", range(len(TOPW_CASES)))
+def test_topw_parity(case):
+    B, Nd, V, W, dtype, kind = TOPW_CASES[case]
+    rng = np.random.default_rng(50 + case)
+    if kind == "ties":
+        x = rng.integers(-4, 4, size=(B, Nd, V)).astype(np.float32)
+    else:
+        x = rng.standard_normal((B, Nd, V), dtype=np.float32) * 2
+    if dtype == "bf16":
+        x = synth.bf16_bits(x)
+    print(f"topw case {TOPW_CASES[case]}", flush=True)
+    tok, lp = _gpu_topw(x, dtype, W)
+    rt, rl = oracle.draft_topw(_host_logits(x, dtype), W)
+    np.testing.assert_array_equal(tok, rt)
+    err = np.abs(lp - rl).max()
+    print(f"  max |logp err| {err:.2e}", flush=True)
+    assert err <= LOGP_TOL
+
+
+def _gpu_build(tok, lp, budget, root=None):
+    import torch
+    from paper_2606_18394_amd import build_tree
+    par, t, d, s, n = build_tree(dev_i32(tok), torch.from_numpy(np.ascontiguousarray(lp, np.float32)).cuda(),
+                                 budget, root_tok=None if root is None else dev_i32(root))
+    torch.cuda.synchronize()
+    return {"parent": par.cpu().numpy(), "token": t.cpu().numpy(), "depth": d.cpu().numpy(),
+            "score": s.cpu().numpy(), "n_nodes": n.cpu().numpy()}
+
+
+def _compare_trees(got, ref):
+    np.testing.assert_array_equal(got["n_nodes"], ref["n_nodes"])
+    np.testing.assert_array_equal(got["parent"], ref["parent"])
+    np.testing.assert_array_equal(got["token"], ref["token"])
+    np.testing.assert_array_equal(got["depth"], ref["depth"])
+    np.testing.assert_array_equal(got["score"], ref["score"])
+
+
+def _candidates(rng, B, Nd, W, kind):
+    if kind == "ties":      # few distinct values: many equal scores
+        lp = -np.sort(rng.integers(0, 3, size=(B, Nd, W)), axis=-1).astype(np.float32)
+    else:
+        lp = -np.sort(rng.exponential(1.5, size=(B, Nd, W)), axis=-1).astype(np.float32)
+    tok = rng.integers(0, 151936, size=(B, Nd, W))
+    return tok, lp
+
+
+BUILD_CASES = [
+    # (B, Nd, W, budget, kind)
+    (1, 8, 4, 64, "normal"),
+    (1, 16, 7, 256, "normal"),
+    (1, 16, 8, 512, "normal"),
+    (16, 8, 4, 64, "normal"),
+    (3, 3, 3, 100, "normal"),      # budget beyond the full tree (40 nodes)
+    (2, 6, 1, 20, "normal"),       # width one: a chain
+    (4, 5, 4, 200, "ties"),        # equal scores: lower node index first
+    (1, 1, 16, 17, "ties"),
+    (2, 12, 16, 2048, "normal"),   # largest budget
+    (5, 4, 3, 1, "normal"),        # root only
+    (1, 64, 2, 1000, "normal"),    # deepest draft
+]
+
+
+@pytest.mark.parametrize("case", range(len(BUILD_CASES)))
+def test_build_parity(case):
+    B, Nd, W, budget, kind = BUILD_CASES[case]
+    rng = np.random.default_rng(300 + case)
+    tok, lp = _candidates(rng, B, Nd, W, kind)
+    root = rng.integers(0, 151936, size=B)
+    print(f"build case {BUILD_CASES[case]}", flush=True)
+    got = _gpu_build(tok, lp, budget, root)
+    ref = oracle.build_tree(tok, lp, budget, root_tok=root)
+    _compare_trees(got, ref)
+
+
+@pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
+def test_workload_drafting(name):
+    """Each workload's drafting: top-W of its draft logits against the
+    oracle, the tree from the oracle's candidates bit-exact, and the tree
+    from the GPU's own candidates a valid input of the verification calls."""
+    import torch
+    from paper_2606_18394_amd import build_tree, draft_topw
+    w = synth.WORKLOADS[name]
+    W = synth.draft_width(w)
+    x = synth.draft_logits(w)
+    print(f"drafting {name}: B={w.B} depth={w.depth} W={W} budget={w.N}", flush=True)
+    tok, lp = _gpu_topw(x, w.logits_dtype, W)
+    rt, rl = oracle.draft_topw(_host_logits(x, w.logits_dtype), W)
+    np.testing.assert_array_equal(tok, rt)
+    assert np.abs(lp - rl).max() <= LOGP_TOL
+    ref = oracle.build_tree(rt, rl.astype(np.float32), w.N)
+    _compare_trees(_gpu_build(rt, rl.astype(np.float32), w.N), ref)
+    # GPU candidates -> GPU tree: structure of a verification input
+    dtok, dlp = draft_topw(_dev_logits(x, w.logits_dtype), W)
+    par, token, dep, _, n = build_tree(dtok, dlp, w.N)
+    torch.cuda.synchronize()
+    par, n = par.cpu().numpy(), n.cpu().numpy()
+    for b in range(w.B):
+        assert n[b] == w.N and par[b, 0] == -1
+        assert ((par[b, 1:] >= 0) & (par[b, 1:] < np.arange(1, w.N))).all()

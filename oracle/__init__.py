@@ -13,6 +13,8 @@ Contents
   draft_topw,     -- budgeted tree drafting: top-W candidates per draft depth
   build_tree         and best-first expansion by accumulated draft
                      log-probability (Sec. 2.4 parallel tree drafting; Alg. 1).
+  kv_commit       -- the cache side: committing the accepted path, paged
+                     caches (App. E).
   brute           -- pure-Python loop versions for tiny inputs, used only to
                      pin the functions above.
 

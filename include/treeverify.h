@@ -109,6 +109,57 @@ int tv_tree_verify_attention(const void* q, const void* k_cache,
                              void* workspace, size_t workspace_bytes,
                              hipStream_t stream);
 
+/*
+ * The same attention over a paged cache (App. E: the verification kernel
+ * reads the serving engine's paged KV cache).  Position t of sequence b is
+ * row t % block_size of pool block block_table[b, t / block_size].
+ *
+ *   k_pool, v_pool [num_blocks, block_size, Hkv, D] bf16
+ *   block_table    [B, max_blocks] int32; entries outside [0, num_blocks)
+ *                  are clamped into it (no memory outside the pool is read;
+ *                  that sequence's result is then meaningless)
+ *   kv_len [B] in [0, max_blocks * block_size], NULL = max_blocks * block_size
+ *
+ * block_size is a power of two >= 32.  Everything else as in
+ * tv_tree_verify_attention with Lmax = max_blocks * block_size, including
+ * the workspace (tv_tree_verify_attention_workspace(B, N, Hq, Hkv, D,
+ * max_blocks * block_size)); results are identical to the padded call on
+ * the gathered cache.
+ */
+int tv_tree_verify_attention_paged(const void* q, const void* k_pool, const void* v_pool,
+                                   const int32_t* block_table, int block_size, int max_blocks,
+                                   int num_blocks, const void* k_tree, const void* v_tree,
+                                   const int32_t* parent, const int32_t* kv_len, void* out,
+                                   int B, int N, int Hq, int Hkv, int D, float scale,
+                                   void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream);
+
+/*
+ * Commit the accepted path (App. E): the keys and values of nodes
+ * path[b, 0 .. accept_len[b]-1] (root first) of k_tree/v_tree are copied to
+ * cache positions kv_len[b] .. kv_len[b] + accept_len[b] - 1 and kv_len[b]
+ * grows by accept_len[b].  A sequence whose accept_len is < 1 or > Dmax,
+ * whose path names a node outside [0, N), or whose commit would pass Lmax,
+ * is left unchanged (cache and kv_len).  The tree buffers must not overlap
+ * the cache.
+ *
+ *   k_tree, v_tree  [B, N, Hkv, D] bf16
+ *   path [B, Dmax], accept_len [B]   as written by tv_tree_accept
+ *   k_cache, v_cache [B, Lmax, Hkv, D] bf16, updated in place
+ *   kv_len [B] int32, updated in place
+ */
+int tv_commit_path(const void* k_tree, const void* v_tree, const int32_t* path,
+                   const int32_t* accept_len, void* k_cache, void* v_cache, int32_t* kv_len,
+                   int B, int N, int Hkv, int D, int Lmax, int Dmax, hipStream_t stream);
+
+/* tv_commit_path into a paged cache (layout as in
+ * tv_tree_verify_attention_paged); the capacity is max_blocks * block_size. */
+int tv_commit_path_paged(const void* k_tree, const void* v_tree, const int32_t* path,
+                         const int32_t* accept_len, void* k_pool, void* v_pool,
+                         const int32_t* block_table, int block_size, int max_blocks,
+                         int num_blocks, int32_t* kv_len, int B, int N, int Hkv, int D, int Dmax,
+                         hipStream_t stream);
+
 /* Workspace bytes tv_tree_accept needs for these sizes (0 when invalid). */
 size_t tv_tree_accept_workspace(int B, int N, int V);
 

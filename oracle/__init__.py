@@ -25,6 +25,8 @@ from .tree_attention import (decode_bf16, tree_structure, full_mask,
                              tree_attention)
 from .tree_accept import target_argmax, tree_accept
 from .tree_build import draft_topw, build_tree
+from .kv_commit import commit_path, gather_paged, commit_path_paged
 
 __all__ = ["decode_bf16", "tree_structure", "full_mask", "tree_attention",
-           "target_argmax", "tree_accept", "draft_topw", "build_tree"]
+           "target_argmax", "tree_accept", "draft_topw", "build_tree",
+           "commit_path", "gather_paged", "commit_path_paged"]

@@ -6,11 +6,27 @@ Importing the package loads nothing; the first call loads libtreeverify.so
 and raises if it is missing.
 """
 
-__all__ = ["tree_verify_attention", "tree_accept", "draft_topw", "build_tree", "load_library"]
+__all__ = ["tree_verify_attention", "tree_verify_attention_paged", "tree_accept",
+           "commit_path", "commit_path_paged", "draft_topw", "build_tree", "load_library"]
 
 
 def tree_verify_attention(*args, **kwargs):
     from .binding import tree_verify_attention as f
+    return f(*args, **kwargs)
+
+
+def tree_verify_attention_paged(*args, **kwargs):
+    from .binding import tree_verify_attention_paged as f
+    return f(*args, **kwargs)
+
+
+def commit_path(*args, **kwargs):
+    from .binding import commit_path as f
+    return f(*args, **kwargs)
+
+
+def commit_path_paged(*args, **kwargs):
+    from .binding import commit_path_paged as f
     return f(*args, **kwargs)
 
 

@@ -58,6 +58,15 @@ def load_library() -> ctypes.CDLL:
         lib.tv_draft_topw.argtypes = [vp] + [ci] * 5 + [i32p, vp, vp, sz, vp]
         lib.tv_build_tree.restype = ci
         lib.tv_build_tree.argtypes = [i32p, vp, i32p] + [ci] * 4 + [i32p, i32p, i32p, vp, i32p, vp]
+        lib.tv_tree_verify_attention_paged.restype = ci
+        lib.tv_tree_verify_attention_paged.argtypes = (
+            [vp, vp, vp, i32p] + [ci] * 3 + [vp, vp, i32p, i32p, vp] + [ci] * 5
+            + [ctypes.c_float, vp, sz, vp])
+        lib.tv_commit_path.restype = ci
+        lib.tv_commit_path.argtypes = [vp, vp, i32p, i32p, vp, vp, i32p] + [ci] * 6 + [vp]
+        lib.tv_commit_path_paged.restype = ci
+        lib.tv_commit_path_paged.argtypes = (
+            [vp, vp, i32p, i32p, vp, vp, i32p] + [ci] * 3 + [i32p] + [ci] * 5 + [vp])
         _lib = lib
         return lib
 
@@ -130,6 +139,85 @@ def tree_verify_attention(q, k_cache, v_cache, k_tree, v_tree, parent, out,
         _ptr(kv_len), _ptr(out), B, N, Hq, Hkv, D, Lmax,
         0.0 if scale is None else float(scale), _ptr(ws), ws.numel(), ctypes.c_void_p(stream)))
     return out
+
+
+def tree_verify_attention_paged(q, k_pool, v_pool, block_table, k_tree, v_tree, parent, out,
+                                kv_len=None, scale=None, workspace_tensor=None):
+    """tree_verify_attention over a paged cache: position t of sequence b is
+    row t % block_size of k_pool/v_pool[block_table[b, t // block_size]].
+
+    k_pool/v_pool [num_blocks, block_size, Hkv, D] bf16; block_table
+    [B, max_blocks] int32; the rest as in tree_verify_attention.
+    """
+    lib = load_library()
+    B, N, Hq, D = q.shape
+    num_blocks, bs, Hkv = k_pool.shape[0], k_pool.shape[1], k_pool.shape[2]
+    max_blocks = block_table.shape[1]
+    dev = q.device
+    _need(q, "q", torch.bfloat16, device=dev)
+    _need(k_pool, "k_pool", torch.bfloat16, (num_blocks, bs, Hkv, D), dev)
+    _need(v_pool, "v_pool", torch.bfloat16, (num_blocks, bs, Hkv, D), dev)
+    _need(block_table, "block_table", torch.int32, (B, max_blocks), dev)
+    _need(k_tree, "k_tree", torch.bfloat16, (B, N, Hkv, D), dev)
+    _need(v_tree, "v_tree", torch.bfloat16, (B, N, Hkv, D), dev)
+    _need(parent, "parent", torch.int32, (B, N), dev)
+    _need(out, "out", torch.bfloat16, (B, N, Hq, D), dev)
+    if kv_len is not None:
+        _need(kv_len, "kv_len", torch.int32, (B,), dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    need = lib.tv_tree_verify_attention_workspace(B, N, Hq, Hkv, D, max_blocks * bs)
+    if need == 0:
+        _check(-2)
+    ws = workspace_tensor if workspace_tensor is not None else workspace("attn", need, dev, stream)
+    _check(lib.tv_tree_verify_attention_paged(
+        _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(block_table), bs, max_blocks, num_blocks,
+        _ptr(k_tree), _ptr(v_tree), _ptr(parent), _ptr(kv_len), _ptr(out), B, N, Hq, Hkv, D,
+        0.0 if scale is None else float(scale), _ptr(ws), ws.numel(), ctypes.c_void_p(stream)))
+    return out
+
+
+def commit_path(k_tree, v_tree, path, accept_len, k_cache, v_cache, kv_len):
+    """Append the accepted path's K/V (root first) to the contiguous cache at
+    kv_len and advance kv_len, in place.  k_tree/v_tree [B,N,Hkv,D],
+    path [B,Dmax], accept_len [B], k_cache/v_cache [B,Lmax,Hkv,D], kv_len [B]."""
+    lib = load_library()
+    B, N, Hkv, D = k_tree.shape
+    Lmax, Dmax = k_cache.shape[1], path.shape[1]
+    dev = k_tree.device
+    _need(k_tree, "k_tree", torch.bfloat16, (B, N, Hkv, D), dev)
+    _need(v_tree, "v_tree", torch.bfloat16, (B, N, Hkv, D), dev)
+    _need(path, "path", torch.int32, (B, Dmax), dev)
+    _need(accept_len, "accept_len", torch.int32, (B,), dev)
+    _need(k_cache, "k_cache", torch.bfloat16, (B, Lmax, Hkv, D), dev)
+    _need(v_cache, "v_cache", torch.bfloat16, (B, Lmax, Hkv, D), dev)
+    _need(kv_len, "kv_len", torch.int32, (B,), dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    _check(lib.tv_commit_path(
+        _ptr(k_tree), _ptr(v_tree), _ptr(path), _ptr(accept_len), _ptr(k_cache), _ptr(v_cache),
+        _ptr(kv_len), B, N, Hkv, D, Lmax, Dmax, ctypes.c_void_p(stream)))
+
+
+def commit_path_paged(k_tree, v_tree, path, accept_len, k_pool, v_pool, block_table, kv_len):
+    """commit_path into a paged cache (layout as in
+    tree_verify_attention_paged), in place."""
+    lib = load_library()
+    B, N, Hkv, D = k_tree.shape
+    num_blocks, bs = k_pool.shape[0], k_pool.shape[1]
+    max_blocks, Dmax = block_table.shape[1], path.shape[1]
+    dev = k_tree.device
+    _need(k_tree, "k_tree", torch.bfloat16, (B, N, Hkv, D), dev)
+    _need(v_tree, "v_tree", torch.bfloat16, (B, N, Hkv, D), dev)
+    _need(path, "path", torch.int32, (B, Dmax), dev)
+    _need(accept_len, "accept_len", torch.int32, (B,), dev)
+    _need(k_pool, "k_pool", torch.bfloat16, (num_blocks, bs, Hkv, D), dev)
+    _need(v_pool, "v_pool", torch.bfloat16, (num_blocks, bs, Hkv, D), dev)
+    _need(block_table, "block_table", torch.int32, (B, max_blocks), dev)
+    _need(kv_len, "kv_len", torch.int32, (B,), dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    _check(lib.tv_commit_path_paged(
+        _ptr(k_tree), _ptr(v_tree), _ptr(path), _ptr(accept_len), _ptr(k_pool), _ptr(v_pool),
+        _ptr(block_table), bs, max_blocks, num_blocks, _ptr(kv_len), B, N, Hkv, D, Dmax,
+        ctypes.c_void_p(stream)))
 
 
 def tree_accept(logits, draft_tok, parent, Dmax, accept_len=None, path=None,

@@ -12,7 +12,13 @@ namespace tv {
 hipError_t launch_attention(const void* q, const void* kc, const void* vc, const void* kt,
                             const void* vt, const int32_t* parent, const int32_t* kv_len,
                             void* out, int B, int N, int Hq, int Hkv, int D, int Lmax,
-                            float scale, void* ws, const AttnPlan& p, hipStream_t st);
+                            float scale, void* ws, const AttnPlan& p, hipStream_t st,
+                            const int32_t* block_table, int block_shift, int max_blocks,
+                            int num_blocks);
+hipError_t launch_commit(const void* kt, const void* vt, const int32_t* path,
+                         const int32_t* accept_len, void* kc, void* vc, int32_t* kv_len,
+                         const int32_t* block_table, int shift, int max_blocks, int num_blocks,
+                         int B, int N, int Hkv, int D, int cap, int Dmax, hipStream_t st);
 hipError_t launch_accept(const void* logits, int f32, const int32_t* draft, const int32_t* parent,
                          int B, int N, int V, int Dmax, int32_t* accept_len, int32_t* path,
                          int32_t* tgt_out, void* ws, hipStream_t st);
@@ -35,6 +41,14 @@ static int check_attention_sizes(int B, int N, int Hq, int Hkv, int D, int Lmax)
   // element offsets are formed in 64-bit, but row indices stay in int32
   if ((long long)B * N * Hq > (1ll << 31) || (long long)B * Lmax > (1ll << 31)) return TV_ERR_UNSUPPORTED;
   return TV_OK;
+}
+
+// log2 of a valid block size (a power of two in [32, 2^20]), else -1
+static int block_shift(int block_size) {
+  if (block_size < 32 || block_size > (1 << 20) || (block_size & (block_size - 1))) return -1;
+  int s = 0;
+  while ((1 << s) < block_size) ++s;
+  return s;
 }
 
 static int check_accept_sizes(int B, int N, int V, int Dmax) {
@@ -92,7 +106,79 @@ int tv_tree_verify_attention(const void* q, const void* k_cache, const void* v_c
   if (misaligned(workspace)) return TV_ERR_ALIGN;
   if (!(scale > 0.f)) scale = 1.0f / sqrtf((float)D);
   hipError_t e = tv::launch_attention(q, k_cache, v_cache, k_tree, v_tree, parent, kv_len, out,
-                                      B, N, Hq, Hkv, D, Lmax, scale, workspace, p, stream);
+                                      B, N, Hq, Hkv, D, Lmax, scale, workspace, p, stream,
+                                      nullptr, 0, 0, 0);
+  return e == hipSuccess ? TV_OK : TV_ERR_LAUNCH;
+}
+
+int tv_tree_verify_attention_paged(const void* q, const void* k_pool, const void* v_pool,
+                                   const int32_t* block_table, int block_size, int max_blocks,
+                                   int num_blocks, const void* k_tree, const void* v_tree,
+                                   const int32_t* parent, const int32_t* kv_len, void* out,
+                                   int B, int N, int Hq, int Hkv, int D, float scale,
+                                   void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream) {
+  const int shift = block_shift(block_size);
+  if (shift < 0 || max_blocks < 0 || num_blocks < 0) return TV_ERR_SHAPE;
+  if ((long long)max_blocks * block_size > (1ll << 30)) return TV_ERR_UNSUPPORTED;
+  const int Lmax = max_blocks * block_size;
+  int rc = check_attention_sizes(B, N, Hq, Hkv, D, Lmax);
+  if (rc != TV_OK) return rc;
+  if (!q || !k_tree || !v_tree || !parent || !out) return TV_ERR_NULL;
+  if (Lmax > 0 && (!k_pool || !v_pool || !block_table || num_blocks < 1)) return TV_ERR_NULL;
+  if (misaligned(q) || misaligned(k_tree) || misaligned(v_tree) || misaligned(out) ||
+      (Lmax > 0 && (misaligned(k_pool) || misaligned(v_pool))))
+    return TV_ERR_ALIGN;
+  const tv::AttnPlan p = tv::attn_plan(B, N, Hq, Hkv, D, Lmax);
+  if (p.ws_bytes > 0 && (!workspace || workspace_bytes < p.ws_bytes)) return TV_ERR_WORKSPACE;
+  if (misaligned(workspace)) return TV_ERR_ALIGN;
+  if (!(scale > 0.f)) scale = 1.0f / sqrtf((float)D);
+  hipError_t e = tv::launch_attention(q, k_pool, v_pool, k_tree, v_tree, parent, kv_len, out, B,
+                                      N, Hq, Hkv, D, Lmax, scale, workspace, p, stream,
+                                      Lmax > 0 ? block_table : nullptr, shift, max_blocks,
+                                      num_blocks);
+  return e == hipSuccess ? TV_OK : TV_ERR_LAUNCH;
+}
+
+static int check_commit(const void* kt, const void* vt, const int32_t* path,
+                        const int32_t* accept_len, const void* kc, const void* vc,
+                        const int32_t* kv_len, int B, int N, int Hkv, int D, int Dmax) {
+  if (B < 1 || N < 1 || Hkv < 1 || Dmax < 1) return TV_ERR_SHAPE;
+  if (D != 64 && D != 128) return TV_ERR_UNSUPPORTED;
+  if (N > TV_MAX_NODES) return TV_ERR_UNSUPPORTED;
+  if (!kt || !vt || !path || !accept_len || !kc || !vc || !kv_len) return TV_ERR_NULL;
+  if (misaligned(kt) || misaligned(vt) || misaligned(kc) || misaligned(vc)) return TV_ERR_ALIGN;
+  return TV_OK;
+}
+
+int tv_commit_path(const void* k_tree, const void* v_tree, const int32_t* path,
+                   const int32_t* accept_len, void* k_cache, void* v_cache, int32_t* kv_len,
+                   int B, int N, int Hkv, int D, int Lmax, int Dmax, hipStream_t stream) {
+  int rc = check_commit(k_tree, v_tree, path, accept_len, k_cache, v_cache, kv_len, B, N, Hkv,
+                        D, Dmax);
+  if (rc != TV_OK) return rc;
+  if (Lmax < 1) return TV_ERR_SHAPE;
+  if ((long long)B * Lmax > (1ll << 31)) return TV_ERR_UNSUPPORTED;
+  hipError_t e = tv::launch_commit(k_tree, v_tree, path, accept_len, k_cache, v_cache, kv_len,
+                                   nullptr, 0, 0, 0, B, N, Hkv, D, Lmax, Dmax, stream);
+  return e == hipSuccess ? TV_OK : TV_ERR_LAUNCH;
+}
+
+int tv_commit_path_paged(const void* k_tree, const void* v_tree, const int32_t* path,
+                         const int32_t* accept_len, void* k_pool, void* v_pool,
+                         const int32_t* block_table, int block_size, int max_blocks,
+                         int num_blocks, int32_t* kv_len, int B, int N, int Hkv, int D, int Dmax,
+                         hipStream_t stream) {
+  int rc = check_commit(k_tree, v_tree, path, accept_len, k_pool, v_pool, kv_len, B, N, Hkv, D,
+                        Dmax);
+  if (rc != TV_OK) return rc;
+  const int shift = block_shift(block_size);
+  if (shift < 0 || max_blocks < 1 || num_blocks < 1) return TV_ERR_SHAPE;
+  if (!block_table) return TV_ERR_NULL;
+  if ((long long)max_blocks * block_size > (1ll << 30)) return TV_ERR_UNSUPPORTED;
+  hipError_t e = tv::launch_commit(k_tree, v_tree, path, accept_len, k_pool, v_pool, kv_len,
+                                   block_table, shift, max_blocks, num_blocks, B, N, Hkv, D,
+                                   max_blocks * block_size, Dmax, stream);
   return e == hipSuccess ? TV_OK : TV_ERR_LAUNCH;
 }
 

@@ -62,6 +62,8 @@ struct AttnArgs {
   int B, N, Hq, Hkv, Lmax, G, M, nRB, S, chunk, nwork;
   int fused;  // split-KV merge inside the main kernel (else a second kernel)
   float c;  // scale * log2(e): scores live in base-2 exponent units
+  const int32_t* block_table;  // paged cache: [B, max_blocks], else NULL
+  int block_shift, max_blocks, num_blocks;
 };
 
 // Four output values, or four NaN when the sequence's tree is invalid (the
@@ -124,6 +126,15 @@ __device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t
                : "memory");
 }
 
+// A wave-uniform pointer the compiler cannot prove uniform, moved to SGPRs
+// (the DMA's base address operand must be scalar).
+__device__ __forceinline__ const char* uniform_ptr(const char* p) {
+  const uint64_t u = (uint64_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+  return (const char*)(((uint64_t)hi << 32) | lo);
+}
+
 // s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding).
 template <int n>
 __device__ __forceinline__ void wait_vm() {
@@ -169,13 +180,19 @@ struct TileLayout {
   }
 };
 
-// Where a wave's K/V rows come from: the padded cache of one (sequence, KV
-// head) pair, then its tree K/V.  Pointers are byte pointers.
+// Where a wave's K/V rows come from: the cache of one (sequence, KV head)
+// pair, then its tree K/V.  The cache is either padded (row t at kcache +
+// t * row_bytes) or paged (row t in pool block btab[t >> shift], whose rows
+// are 2^shift apart from kcache + block * 2^shift * row_bytes; a 32-key
+// tile never straddles blocks since blocks hold a power of two >= 32 rows).
+// Block numbers are clamped into the pool.  Pointers are byte pointers.
 struct TreeSrc {
   const char* kcache;
   const char* vcache;
   const char* ktree;
   const char* vtree;
+  const int32_t* btab;  // this sequence's block table row, or NULL
+  int shift, nblk;      // log2(block size), blocks in the pool
   int row_bytes;  // bytes between consecutive keys
   int kvl;        // valid cache rows
   int nct;        // cache tiles
@@ -187,15 +204,28 @@ struct TreeSrc {
 // the valid range are clamped onto a valid row (the mask gives them zero
 // weight, the clamp keeps reads in range).  dma_off is the per-lane byte
 // offset of its chunk within a full tile.
-template <int D, int PW>
+template <int D, int PW, bool kPaged>
 __device__ __forceinline__ void issue_tile(const TreeSrc& src, const uint32_t (&dma_off)[PW],
                                            int wr, int lane, int t, uint32_t kdst) {
   using TL = TileLayout<D>;
   const bool cache = t < src.nct;
   const int first = cache ? t * kKeyTile : (t - src.nct) * kKeyTile;
-  const size_t tofs = (size_t)first * src.row_bytes;
-  const char* kb = (cache ? src.kcache : src.ktree) + tofs;
-  const char* vb = (cache ? src.vcache : src.vtree) + tofs;
+  const char* kb;
+  const char* vb;
+  if constexpr (kPaged) {
+    size_t tofs = (size_t)first * src.row_bytes;
+    if (cache) {
+      // wave-uniform: the tile index is, so the block is
+      int blk = __builtin_amdgcn_readfirstlane(src.btab[first >> src.shift]);
+      blk = blk < 0 ? 0 : (blk >= src.nblk ? src.nblk - 1 : blk);
+      tofs = (((size_t)blk << src.shift) + (first & ((1 << src.shift) - 1))) * src.row_bytes;
+    }
+    kb = uniform_ptr((cache ? src.kcache : src.ktree) + tofs);
+    vb = uniform_ptr((cache ? src.vcache : src.vtree) + tofs);
+  } else {
+    kb = (cache ? src.kcache : src.ktree) + (size_t)first * src.row_bytes;
+    vb = (cache ? src.vcache : src.vtree) + (size_t)first * src.row_bytes;
+  }
   if (cache && (t + 1) * kKeyTile <= src.kvl) {
 #pragma unroll
     for (int k = 0; k < PW; ++k) {
@@ -450,7 +480,7 @@ __device__ __forceinline__ void merge_chunks(const AttnArgs& a, size_t part0, in
 // waves of a key group share one LDS ring and walk that group's tiles (every
 // WK-th tile of the chunk) in lock step; WK > 1 groups merge their partial
 // softmax states in LDS at the end.
-template <int D, int WR, int WK, int NS>
+template <int D, int WR, int WK, int NS, bool kPaged>
 __global__ __launch_bounds__(64 * WR * WK) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_main(AttnArgs a) {
   using TL = TileLayout<D>;
@@ -504,8 +534,9 @@ void attn_main(AttnArgs a) {
   int* flag = par + a.N;
 
   const size_t krow = (size_t)a.Hkv * D;  // elements between consecutive keys
-  const __bf16* kcache = a.kc + (size_t)b * a.Lmax * krow + (size_t)g * D;
-  const __bf16* vcache = a.vc + (size_t)b * a.Lmax * krow + (size_t)g * D;
+  const size_t cache0 = kPaged ? 0 : (size_t)b * a.Lmax * krow;  // paged: pool base
+  const __bf16* kcache = a.kc + cache0 + (size_t)g * D;
+  const __bf16* vcache = a.vc + cache0 + (size_t)g * D;
   const __bf16* ktree = a.kt + (size_t)b * a.N * krow + (size_t)g * D;
   const __bf16* vtree = a.vt + (size_t)b * a.N * krow + (size_t)g * D;
 
@@ -521,8 +552,17 @@ void attn_main(AttnArgs a) {
     const int r = (q % TL::kDma) * TL::kRowsPerDma + lane / TL::kCPR;
     dma_off[k] = (uint32_t)(r * (int)krow * 2 + ((lane % TL::kCPR) ^ TL::swz(r)) * 16);
   }
-  const TreeSrc src{(const char*)kcache, (const char*)vcache, (const char*)ktree,
-                    (const char*)vtree, (int)krow * 2, kvl, nct, i_hi};
+  const TreeSrc src{(const char*)kcache,
+                    (const char*)vcache,
+                    (const char*)ktree,
+                    (const char*)vtree,
+                    kPaged ? a.block_table + (size_t)b * a.max_blocks : nullptr,
+                    a.block_shift,
+                    a.num_blocks,
+                    (int)krow * 2,
+                    kvl,
+                    nct,
+                    i_hi};
 
   // iteration i handles tile t0 + wk + WK*i of this wave's key group; all
   // waves run n_iter iterations so the per-iteration barriers line up
@@ -530,7 +570,7 @@ void attn_main(AttnArgs a) {
   const int n_mine = t0 + wk < t1 ? (t1 - t0 - wk + WK - 1) / WK : 0;  // valid tiles
 #pragma unroll
   for (int i = 0; i < NS - 1; ++i)
-    if (i < n_mine) issue_tile<D, PW>(src, dma_off, wr, lane, t0 + wk + WK * i, ring + i * STAGE);
+    if (i < n_mine) issue_tile<D, PW, kPaged>(src, dma_off, wr, lane, t0 + wk + WK * i, ring + i * STAGE);
 
   // ---- queries: B operand of S^T = K Q^T, lane holds Q[row l16][8*g4 .. +8]
   const int wrow0 = r0 + kRowsPerWave * wr;
@@ -615,11 +655,11 @@ void attn_main(AttnArgs a) {
       if (mine) wait_vm_dyn(min(n_mine - 1 - i, NS - 2) * PW);
       __syncthreads();
       if (i + NS - 1 < n_mine)
-        issue_tile<D, PW>(src, dma_off, wr, lane, t0 + wk + WK * (i + NS - 1),
+        issue_tile<D, PW, kPaged>(src, dma_off, wr, lane, t0 + wk + WK * (i + NS - 1),
                           ring + ((i + NS - 1) % NS) * STAGE);
     } else {
       if (i + NS - 1 < n_mine)
-        issue_tile<D, PW>(src, dma_off, wr, lane, t0 + wk + WK * (i + NS - 1),
+        issue_tile<D, PW, kPaged>(src, dma_off, wr, lane, t0 + wk + WK * (i + NS - 1),
                           ring + ((i + NS - 1) % NS) * STAGE);
       if (mine) wait_vm_dyn(min(n_mine - 1 - i, NS - 1) * PW);
     }
@@ -807,18 +847,18 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
              bad != 0);
 }
 
-template <int D, int ARR>
+template <int D, int ARR, bool kPaged>
 static hipError_t launch_attn_t(const AttnArgs& a, const AttnPlan& p, hipStream_t st) {
   constexpr Arrangement ar = kArrangements[ARR];
   constexpr int NS = arr_stages(ar, D);
   if constexpr (NS == 0) {
     return hipErrorInvalidValue;  // never planned: the ring does not fit
   } else {
-    hipError_t e = hipFuncSetAttribute((const void*)attn_main<D, ar.WR, ar.WK, NS>,
+    hipError_t e = hipFuncSetAttribute((const void*)attn_main<D, ar.WR, ar.WK, NS, kPaged>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)p.lds_bytes);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((attn_main<D, ar.WR, ar.WK, NS>), dim3(p.grid), dim3(64 * ar.WR * ar.WK),
+    hipLaunchKernelGGL((attn_main<D, ar.WR, ar.WK, NS, kPaged>), dim3(p.grid), dim3(64 * ar.WR * ar.WK),
                        p.lds_bytes, st, a);
     e = hipGetLastError();
     if (e != hipSuccess || p.S == 1 || p.fused) return e;
@@ -832,7 +872,9 @@ static hipError_t launch_attn_t(const AttnArgs& a, const AttnPlan& p, hipStream_
 template <int D, int K = 0>
 static hipError_t launch_attn_d(const AttnArgs& a, const AttnPlan& p, hipStream_t st) {
   if constexpr (K < kNumArrangements) {
-    if (p.arr == K) return launch_attn_t<D, K>(a, p, st);
+    if (p.arr == K)
+      return a.block_table ? launch_attn_t<D, K, true>(a, p, st)
+                           : launch_attn_t<D, K, false>(a, p, st);
     return launch_attn_d<D, K + 1>(a, p, st);
   } else {
     return hipErrorInvalidValue;
@@ -842,8 +884,14 @@ static hipError_t launch_attn_d(const AttnArgs& a, const AttnPlan& p, hipStream_
 hipError_t launch_attention(const void* q, const void* kc, const void* vc, const void* kt,
                             const void* vt, const int32_t* parent, const int32_t* kv_len,
                             void* out, int B, int N, int Hq, int Hkv, int D, int Lmax,
-                            float scale, void* ws, const AttnPlan& p, hipStream_t st) {
+                            float scale, void* ws, const AttnPlan& p, hipStream_t st,
+                            const int32_t* block_table, int block_shift, int max_blocks,
+                            int num_blocks) {
   AttnArgs a;
+  a.block_table = block_table;
+  a.block_shift = block_shift;
+  a.max_blocks = max_blocks;
+  a.num_blocks = num_blocks;
   a.q = (const __bf16*)q;
   a.kc = (const __bf16*)kc;
   a.vc = (const __bf16*)vc;

@@ -227,3 +227,35 @@ def draft_logits(w: Workload, seed: Optional[int] = None) -> np.ndarray:
 
 def with_shape(w: Workload, **kw) -> Workload:
     return replace(w, **kw)
+
+
+def block_table(rng: np.random.Generator, B: int, max_blocks: int, spare: int = 0,
+                used=None) -> Tuple[np.ndarray, int]:
+    """A shuffled paged-cache block table: every sequence gets max_blocks
+    distinct pool blocks drawn from a pool of B * max_blocks + spare blocks.
+    With ``used`` ([B] block counts), entries past a sequence's used blocks
+    are -1 (unallocated).  Returns (table [B, max_blocks] int32, num_blocks)."""
+    num_blocks = B * max_blocks + spare
+    bt = rng.permutation(num_blocks)[:B * max_blocks].astype(np.int32).reshape(B, max_blocks)
+    if used is not None:
+        for b in range(B):
+            bt[b, int(used[b]):] = -1
+    return bt, num_blocks
+
+
+def scatter_pool(rng: np.random.Generator, cache: np.ndarray, bt: np.ndarray, num_blocks: int,
+                 block_size: int) -> np.ndarray:
+    """Lay a contiguous cache [B, Lmax, ...] out as a pool [num_blocks,
+    block_size, ...]: rows j*block_size.. of sequence b go to block bt[b, j]
+    (entries < 0 are skipped, as are rows past Lmax).  Blocks no sequence
+    owns hold random bf16 values."""
+    B, Lmax = cache.shape[:2]
+    pool = _normal_bf16(rng, (num_blocks, block_size) + cache.shape[2:])
+    for b in range(B):
+        for j in range(bt.shape[1]):
+            lo = j * block_size
+            if bt[b, j] < 0 or lo >= Lmax:
+                continue
+            hi = min(lo + block_size, Lmax)
+            pool[bt[b, j], :hi - lo] = cache[b, lo:hi]
+    return pool

@@ -28,7 +28,8 @@ def test_header_declares_the_api():
     names = _declared()
     for n in ["tv_tree_verify_attention", "tv_tree_accept", "tv_tree_verify_attention_workspace",
               "tv_tree_accept_workspace", "tv_status_string", "tv_version",
-              "tv_draft_topw", "tv_draft_topw_workspace", "tv_build_tree"]:
+              "tv_draft_topw", "tv_draft_topw_workspace", "tv_build_tree",
+              "tv_tree_verify_attention_paged", "tv_commit_path", "tv_commit_path_paged"]:
         assert n in names
 
 
@@ -162,3 +163,67 @@ def test_drafting_host_errors():
     assert _build(lib, budget=2049) == -4
     assert _build(lib, W=17) == -4
     assert _build(lib, Nd=65) == -4
+
+
+def _attn_paged(lib, **kw):
+    a = dict(q=FAKE, kp=FAKE, vp=FAKE, bt=FAKE, bs=256, mb=16, nb=64, kt=FAKE, vt=FAKE,
+             parent=FAKE, kv_len=None, out=FAKE, B=1, N=64, Hq=32, Hkv=8, D=128, scale=0.0,
+             ws=FAKE, wsb=1 << 40)
+    a.update(kw)
+    return lib.tv_tree_verify_attention_paged(
+        a["q"], a["kp"], a["vp"], a["bt"], a["bs"], a["mb"], a["nb"], a["kt"], a["vt"],
+        a["parent"], a["kv_len"], a["out"], a["B"], a["N"], a["Hq"], a["Hkv"], a["D"],
+        ctypes.c_float(a["scale"]), a["ws"], a["wsb"], None)
+
+
+def test_paged_attention_host_errors():
+    lib = _lib()
+    assert _attn_paged(lib, bs=48) == -2          # not a power of two
+    assert _attn_paged(lib, bs=16) == -2          # below the smallest block
+    assert _attn_paged(lib, mb=-1) == -2
+    assert _attn_paged(lib, nb=-1) == -2
+    assert _attn_paged(lib, bt=None) == -1
+    assert _attn_paged(lib, nb=0) == -1           # a cache but no pool
+    assert _attn_paged(lib, kp=None) == -1
+    assert _attn_paged(lib, q=None) == -1
+    assert _attn_paged(lib, Hq=30) == -2
+    assert _attn_paged(lib, D=96) == -4
+    assert _attn_paged(lib, kp=FAKE + 8) == -7
+    assert _attn_paged(lib, ws=None) == -5
+    assert _attn_paged(lib, mb=1 << 20, bs=1 << 11) == -4   # capacity above 2^30
+
+
+def _commit(lib, **kw):
+    a = dict(kt=FAKE, vt=FAKE, path=FAKE, ln=FAKE, kc=FAKE, vc=FAKE, kvl=FAKE, B=1, N=64,
+             Hkv=8, D=128, Lmax=4096, Dmax=9)
+    a.update(kw)
+    return lib.tv_commit_path(a["kt"], a["vt"], a["path"], a["ln"], a["kc"], a["vc"], a["kvl"],
+                              a["B"], a["N"], a["Hkv"], a["D"], a["Lmax"], a["Dmax"], None)
+
+
+def _commit_paged(lib, **kw):
+    a = dict(kt=FAKE, vt=FAKE, path=FAKE, ln=FAKE, kp=FAKE, vp=FAKE, bt=FAKE, bs=256, mb=16,
+             nb=64, kvl=FAKE, B=1, N=64, Hkv=8, D=128, Dmax=9)
+    a.update(kw)
+    return lib.tv_commit_path_paged(a["kt"], a["vt"], a["path"], a["ln"], a["kp"], a["vp"],
+                                    a["bt"], a["bs"], a["mb"], a["nb"], a["kvl"], a["B"],
+                                    a["N"], a["Hkv"], a["D"], a["Dmax"], None)
+
+
+def test_commit_host_errors():
+    lib = _lib()
+    assert _commit(lib, kt=None) == -1
+    assert _commit(lib, path=None) == -1
+    assert _commit(lib, kvl=None) == -1
+    assert _commit(lib, B=0) == -2
+    assert _commit(lib, Lmax=0) == -2
+    assert _commit(lib, Dmax=0) == -2
+    assert _commit(lib, D=96) == -4
+    assert _commit(lib, N=2049) == -4
+    assert _commit(lib, kc=FAKE + 8) == -7
+    assert _commit_paged(lib, bt=None) == -1
+    assert _commit_paged(lib, bs=100) == -2
+    assert _commit_paged(lib, mb=0) == -2
+    assert _commit_paged(lib, nb=0) == -2
+    assert _commit_paged(lib, vp=FAKE + 2) == -7
+    assert _commit_paged(lib, D=80) == -4

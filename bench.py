@@ -30,6 +30,7 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 MALL_BYTES = 256 << 20
+PAGE_BLOCK = 64                # rows per paged-cache block in the paged timing
 
 
 def parse():
@@ -44,10 +45,145 @@ def parse():
     ap.add_argument("--copy-only", action="store_true",
                     help="only run 10 plain device copies of 256 MiB (calibrates the HBM "
                          "traffic counters: each copy reads and writes exactly 256 MiB)")
+    ap.add_argument("--summarize-traffic", nargs=4, default=None,
+                    metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
+                    help="no GPU: turn the counter CSVs of four rocprofv3 --pmc runs (FETCH_SIZE "
+                         "and WRITE_SIZE of this benchmark, then of --copy-only) into "
+                         "profiles/traffic_attn_main_<workload>.json and .md")
+    ap.add_argument("--summarize-trace", nargs=2, default=None, metavar=("TRACE_DIR", "BENCH_LOG"),
+                    help="no GPU: turn a rocprofv3 --kernel-trace --stats run of this benchmark and "
+                         "the log of the same command run without the profiler into "
+                         "profiles/kernel_trace_<workload>.md")
     return ap.parse_args()
 
 
 COPY_BYTES = 256 << 20
+
+
+def _counter_rows(d, counter):
+    import csv
+    import glob
+    rows = []
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(f) as fh:
+            rows += [r for r in csv.DictReader(fh) if r["Counter_Name"] == counter]
+    if not rows:
+        raise SystemExit(f"no {counter} rows under {d}")
+    return rows
+
+
+def summarize_traffic(dirs, workload):
+    """HBM bytes per launch of the contiguous-cache attention kernel from
+    FETCH_SIZE / WRITE_SIZE (KiB per dispatch), each scaled by what the same
+    counter reads for a 256 MiB device copy."""
+    import re
+    import statistics
+    pat = re.compile(r"attn_main<(\d+), (\d+), (\d+), (\d+)(?:, false)?>")
+    med, names, n = {}, set(), {}
+    for d, c in zip(dirs[:2], ["FETCH_SIZE", "WRITE_SIZE"]):
+        vals = []
+        for r in _counter_rows(d, c):
+            m = pat.search(r["Kernel_Name"])
+            if m:
+                vals.append(float(r["Counter_Value"]))
+                names.add("attn_main<%s,%s,%s,%s>" % m.groups())
+        if not vals:
+            raise SystemExit(f"no contiguous attn_main dispatches in {d}")
+        med[c], n[c] = statistics.median(vals), len(vals)
+    if len(names) != 1:
+        raise SystemExit(f"expected one attn_main instantiation, got {sorted(names)}")
+    cal = {}
+    for d, c in zip(dirs[2:], ["FETCH_SIZE", "WRITE_SIZE"]):
+        vals = [float(r["Counter_Value"]) for r in _counter_rows(d, c)
+                if "copyBuffer" in r["Kernel_Name"] or "copy" in r["Kernel_Name"].lower()]
+        cal[c] = statistics.median(vals)
+    kib = COPY_BYTES / 1024
+    fs, ws = kib / cal["FETCH_SIZE"], kib / cal["WRITE_SIZE"]
+    fetch_b = med["FETCH_SIZE"] * fs * 1024
+    write_b = med["WRITE_SIZE"] * ws * 1024
+    kernel = names.pop()
+    rec = {"kernel": kernel, "workload": workload,
+           "fetch_kib_per_dispatch": med["FETCH_SIZE"], "write_kib_per_dispatch": med["WRITE_SIZE"],
+           "dispatches": n,
+           "copy_calibration": {"bytes": COPY_BYTES, "fetch_kib": cal["FETCH_SIZE"],
+                                "write_kib": cal["WRITE_SIZE"], "fetch_scale": round(fs, 4),
+                                "write_scale": round(ws, 4)},
+           "hbm_bytes_per_launch": int(round(fetch_b + write_b)),
+           "kernel_src_sha": kernel_source_sha()}
+    base = os.path.join(ROOT, "profiles", f"traffic_attn_main_{workload}")
+    with open(base + ".json", "w") as fh:
+        json.dump(rec, fh, indent=1)
+        fh.write("\n")
+    with open(base + ".md", "w") as fh:
+        fh.write(f"""# HBM traffic: {kernel}, workload {workload}
+
+Commands (repository root, rocprofv3 run from /tmp with TMPDIR=/tmp; one counter per run):
+
+    rocprofv3 --pmc FETCH_SIZE --output-format csv -d <f> -o b -- python3 bench.py --workload {workload} --no-cpu-baseline --steps 40 --warmup 5
+    rocprofv3 --pmc WRITE_SIZE --output-format csv -d <w> -o b -- python3 bench.py --workload {workload} --no-cpu-baseline --steps 40 --warmup 5
+    rocprofv3 --pmc FETCH_SIZE --output-format csv -d <cf> -o c -- python3 bench.py --copy-only
+    rocprofv3 --pmc WRITE_SIZE --output-format csv -d <cw> -o c -- python3 bench.py --copy-only
+    python3 bench.py --workload {workload} --summarize-traffic <f> <w> <cf> <cw>
+
+Calibration: a plain {COPY_BYTES >> 20} MiB device copy reads FETCH_SIZE = {cal['FETCH_SIZE']:.1f} KiB
+and WRITE_SIZE = {cal['WRITE_SIZE']:.1f} KiB per dispatch against {kib:.0f} KiB moved each way, so
+the scale factors are {fs:.4f} (fetch) and {ws:.4f} (write).
+
+| counter | raw KiB / dispatch (median of {n['FETCH_SIZE']}) | scaled MB |
+|---|---|---|
+| FETCH_SIZE | {med['FETCH_SIZE']:.1f} | {fetch_b / 1e6:.2f} |
+| WRITE_SIZE | {med['WRITE_SIZE']:.1f} | {write_b / 1e6:.2f} |
+| total | | {(fetch_b + write_b) / 1e6:.2f} |
+""")
+    print(json.dumps(rec))
+
+
+def summarize_trace(trace_dir, bench_log, workload):
+    """Kernel-time table from rocprofv3's kernel stats, beside the event-timed
+    figures of the same command run without the profiler."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)
+    if len(files) != 1:
+        raise SystemExit(f"expected one kernel_stats.csv under {trace_dir}, got {files}")
+    with open(files[0]) as fh:
+        rows = list(csv.DictReader(fh))
+    line = None
+    with open(bench_log) as fh:
+        for ln in fh:
+            if ln.startswith("{") and '"metric"' in ln:
+                line = json.loads(ln)
+    if line is None or line["config"]["workload"] != workload:
+        raise SystemExit(f"no bench line for {workload} in {bench_log}")
+    c, d = line["config"], line["detail"]
+    out = [f"# Kernel trace: workload {workload} (B={c['B']}, Hq={c['Hq']}, Hkv={c['Hkv']}, "
+           f"D={c['D']}, L={c['Lmax']}, N={c['N']}, V={c['V']} {c['logits']})", "",
+           "Command (repository root; rocprofv3 run from /tmp with TMPDIR=/tmp):", "",
+           f"    rocprofv3 --kernel-trace --stats --output-format csv -d <out> -o bench -- "
+           f"python3 bench.py --workload {workload} --no-cpu-baseline",
+           f"    python3 bench.py --workload {workload} --summarize-trace <out> <log of the same "
+           f"bench.py command without the profiler>", "",
+           "Calls include warm-up, graph capture and every timed graph (step, attention, "
+           "acceptance, draft top-W, tree build, paged attention, path commit).", "",
+           "| kernel | calls | avg us | min us | max us | % of GPU time |",
+           "|---|---|---|---|---|---|"]
+    for r in rows:
+        name = r["Name"] if len(r["Name"]) <= 72 else r["Name"][:69] + "..."
+        out.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                   f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
+                   f"{float(r['Percentage']):.2f} |")
+    out += ["", "Same command without the profiler (HIP events around graph replays on the "
+            "launch stream):", "",
+            f"    step {d['us_per_step']:.2f} us = attention {d['attention_us']:.2f} us + "
+            f"acceptance {d['accept_us']:.2f} us",
+            f"    drafting (not in the step): top-W {d['draft_topw_us']:.2f} us, tree build "
+            f"{d['build_tree_us']:.2f} us",
+            f"    paged attention ({d['page_block']}-row blocks) {d['paged_attention_us']:.2f} us, "
+            f"path commit {d['commit_us']:.2f} us", ""]
+    path = os.path.join(ROOT, "profiles", f"kernel_trace_{workload}.md")
+    with open(path, "w") as fh:
+        fh.write("\n".join(out))
+    print(path)
 
 
 def copy_only():
@@ -141,6 +277,12 @@ def cpu_baseline(inp, w, draft, budget_s):
 
 def main():
     args = parse()
+    if args.summarize_traffic:
+        summarize_traffic(args.summarize_traffic, args.workload)
+        return
+    if args.summarize_trace:
+        summarize_trace(*args.summarize_trace, args.workload)
+        return
     if args.copy_only:
         copy_only()
         return
@@ -150,7 +292,8 @@ def main():
         sys.exit(2)
 
     import torch
-    from paper_2606_18394_amd import build_tree, draft_topw, synth, tree_accept, tree_verify_attention
+    from paper_2606_18394_amd import (build_tree, commit_path, draft_topw, synth, tree_accept,
+                                      tree_verify_attention, tree_verify_attention_paged)
     from paper_2606_18394_amd.binding import load_library
 
     load_library()
@@ -216,6 +359,37 @@ def main():
     def topw(r):
         draft_topw(dlogs[r], Wd, tok=dtok, logp=dlp)
 
+    # The serving side, timed apart: the same attention over a paged cache
+    # (shuffled blocks of PAGE_BLOCK rows), and committing the accepted path
+    # (kv_len is reset from a copy first, so every replay commits the same
+    # rows; the reset alone is timed too and subtracted).
+    prng = np.random.default_rng(w.seed + 77)
+    mb = -(-w.L // PAGE_BLOCK)
+    btab, nblk = synth.block_table(prng, w.B, mb, spare=7)
+    kpool0 = bf(synth.scatter_pool(prng, inp["k_cache"], btab, nblk, PAGE_BLOCK))
+    vpool0 = bf(synth.scatter_pool(prng, inp["v_cache"], btab, nblk, PAGE_BLOCK))
+    pools = [(kpool0, vpool0)] + [(kpool0.clone(), vpool0.clone()) for _ in range(R - 1)]
+    btab_d = i32(btab)
+
+    def attn_paged(r):
+        kp, vp = pools[r]
+        x = reps[r]
+        tree_verify_attention_paged(x["q"], kp, vp, btab_d, x["kt"], x["vt"], parent, outs[r],
+                                    kv_len=kv_len, workspace_tensor=ws_attn)
+
+    ccap = w.L + w.Dmax
+    ckc = torch.zeros(w.B, ccap, w.Hkv, w.D, dtype=torch.bfloat16, device=dev)
+    cvc = torch.zeros_like(ckc)
+    ckl0 = kv_len.clone()
+    ckl = kv_len.clone()
+
+    def reset(r):
+        ckl.copy_(ckl0)
+
+    def commit(r):
+        reset(r)
+        commit_path(reps[r]["kt"], reps[r]["vt"], path, acc_len, ckc, cvc, ckl)
+
     def build(r):
         build_tree(dtok, dlp, w.N)
 
@@ -242,7 +416,8 @@ def main():
         topw(s % R)
         build(s % R)
     for name, fn in [("step", step), ("attn", attn), ("accept", accept), ("topw", topw),
-                     ("build", build)]:
+                     ("build", build), ("attn_paged", attn_paged), ("reset", reset),
+                     ("commit", commit)]:
         graphs[name] = (capture(fn, range(R)), [capture(fn, [r]) for r in range(R)])
     torch.cuda.synchronize()
     print(f"[bench] {w.name}: {R} replicas of {per_rep / 2**20:.1f} MiB; warmup done, "
@@ -268,6 +443,13 @@ def main():
     ms_acc = timed("accept", args.steps)
     ms_topw = timed("topw", args.steps)
     ms_build = timed("build", args.steps)
+    ms_paged = timed("attn_paged", args.steps)
+    ms_commit = max(0.0, timed("commit", args.steps) - timed("reset", args.steps))
+    attn(0)
+    ref0 = outs[0].clone()
+    attn_paged(0)
+    torch.cuda.synchronize()
+    paged_same = bool(torch.equal(outs[0].view(torch.int16), ref0.view(torch.int16)))
     print(f"[bench] step {ms_step * 1e3:.2f} us, attention {ms_attn * 1e3:.2f} us, "
           f"accept {ms_acc * 1e3:.2f} us", file=sys.stderr, flush=True)
 
@@ -324,7 +506,11 @@ def main():
                    "attention_TFLOPs": attn_flops / (ms_attn * 1e-3) / 1e12,
                    "accept_GBps": acc_bytes / (ms_acc * 1e-3) / 1e9,
                    "draft_topw_us": ms_topw * 1e3, "build_tree_us": ms_build * 1e3,
-                   "draft": {"depth": w.depth, "width": Wd, "budget": w.N}},
+                   "draft": {"depth": w.depth, "width": Wd, "budget": w.N},
+                   "paged_attention_us": ms_paged * 1e3, "page_block": PAGE_BLOCK,
+                   "paged_bit_identical": paged_same,
+                   "paged_attention_GBps": attn_bytes / (ms_paged * 1e-3) / 1e9,
+                   "commit_us": ms_commit * 1e3, "commit_rows": int(acc_len.sum().item())},
     }
     print(json.dumps(line), flush=True)
 

@@ -215,8 +215,11 @@ __device__ __forceinline__ void issue_tile(const TreeSrc& src, const uint32_t (&
   if constexpr (kPaged) {
     size_t tofs = (size_t)first * src.row_bytes;
     if (cache) {
-      // wave-uniform: the tile index is, so the block is
-      int blk = __builtin_amdgcn_readfirstlane(src.btab[first >> src.shift]);
+      // A scalar load through the constant address space (the table is
+      // read-only here and the tile index wave-uniform): a vector load
+      // would make the compiler wait for every DMA in flight.
+      typedef const __attribute__((address_space(4))) int32_t ctab_t;
+      int blk = ((ctab_t*)src.btab)[__builtin_amdgcn_readfirstlane(first >> src.shift)];
       blk = blk < 0 ? 0 : (blk >= src.nblk ? src.nblk - 1 : blk);
       tofs = (((size_t)blk << src.shift) + (first & ((1 << src.shift) - 1))) * src.row_bytes;
     }

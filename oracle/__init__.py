@@ -14,7 +14,7 @@ Contents
   build_tree         and best-first expansion by accumulated draft
                      log-probability (Sec. 2.4 parallel tree drafting; Alg. 1).
   kv_commit       -- the cache side: committing the accepted path, paged
-                     caches (App. E).
+                     caches, the tree-tail layout (App. E).
   brute           -- pure-Python loop versions for tiny inputs, used only to
                      pin the functions above.
 
@@ -25,8 +25,9 @@ from .tree_attention import (decode_bf16, tree_structure, full_mask,
                              tree_attention)
 from .tree_accept import target_argmax, tree_accept
 from .tree_build import draft_topw, build_tree
-from .kv_commit import commit_path, gather_paged, commit_path_paged
+from .kv_commit import commit_path, gather_paged, commit_path_paged, tree_tail, commit_path_tail
 
 __all__ = ["decode_bf16", "tree_structure", "full_mask", "tree_attention",
            "target_argmax", "tree_accept", "draft_topw", "build_tree",
-           "commit_path", "gather_paged", "commit_path_paged"]
+           "commit_path", "gather_paged", "commit_path_paged", "tree_tail",
+           "commit_path_tail"]

@@ -9,7 +9,9 @@ Independent constructions used to pin the oracle:
     (length, then lowest end node);
   * top-W: Python sort on (value, index) and an exactly summed log-sum-exp;
   * tree building: the full W-ary tree is enumerated and its nodes visited in
-    descending score order, with no priority queue.
+    descending score order, with no priority queue;
+  * tree-tail commit: rows moved in place one at a time, with no snapshot of
+    the tree rows.
 """
 from __future__ import annotations
 
@@ -158,3 +160,19 @@ def tree_in_score_order(tok, logp, budget):
             depth.append(len(c))
             score.append(full[c])
     return parent, token, depth, score
+
+
+def commit_tail_in_place(cache, path, accept_len, kv_len):
+    """Tree-tail commit done in place, one row at a time in increasing
+    order: row kv_len + j takes row kv_len + path[j].  Correct because a
+    root-to-node path has path[j] >= j (a node's index exceeds its depth),
+    so no row is read after it was overwritten."""
+    c = [[row.copy() for row in seq] for seq in np.asarray(cache)]
+    for b in range(len(c)):
+        n = int(accept_len[b])
+        if n < 1:
+            continue
+        kl = int(kv_len[b])
+        for j in range(n):
+            c[b][kl + j] = c[b][kl + int(path[b][j])].copy()
+    return np.array(c)

@@ -8,6 +8,11 @@ committed to the cache, and the verification kernel reads a paged cache):
                 kv_len + accept_len - 1, and kv_len grows by accept_len.
   gather_paged  the contiguous cache that a paged cache (a pool of fixed-size
                 blocks and a per-sequence block table) stands for.
+  tree_tail,    the tree-tail layout, in which the draft nodes' K/V were
+  commit_path_tail  written to the cache right after the context (node i at
+                position kv_len + i) before verification: the tree K/V are
+                that slice, and committing moves the accepted path's rows
+                down to kv_len .. kv_len + accept_len - 1.
 
 Readings where the paper is silent:
   * the root (the token sampled by the previous step) is committed with the
@@ -15,7 +20,9 @@ Readings where the paper is silent:
   * a sequence whose acceptance failed (accept_len < 1) or whose commit would
     pass the cache capacity is left unchanged (cache and kv_len);
   * paged caches use blocks of block_size consecutive positions; logical
-    block j of sequence b is pool block block_table[b, j].
+    block j of sequence b is pool block block_table[b, j];
+  * in the tree-tail layout a sequence needs kv_len + N <= capacity; a
+    sequence with less room is left unchanged by the commit.
 """
 from __future__ import annotations
 
@@ -76,3 +83,28 @@ def commit_path_paged(k_pool, v_pool, block_table, k_tree, v_tree, path, accept_
             vp[bt[b, t // bs], t % bs] = v_tree[b, node]
         kl[b] += n
     return kp, vp, kl
+
+
+def tree_tail(cache, kv_len, n_nodes):
+    """Tree-tail layout: the [B, N, ...] tree K (or V) a contiguous cache holds
+    at positions kv_len[b] .. kv_len[b] + N - 1."""
+    cache = np.asarray(cache)
+    out = np.empty((cache.shape[0], n_nodes) + cache.shape[2:], dtype=cache.dtype)
+    for b in range(cache.shape[0]):
+        kl = int(kv_len[b])
+        out[b] = cache[b, kl:kl + n_nodes]
+    return out
+
+
+def commit_path_tail(k_cache, v_cache, path, accept_len, kv_len, n_nodes):
+    """commit_path in the tree-tail layout: the tree K/V are the cache rows
+    kv_len .. kv_len + N - 1 as they are before the commit.  Returns new
+    copies (k_cache, v_cache, kv_len)."""
+    Lmax = np.asarray(k_cache).shape[1]
+    kl = np.asarray(kv_len, dtype=np.int64)
+    room = kl + n_nodes <= Lmax
+    safe_kl = np.where(room, kl, 0)                 # only read where there is room
+    kt = tree_tail(k_cache, safe_kl, n_nodes)
+    vt = tree_tail(v_cache, safe_kl, n_nodes)
+    n = np.where(room, np.asarray(accept_len), 0)   # no room: left unchanged
+    return commit_path(k_cache, v_cache, kt, vt, path, n, kv_len)

@@ -84,3 +84,67 @@ def test_gather_paged_elementwise():
     for b in range(2):
         for t in range(12):
             np.testing.assert_array_equal(g[b, t], pool[bt[b, t // 4], t % 4])
+
+
+def _tree_paths(rng, B, N):
+    """Random trees (parent before child) and one root-to-node path each,
+    root first, padded with -1 to N entries."""
+    from paper_2606_18394_amd import synth
+    par = np.stack([synth.random_tree(rng, N, depth=min(N - 1, 6), branching=3)
+                    for _ in range(B)])
+    path = np.full((B, N), -1)
+    n = np.zeros(B, dtype=np.int64)
+    for b in range(B):
+        u, p = int(rng.integers(0, N)), []
+        while u != -1:
+            p.append(u)
+            u = int(par[b, u])
+        p.reverse()
+        path[b, :len(p)] = p
+        n[b] = len(p)
+    return par, path, n
+
+
+def test_tree_tail_is_the_slice_after_the_context():
+    rng = np.random.default_rng(11)
+    c = rng.normal(size=(2, 20, 1, 3))
+    t = kv_commit.tree_tail(c, np.array([4, 11]), 6)
+    for b, kl in enumerate([4, 11]):
+        for i in range(6):
+            np.testing.assert_array_equal(t[b, i], c[b, kl + i])
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_tail_commit_matches_in_place_moves(seed):
+    from oracle import brute
+    rng = np.random.default_rng(100 + seed)
+    B, N, Lmax = 4, 12, 40
+    _, path, n = _tree_paths(rng, B, N)
+    kc = rng.normal(size=(B, Lmax, 2, 3))
+    vc = rng.normal(size=(B, Lmax, 2, 3))
+    kl = rng.integers(0, Lmax - N + 1, size=B)
+    nk, nv, nl = kv_commit.commit_path_tail(kc, vc, path, n, kl, N)
+    np.testing.assert_array_equal(nk, brute.commit_tail_in_place(kc, path, n, kl))
+    np.testing.assert_array_equal(nv, brute.commit_tail_in_place(vc, path, n, kl))
+    np.testing.assert_array_equal(nl, kl + n)
+
+
+def test_tail_commit_reads_rows_before_overwriting_them():
+    """path [0, 2, 5]: row kl+1 takes row kl+2, which row kl+2 then takes
+    from row kl+5; a commit that wrote before reading would copy the wrong
+    row into kl+1."""
+    c = np.arange(10, dtype=float).reshape(1, 10, 1, 1)
+    nk, _, nl = kv_commit.commit_path_tail(c, c, np.array([[0, 2, 5]]), np.array([3]),
+                                           np.array([2]), 6)
+    assert nk[0, :, 0, 0].tolist() == [0, 1, 2, 4, 7, 5, 6, 7, 8, 9]
+    assert nl.tolist() == [5]
+
+
+def test_tail_commit_without_room_leaves_the_sequence():
+    rng = np.random.default_rng(3)
+    c = rng.normal(size=(2, 10, 1, 2))
+    path = np.array([[0, 1, -1], [0, 1, 2]])
+    nk, _, nl = kv_commit.commit_path_tail(c, c, path, np.array([2, 3]), np.array([5, 4]), 6)
+    np.testing.assert_array_equal(nk[0], c[0])      # 5 + 6 > 10: no room for the tree
+    assert nl.tolist() == [5, 7]
+    np.testing.assert_array_equal(nk[1, 4:7], c[1, [4, 5, 6]])

@@ -164,7 +164,8 @@ def summarize_trace(trace_dir, bench_log, workload):
            f"    python3 bench.py --workload {workload} --summarize-trace <out> <log of the same "
            f"bench.py command without the profiler>", "",
            "Calls include warm-up, graph capture and every timed graph (step, attention, "
-           "acceptance, draft top-W, tree build, paged attention, path commit).", "",
+           "acceptance, draft top-W, tree build, paged attention, tree-tail attention, path "
+           "commit).", "",
            "| kernel | calls | avg us | min us | max us | % of GPU time |",
            "|---|---|---|---|---|---|"]
     for r in rows:
@@ -179,6 +180,7 @@ def summarize_trace(trace_dir, bench_log, workload):
             f"    drafting (not in the step): top-W {d['draft_topw_us']:.2f} us, tree build "
             f"{d['build_tree_us']:.2f} us",
             f"    paged attention ({d['page_block']}-row blocks) {d['paged_attention_us']:.2f} us, "
+            f"tree-tail attention {d['tree_tail_attention_us']:.2f} us, "
             f"path commit {d['commit_us']:.2f} us", ""]
     path = os.path.join(ROOT, "profiles", f"kernel_trace_{workload}.md")
     with open(path, "w") as fh:
@@ -377,6 +379,28 @@ def main():
         tree_verify_attention_paged(x["q"], kp, vp, btab_d, x["kt"], x["vt"], parent, outs[r],
                                     kv_len=kv_len, workspace_tensor=ws_attn)
 
+    # tree-tail layout: the tree's K/V written into the cache after the context
+    kt_np, vt_np = inp["k_tree"], inp["v_tree"]
+    tk = np.concatenate([inp["k_cache"], np.zeros((w.B, w.N) + inp["k_cache"].shape[2:],
+                                                  inp["k_cache"].dtype)], axis=1)
+    tv = np.concatenate([inp["v_cache"], np.zeros_like(tk[:, :w.N])], axis=1)
+    for b in range(w.B):
+        kl = int(inp["kv_len"][b])
+        tk[b, kl:kl + w.N] = kt_np[b]
+        tv[b, kl:kl + w.N] = vt_np[b]
+    tail0 = (bf(tk), bf(tv))
+    tails = [tail0] + [(tail0[0].clone(), tail0[1].clone()) for _ in range(R - 1)]
+    del tk, tv
+
+    def attn_tail(r):
+        kc, vc = tails[r]
+        tree_verify_attention(reps[r]["q"], kc, vc, None, None, parent, outs[r], kv_len=kv_len,
+                              workspace_tensor=ws_tail)
+
+    ws_tail = torch.zeros(
+        max(256, load_library().tv_tree_verify_attention_workspace(
+            w.B, w.N, w.Hq, w.Hkv, w.D, w.L + w.N)), dtype=torch.uint8, device=dev)
+
     ccap = w.L + w.Dmax
     ckc = torch.zeros(w.B, ccap, w.Hkv, w.D, dtype=torch.bfloat16, device=dev)
     cvc = torch.zeros_like(ckc)
@@ -416,7 +440,8 @@ def main():
         topw(s % R)
         build(s % R)
     for name, fn in [("step", step), ("attn", attn), ("accept", accept), ("topw", topw),
-                     ("build", build), ("attn_paged", attn_paged), ("reset", reset),
+                     ("build", build), ("attn_paged", attn_paged), ("attn_tail", attn_tail),
+                     ("reset", reset),
                      ("commit", commit)]:
         graphs[name] = (capture(fn, range(R)), [capture(fn, [r]) for r in range(R)])
     torch.cuda.synchronize()
@@ -444,6 +469,7 @@ def main():
     ms_topw = timed("topw", args.steps)
     ms_build = timed("build", args.steps)
     ms_paged = timed("attn_paged", args.steps)
+    ms_tail = timed("attn_tail", args.steps)
     ms_commit = max(0.0, timed("commit", args.steps) - timed("reset", args.steps))
     attn(0)
     ref0 = outs[0].clone()
@@ -510,6 +536,7 @@ def main():
                    "paged_attention_us": ms_paged * 1e3, "page_block": PAGE_BLOCK,
                    "paged_bit_identical": paged_same,
                    "paged_attention_GBps": attn_bytes / (ms_paged * 1e-3) / 1e9,
+                   "tree_tail_attention_us": ms_tail * 1e3,
                    "commit_us": ms_commit * 1e3, "commit_rows": int(acc_len.sum().item())},
     }
     print(json.dumps(line), flush=True)

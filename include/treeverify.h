@@ -100,6 +100,12 @@ size_t tv_tree_verify_attention_workspace(int B, int N, int Hq, int Hkv, int D,
  * accumulation run in fp32, products of bf16 operands on the matrix cores.
  * Requirements: Hq % Hkv == 0, D in {64, 128}, 1 <= N <= TV_MAX_NODES,
  * B >= 1, Lmax >= 0; visible keys and values must be finite.
+ *
+ * Tree-tail layout (the serving engine wrote the draft nodes' K/V into the
+ * cache right after the context, App. E): pass k_tree = v_tree = NULL.  Node
+ * i's key and value are then cache row kv_len[b] + i; kv_len is clamped to
+ * [0, Lmax - N] (NULL: Lmax - N for all) and Lmax >= N is required
+ * (TV_ERR_SHAPE otherwise).  Exactly one of them NULL is TV_ERR_NULL.
  */
 int tv_tree_verify_attention(const void* q, const void* k_cache,
                              const void* v_cache, const void* k_tree,
@@ -142,6 +148,12 @@ int tv_tree_verify_attention_paged(const void* q, const void* k_pool, const void
  * whose path names a node outside [0, N), or whose commit would pass Lmax,
  * is left unchanged (cache and kv_len).  The tree buffers must not overlap
  * the cache.
+ *
+ * Tree-tail layout (k_tree = v_tree = NULL, as in tv_tree_verify_attention):
+ * node i's K/V are cache row kv_len[b] + i, and the commit moves row
+ * kv_len[b] + path[b, j] to row kv_len[b] + j in place (path must be a
+ * root-to-node path as tv_tree_accept writes it: path[j] >= j).  A sequence
+ * with kv_len[b] + N > Lmax is left unchanged.
  *
  *   k_tree, v_tree  [B, N, Hkv, D] bf16
  *   path [B, Dmax], accept_len [B]   as written by tv_tree_accept

@@ -99,6 +99,15 @@ def _need(t, name, dtype, shape=None, device=None):
         raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
 
 
+def _need_tree(k_tree, v_tree, shape, device):
+    """Tree K/V tensors, or both None (tree-tail layout)."""
+    if (k_tree is None) != (v_tree is None):
+        raise ValueError("k_tree and v_tree must both be given or both be None")
+    if k_tree is not None:
+        _need(k_tree, "k_tree", torch.bfloat16, shape, device)
+        _need(v_tree, "v_tree", torch.bfloat16, shape, device)
+
+
 def workspace(kind: str, nbytes: int, device, stream_ptr: int) -> torch.Tensor:
     """Zero-filled workspace cached per (kind, device, stream); grows as needed."""
     key = (kind, str(device), stream_ptr)
@@ -115,6 +124,8 @@ def tree_verify_attention(q, k_cache, v_cache, k_tree, v_tree, parent, out,
 
     q [B,N,Hq,D], k_cache/v_cache [B,Lmax,Hkv,D], k_tree/v_tree [B,N,Hkv,D]
     (bf16); parent [B,N] int32; kv_len [B] int32 or None; out [B,N,Hq,D].
+    k_tree = v_tree = None selects the tree-tail layout: node i's K/V are
+    cache row kv_len[b] + i.
     """
     lib = load_library()
     B, N, Hq, D = q.shape
@@ -123,8 +134,7 @@ def tree_verify_attention(q, k_cache, v_cache, k_tree, v_tree, parent, out,
     _need(q, "q", torch.bfloat16, device=dev)
     _need(k_cache, "k_cache", torch.bfloat16, (B, Lmax, Hkv, D), dev)
     _need(v_cache, "v_cache", torch.bfloat16, (B, Lmax, Hkv, D), dev)
-    _need(k_tree, "k_tree", torch.bfloat16, (B, N, Hkv, D), dev)
-    _need(v_tree, "v_tree", torch.bfloat16, (B, N, Hkv, D), dev)
+    _need_tree(k_tree, v_tree, (B, N, Hkv, D), dev)
     _need(parent, "parent", torch.int32, (B, N), dev)
     _need(out, "out", torch.bfloat16, (B, N, Hq, D), dev)
     if kv_len is not None:
@@ -158,8 +168,7 @@ def tree_verify_attention_paged(q, k_pool, v_pool, block_table, k_tree, v_tree, 
     _need(k_pool, "k_pool", torch.bfloat16, (num_blocks, bs, Hkv, D), dev)
     _need(v_pool, "v_pool", torch.bfloat16, (num_blocks, bs, Hkv, D), dev)
     _need(block_table, "block_table", torch.int32, (B, max_blocks), dev)
-    _need(k_tree, "k_tree", torch.bfloat16, (B, N, Hkv, D), dev)
-    _need(v_tree, "v_tree", torch.bfloat16, (B, N, Hkv, D), dev)
+    _need_tree(k_tree, v_tree, (B, N, Hkv, D), dev)
     _need(parent, "parent", torch.int32, (B, N), dev)
     _need(out, "out", torch.bfloat16, (B, N, Hq, D), dev)
     if kv_len is not None:
@@ -176,16 +185,25 @@ def tree_verify_attention_paged(q, k_pool, v_pool, block_table, k_tree, v_tree, 
     return out
 
 
-def commit_path(k_tree, v_tree, path, accept_len, k_cache, v_cache, kv_len):
+def _tree_nodes(k_tree, n_nodes):
+    if k_tree is not None:
+        return k_tree.shape[1]
+    if n_nodes is None:
+        raise ValueError("the tree-tail layout (k_tree=None) needs n_nodes")
+    return int(n_nodes)
+
+
+def commit_path(k_tree, v_tree, path, accept_len, k_cache, v_cache, kv_len, n_nodes=None):
     """Append the accepted path's K/V (root first) to the contiguous cache at
     kv_len and advance kv_len, in place.  k_tree/v_tree [B,N,Hkv,D],
-    path [B,Dmax], accept_len [B], k_cache/v_cache [B,Lmax,Hkv,D], kv_len [B]."""
+    path [B,Dmax], accept_len [B], k_cache/v_cache [B,Lmax,Hkv,D], kv_len [B].
+    k_tree = v_tree = None: tree-tail layout (node i at cache row
+    kv_len + i, N = n_nodes); the accepted rows are moved down in place."""
     lib = load_library()
-    B, N, Hkv, D = k_tree.shape
-    Lmax, Dmax = k_cache.shape[1], path.shape[1]
-    dev = k_tree.device
-    _need(k_tree, "k_tree", torch.bfloat16, (B, N, Hkv, D), dev)
-    _need(v_tree, "v_tree", torch.bfloat16, (B, N, Hkv, D), dev)
+    B, Lmax, Hkv, D = k_cache.shape
+    N, Dmax = _tree_nodes(k_tree, n_nodes), path.shape[1]
+    dev = k_cache.device
+    _need_tree(k_tree, v_tree, (B, N, Hkv, D), dev)
     _need(path, "path", torch.int32, (B, Dmax), dev)
     _need(accept_len, "accept_len", torch.int32, (B,), dev)
     _need(k_cache, "k_cache", torch.bfloat16, (B, Lmax, Hkv, D), dev)
@@ -197,16 +215,17 @@ def commit_path(k_tree, v_tree, path, accept_len, k_cache, v_cache, kv_len):
         _ptr(kv_len), B, N, Hkv, D, Lmax, Dmax, ctypes.c_void_p(stream)))
 
 
-def commit_path_paged(k_tree, v_tree, path, accept_len, k_pool, v_pool, block_table, kv_len):
+def commit_path_paged(k_tree, v_tree, path, accept_len, k_pool, v_pool, block_table, kv_len,
+                      n_nodes=None):
     """commit_path into a paged cache (layout as in
-    tree_verify_attention_paged), in place."""
+    tree_verify_attention_paged), in place; tree-tail layout as in
+    commit_path."""
     lib = load_library()
-    B, N, Hkv, D = k_tree.shape
-    num_blocks, bs = k_pool.shape[0], k_pool.shape[1]
-    max_blocks, Dmax = block_table.shape[1], path.shape[1]
-    dev = k_tree.device
-    _need(k_tree, "k_tree", torch.bfloat16, (B, N, Hkv, D), dev)
-    _need(v_tree, "v_tree", torch.bfloat16, (B, N, Hkv, D), dev)
+    num_blocks, bs, Hkv, D = k_pool.shape
+    B, max_blocks = block_table.shape
+    N, Dmax = _tree_nodes(k_tree, n_nodes), path.shape[1]
+    dev = k_pool.device
+    _need_tree(k_tree, v_tree, (B, N, Hkv, D), dev)
     _need(path, "path", torch.int32, (B, Dmax), dev)
     _need(accept_len, "accept_len", torch.int32, (B,), dev)
     _need(k_pool, "k_pool", torch.bfloat16, (num_blocks, bs, Hkv, D), dev)

@@ -51,6 +51,15 @@ static int block_shift(int block_size) {
   return s;
 }
 
+// Tree K/V: both given, or both NULL for the tree-tail layout (node i at
+// cache row kv_len + i), which needs room for the N tree rows in the cache.
+static int check_tree(const void* kt, const void* vt, int N, int Lmax) {
+  if (!kt != !vt) return TV_ERR_NULL;
+  if (!kt && Lmax < N) return TV_ERR_SHAPE;
+  if (misaligned(kt) || misaligned(vt)) return TV_ERR_ALIGN;
+  return TV_OK;
+}
+
 static int check_accept_sizes(int B, int N, int V, int Dmax) {
   if (B < 1 || N < 1 || V < 1 || Dmax < 1) return TV_ERR_SHAPE;
   if (N > TV_MAX_NODES) return TV_ERR_UNSUPPORTED;
@@ -96,9 +105,10 @@ int tv_tree_verify_attention(const void* q, const void* k_cache, const void* v_c
                              size_t workspace_bytes, hipStream_t stream) {
   int rc = check_attention_sizes(B, N, Hq, Hkv, D, Lmax);
   if (rc != TV_OK) return rc;
-  if (!q || !k_tree || !v_tree || !parent || !out) return TV_ERR_NULL;
+  if (!q || !parent || !out) return TV_ERR_NULL;
+  if ((rc = check_tree(k_tree, v_tree, N, Lmax)) != TV_OK) return rc;
   if (Lmax > 0 && (!k_cache || !v_cache)) return TV_ERR_NULL;
-  if (misaligned(q) || misaligned(k_tree) || misaligned(v_tree) || misaligned(out) ||
+  if (misaligned(q) || misaligned(out) ||
       (Lmax > 0 && (misaligned(k_cache) || misaligned(v_cache))))
     return TV_ERR_ALIGN;
   const tv::AttnPlan p = tv::attn_plan(B, N, Hq, Hkv, D, Lmax);
@@ -124,9 +134,10 @@ int tv_tree_verify_attention_paged(const void* q, const void* k_pool, const void
   const int Lmax = max_blocks * block_size;
   int rc = check_attention_sizes(B, N, Hq, Hkv, D, Lmax);
   if (rc != TV_OK) return rc;
-  if (!q || !k_tree || !v_tree || !parent || !out) return TV_ERR_NULL;
+  if (!q || !parent || !out) return TV_ERR_NULL;
+  if ((rc = check_tree(k_tree, v_tree, N, Lmax)) != TV_OK) return rc;
   if (Lmax > 0 && (!k_pool || !v_pool || !block_table || num_blocks < 1)) return TV_ERR_NULL;
-  if (misaligned(q) || misaligned(k_tree) || misaligned(v_tree) || misaligned(out) ||
+  if (misaligned(q) || misaligned(out) ||
       (Lmax > 0 && (misaligned(k_pool) || misaligned(v_pool))))
     return TV_ERR_ALIGN;
   const tv::AttnPlan p = tv::attn_plan(B, N, Hq, Hkv, D, Lmax);
@@ -142,12 +153,14 @@ int tv_tree_verify_attention_paged(const void* q, const void* k_pool, const void
 
 static int check_commit(const void* kt, const void* vt, const int32_t* path,
                         const int32_t* accept_len, const void* kc, const void* vc,
-                        const int32_t* kv_len, int B, int N, int Hkv, int D, int Dmax) {
-  if (B < 1 || N < 1 || Hkv < 1 || Dmax < 1) return TV_ERR_SHAPE;
+                        const int32_t* kv_len, int B, int N, int Hkv, int D, int Dmax, int cap) {
+  if (B < 1 || N < 1 || Hkv < 1 || Dmax < 1 || cap < 1) return TV_ERR_SHAPE;
   if (D != 64 && D != 128) return TV_ERR_UNSUPPORTED;
   if (N > TV_MAX_NODES) return TV_ERR_UNSUPPORTED;
-  if (!kt || !vt || !path || !accept_len || !kc || !vc || !kv_len) return TV_ERR_NULL;
-  if (misaligned(kt) || misaligned(vt) || misaligned(kc) || misaligned(vc)) return TV_ERR_ALIGN;
+  if (!path || !accept_len || !kc || !vc || !kv_len) return TV_ERR_NULL;
+  const int rc = check_tree(kt, vt, N, cap);
+  if (rc != TV_OK) return rc;
+  if (misaligned(kc) || misaligned(vc)) return TV_ERR_ALIGN;
   return TV_OK;
 }
 
@@ -155,9 +168,8 @@ int tv_commit_path(const void* k_tree, const void* v_tree, const int32_t* path,
                    const int32_t* accept_len, void* k_cache, void* v_cache, int32_t* kv_len,
                    int B, int N, int Hkv, int D, int Lmax, int Dmax, hipStream_t stream) {
   int rc = check_commit(k_tree, v_tree, path, accept_len, k_cache, v_cache, kv_len, B, N, Hkv,
-                        D, Dmax);
+                        D, Dmax, Lmax);
   if (rc != TV_OK) return rc;
-  if (Lmax < 1) return TV_ERR_SHAPE;
   if ((long long)B * Lmax > (1ll << 31)) return TV_ERR_UNSUPPORTED;
   hipError_t e = tv::launch_commit(k_tree, v_tree, path, accept_len, k_cache, v_cache, kv_len,
                                    nullptr, 0, 0, 0, B, N, Hkv, D, Lmax, Dmax, stream);
@@ -169,13 +181,13 @@ int tv_commit_path_paged(const void* k_tree, const void* v_tree, const int32_t* 
                          const int32_t* block_table, int block_size, int max_blocks,
                          int num_blocks, int32_t* kv_len, int B, int N, int Hkv, int D, int Dmax,
                          hipStream_t stream) {
-  int rc = check_commit(k_tree, v_tree, path, accept_len, k_pool, v_pool, kv_len, B, N, Hkv, D,
-                        Dmax);
-  if (rc != TV_OK) return rc;
   const int shift = block_shift(block_size);
   if (shift < 0 || max_blocks < 1 || num_blocks < 1) return TV_ERR_SHAPE;
-  if (!block_table) return TV_ERR_NULL;
   if ((long long)max_blocks * block_size > (1ll << 30)) return TV_ERR_UNSUPPORTED;
+  int rc = check_commit(k_tree, v_tree, path, accept_len, k_pool, v_pool, kv_len, B, N, Hkv, D,
+                        Dmax, max_blocks * block_size);
+  if (rc != TV_OK) return rc;
+  if (!block_table) return TV_ERR_NULL;
   hipError_t e = tv::launch_commit(k_tree, v_tree, path, accept_len, k_pool, v_pool, kv_len,
                                    block_table, shift, max_blocks, num_blocks, B, N, Hkv, D,
                                    max_blocks * block_size, Dmax, stream);

@@ -64,7 +64,32 @@ struct AttnArgs {
   float c;  // scale * log2(e): scores live in base-2 exponent units
   const int32_t* block_table;  // paged cache: [B, max_blocks], else NULL
   int block_shift, max_blocks, num_blocks;
+  int tail;  // tree-tail layout: node i's K/V are cache row kv_len + i
 };
+
+// The keys a sequence's row block attends over.  Separate tree K/V: nct
+// cache tiles (rows < kvl) then the tree tiles of nodes 0..i_hi.  Tree-tail
+// layout: the tree rows follow the context in the cache (kvl is clamped to
+// Lmax - N so they fit) and one run of nct = T tiles covers rows
+// 0 .. kvl + i_hi.  A NULL kv_len means full caches.
+struct Segment {
+  int kvl, nct, T;
+};
+__device__ __forceinline__ Segment segment(const AttnArgs& a, int b, int i_hi) {
+  const int cap = a.tail ? a.Lmax - a.N : a.Lmax;
+  int kvl = a.kv_len ? a.kv_len[b] : cap;
+  kvl = kvl < 0 ? 0 : (kvl > cap ? cap : kvl);
+  Segment sg;
+  sg.kvl = kvl;
+  if (a.tail) {
+    sg.nct = (kvl + i_hi + kKeyTile) / kKeyTile;
+    sg.T = sg.nct;
+  } else {
+    sg.nct = (kvl + kKeyTile - 1) / kKeyTile;
+    sg.T = sg.nct + i_hi / kKeyTile + 1;
+  }
+  return sg;
+}
 
 // Four output values, or four NaN when the sequence's tree is invalid (the
 // NaN is written as a bit pattern: the kernels assume no NaN arithmetic).
@@ -194,7 +219,7 @@ struct TreeSrc {
   const int32_t* btab;  // this sequence's block table row, or NULL
   int shift, nblk;      // log2(block size), blocks in the pool
   int row_bytes;  // bytes between consecutive keys
-  int kvl;        // valid cache rows
+  int rows;       // valid cache rows (the tree's too in the tree-tail layout)
   int nct;        // cache tiles
   int i_hi;       // last tree node the row block can see
 };
@@ -229,7 +254,7 @@ __device__ __forceinline__ void issue_tile(const TreeSrc& src, const uint32_t (&
     kb = (cache ? src.kcache : src.ktree) + (size_t)first * src.row_bytes;
     vb = (cache ? src.vcache : src.vtree) + (size_t)first * src.row_bytes;
   }
-  if (cache && (t + 1) * kKeyTile <= src.kvl) {
+  if (cache && (t + 1) * kKeyTile <= src.rows) {
 #pragma unroll
     for (int k = 0; k < PW; ++k) {
       const int q = wr * PW + k;
@@ -238,7 +263,7 @@ __device__ __forceinline__ void issue_tile(const TreeSrc& src, const uint32_t (&
     }
     return;
   }
-  const int last = cache ? src.kvl - 1 : src.i_hi;  // >= first for every existing tile
+  const int last = cache ? src.rows - 1 : src.i_hi;  // >= first for every existing tile
 #pragma unroll
   for (int k = 0; k < PW; ++k) {
     const int q = wr * PW + k;
@@ -252,7 +277,7 @@ __device__ __forceinline__ void issue_tile(const TreeSrc& src, const uint32_t (&
 
 // Where a tile's scores need masking: the cache tail and the tree tiles.
 struct MaskInfo {
-  int t, nct, kvl, ntt, g4;
+  int t, nct, kvl, ntt, g4, tail;
   const uint32_t* anc;
 };
 
@@ -290,7 +315,26 @@ __device__ __forceinline__ void tile_scores(const unsigned char* kt_lds, const b
 template <int NT>
 __device__ __forceinline__ void tile_mask(f32x4 (&sc)[2][NT], const MaskInfo& mk,
                                           const int (&node_rel)[NT]) {
-  if (mk.t < mk.nct) {
+  if (mk.tail) {
+    // Tree-tail layout: key k of the tile is node s + k (s < 0: a context
+    // row).  Its visibility bits are a 32-bit window of the row's ancestor
+    // bitmask, words w0 and w0 + 1, with all-ones standing in for context
+    // rows (word -1) and zeros past the last word.
+    const int s = mk.t * kKeyTile - mk.kvl;  // > -kKeyTile in the masked tiles
+    const int w0 = s >> 5, sh = s & 31;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const uint32_t* wp = mk.anc + node_rel[nt] * mk.ntt;
+      const uint32_t lo = w0 < 0 ? 0xFFFFFFFFu : wp[w0];
+      const uint32_t hi = w0 + 1 < mk.ntt ? wp[w0 + 1] : 0u;
+      const uint32_t bits = (uint32_t)((((uint64_t)hi << 32) | lo) >> sh);
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (!((bits >> (16 * tt + 4 * mk.g4 + j)) & 1u)) sc[tt][nt][j] = -INFINITY;
+    }
+  } else if (mk.t < mk.nct) {
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
@@ -515,18 +559,16 @@ void attn_main(AttnArgs a) {
   const int wr = wave % WR, wk = wave / WR;
   const int g4 = lane >> 4, l16 = lane & 15;
 
-  int kvl = a.kv_len ? a.kv_len[b] : a.Lmax;
-  kvl = kvl < 0 ? 0 : (kvl > a.Lmax ? a.Lmax : kvl);
   const int r0 = rb * RB;
   const int rows = min(RB, a.M - r0);
   const int i_lo = r0 / a.G, i_hi = (r0 + rows - 1) / a.G;
-  const int nct = (kvl + kKeyTile - 1) / kKeyTile;
-  const int ntt = i_hi / kKeyTile + 1;
-  const int T = nct + ntt;
+  const Segment sg = segment(a, b, i_hi);
+  const int kvl = sg.kvl, nct = sg.nct, T = sg.T;
+  const int ntt = i_hi / kKeyTile + 1;  // words of a node's ancestor bitmask
   const int t0 = s * a.chunk;
   const int t1 = min(T, t0 + a.chunk);
   if (t0 >= t1) return;  // empty chunk: the merge reads only chunks with tiles
-  const bool has_tree = t1 > nct;
+  const bool has_tree = a.tail ? t1 * kKeyTile > kvl : t1 > nct;
 
   constexpr int RING = WK * NS * STAGE;
   const uint32_t ring = (uint32_t)(uintptr_t)smem + wk * NS * STAGE;
@@ -540,8 +582,9 @@ void attn_main(AttnArgs a) {
   const size_t cache0 = kPaged ? 0 : (size_t)b * a.Lmax * krow;  // paged: pool base
   const __bf16* kcache = a.kc + cache0 + (size_t)g * D;
   const __bf16* vcache = a.vc + cache0 + (size_t)g * D;
-  const __bf16* ktree = a.kt + (size_t)b * a.N * krow + (size_t)g * D;
-  const __bf16* vtree = a.vt + (size_t)b * a.N * krow + (size_t)g * D;
+  const size_t tree0 = (size_t)b * a.N * krow + (size_t)g * D;  // unused with a tree tail
+  const __bf16* ktree = a.tail ? kcache : a.kt + tree0;
+  const __bf16* vtree = a.tail ? vcache : a.vt + tree0;
 
   // This lane's share of the DMA instructions of one tile: instruction q
   // (q < kDma: K, else V) covers tile rows j*kRowsPerDma.. (j = q % kDma);
@@ -563,7 +606,7 @@ void attn_main(AttnArgs a) {
                     a.block_shift,
                     a.num_blocks,
                     (int)krow * 2,
-                    kvl,
+                    a.tail ? kvl + i_hi + 1 : kvl,
                     nct,
                     i_hi};
 
@@ -674,7 +717,7 @@ void attn_main(AttnArgs a) {
     ring_step(i);
     const int t = t0 + wk + WK * i;
     if (i >= n_mine || t >= nct || (t + 1) * kKeyTile > kvl) break;
-    const MaskInfo mk{t, nct, kvl, ntt, g4, anc};
+    const MaskInfo mk{t, nct, kvl, ntt, g4, a.tail, anc};
     attend_tile<D, NT, false>(ring_ptr + (i % NS) * STAGE, qf, o, lacc, m, thr, ones_v, a.c, inv_c,
                               mk, node_rel, g4, l16);
   }
@@ -682,7 +725,7 @@ void attn_main(AttnArgs a) {
     if (!stepped) ring_step(i);
     if (i >= n_mine) continue;
     const int t = t0 + wk + WK * i;
-    const MaskInfo mk{t, nct, kvl, ntt, g4, anc};
+    const MaskInfo mk{t, nct, kvl, ntt, g4, a.tail, anc};
     attend_tile<D, NT, true>(ring_ptr + (i % NS) * STAGE, qf, o, lacc, m, thr, ones_v, a.c, inv_c,
                              mk, node_rel, g4, l16);
   }
@@ -810,10 +853,8 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
   if (r >= a.M) return;
   // chunks of this row block that hold tiles (the same count the main
   // kernel derives from kv_len and the block's last node)
-  int kvl = a.kv_len ? a.kv_len[b] : a.Lmax;
-  kvl = kvl < 0 ? 0 : (kvl > a.Lmax ? a.Lmax : kvl);
   const int i_hi = (min(rb * RB + RB, a.M) - 1) / a.G;
-  const int T = (kvl + kKeyTile - 1) / kKeyTile + i_hi / kKeyTile + 1;
+  const int T = segment(a, b, i_hi).T;
   const int nval = min(a.S, (T + a.chunk - 1) / a.chunk);
   const size_t base = (size_t)(bg * a.nRB + rb) * a.S;  // first chunk partial
   float mstar = -INFINITY;
@@ -891,6 +932,7 @@ hipError_t launch_attention(const void* q, const void* kc, const void* vc, const
                             const int32_t* block_table, int block_shift, int max_blocks,
                             int num_blocks) {
   AttnArgs a;
+  a.tail = kt == nullptr;
   a.block_table = block_table;
   a.block_shift = block_shift;
   a.max_blocks = max_blocks;

@@ -10,6 +10,13 @@
 // sequence whose acceptance failed (accept_len < 1 or > Dmax), whose path
 // names a node outside [0, N) or whose commit would pass the capacity is
 // left unchanged.
+//
+// Tree-tail layout (no separate tree K/V: node i sits at cache row
+// kv_len + i): the commit moves rows within the cache, row kv_len + j taking
+// row kv_len + path[j].  A root-to-node path has path[j] >= j, so taking the
+// rows in increasing j never reads a row after it was overwritten; the copy
+// runs in rounds in that order, each round reading all its rows before the
+// workgroup barrier and writing them after it.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -28,33 +35,71 @@ struct CommitArgs {
   int N, cpr, cap, Dmax;  // cpr: 16-byte chunks per row (Hkv * D * 2 / 16)
 };
 
+// Row of cache position pos of sequence b (paged: through the block table,
+// block numbers clamped into the pool).
+__device__ __forceinline__ size_t cache_row(const CommitArgs& a, int b, int pos) {
+  if (a.block_table) {
+    int blk = a.block_table[(size_t)b * a.max_blocks + (pos >> a.shift)];
+    blk = blk < 0 ? 0 : (blk >= a.num_blocks ? a.num_blocks - 1 : blk);
+    return ((size_t)blk << a.shift) + (pos & ((1 << a.shift) - 1));
+  }
+  return (size_t)b * a.cap + pos;
+}
+
+constexpr int kTailBatch = 4;  // 16-byte pieces per thread per round of a tree-tail commit
+
 __global__ __launch_bounds__(256) void commit_path(CommitArgs a) {
   const int b = blockIdx.x, tid = threadIdx.x;
+  const bool tail = a.kt == nullptr;
   const int kl = a.kv_len[b];
   const int n = a.accept_len[b];
   const int32_t* path = a.path + (size_t)b * a.Dmax;
-  int bad = n < 1 || n > a.Dmax || kl < 0 || kl > a.cap - n;
+  // a tree tail needs its N rows inside the capacity
+  int bad = n < 1 || n > a.Dmax || kl < 0 || kl > a.cap - (tail ? a.N : n);
   if (!bad)
     for (int j = tid; j < n; j += 256) bad |= path[j] < 0 || path[j] >= a.N;
   if (__syncthreads_or(bad)) return;
   const int per = n * a.cpr;  // chunks of K (or of V)
-  for (int c = tid; c < 2 * per; c += 256) {
-    const bool isv = c >= per;
-    const int r = isv ? c - per : c;
-    const int j = r / a.cpr, q = r % a.cpr;
-    const size_t src = ((size_t)b * a.N + path[j]) * a.cpr + q;
-    const int pos = kl + j;
-    size_t row;
-    if (a.block_table) {
-      int blk = a.block_table[(size_t)b * a.max_blocks + (pos >> a.shift)];
-      blk = blk < 0 ? 0 : (blk >= a.num_blocks ? a.num_blocks - 1 : blk);
-      row = ((size_t)blk << a.shift) + (pos & ((1 << a.shift) - 1));
-    } else {
-      row = (size_t)b * a.cap + pos;
+  if (!tail) {
+    for (int c = tid; c < 2 * per; c += 256) {
+      const bool isv = c >= per;
+      const int r = isv ? c - per : c;
+      const int j = r / a.cpr, q = r % a.cpr;
+      const size_t src = ((size_t)b * a.N + path[j]) * a.cpr + q;
+      const size_t dst = cache_row(a, b, kl + j) * a.cpr + q;
+      if (isv) a.vc[dst] = a.vt[src];
+      else a.kc[dst] = a.kt[src];
     }
-    const size_t dst = row * a.cpr + q;
-    if (isv) a.vc[dst] = a.vt[src];
-    else a.kc[dst] = a.kt[src];
+  } else {
+    // piece c: row j = c / (2 cpr), then K or V, then the 16-byte piece
+    const int rowp = 2 * a.cpr;
+    for (int c0 = 0; c0 < 2 * per; c0 += kTailBatch * 256) {
+      uint4 v[kTailBatch];
+      size_t dst[kTailBatch];
+      bool isv[kTailBatch];
+#pragma unroll
+      for (int u = 0; u < kTailBatch; ++u) {
+        const int c = c0 + u * 256 + tid;
+        if (c < 2 * per) {
+          const int j = c / rowp, r = c % rowp;
+          isv[u] = r >= a.cpr;
+          const int q = isv[u] ? r - a.cpr : r;
+          const size_t src = cache_row(a, b, kl + path[j]) * a.cpr + q;
+          dst[u] = cache_row(a, b, kl + j) * a.cpr + q;
+          v[u] = isv[u] ? a.vc[src] : a.kc[src];
+        }
+      }
+      __syncthreads();  // the round's reads are done before any of its writes
+#pragma unroll
+      for (int u = 0; u < kTailBatch; ++u) {
+        const int c = c0 + u * 256 + tid;
+        if (c < 2 * per) {
+          if (isv[u]) a.vc[dst[u]] = v[u];
+          else a.kc[dst[u]] = v[u];
+        }
+      }
+      __syncthreads();
+    }
   }
   __syncthreads();  // every thread has read kv_len
   if (tid == 0) a.kv_len[b] = kl + n;

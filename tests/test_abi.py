@@ -227,3 +227,16 @@ def test_commit_host_errors():
     assert _commit_paged(lib, nb=0) == -2
     assert _commit_paged(lib, vp=FAKE + 2) == -7
     assert _commit_paged(lib, D=80) == -4
+
+
+def test_tree_tail_host_errors():
+    lib = _lib()
+    assert _attn(lib, kt=None) == -1                         # only one of the two NULL
+    assert _attn(lib, vt=None) == -1
+    assert _attn(lib, kt=None, vt=None, N=64, Lmax=63) == -2  # no room for the tree
+    assert _attn(lib, kt=None, vt=None, N=64, Lmax=0) == -2
+    assert _attn_paged(lib, kt=None) == -1
+    assert _attn_paged(lib, kt=None, vt=None, N=64, mb=1, bs=32) == -2
+    assert _commit(lib, vt=None) == -1
+    assert _commit(lib, kt=None, vt=None, N=64, Lmax=63) == -2
+    assert _commit_paged(lib, kt=None, vt=None, N=64, mb=1, bs=32) == -2

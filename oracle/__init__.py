@@ -15,6 +15,9 @@ Contents
                      log-probability (Sec. 2.4 parallel tree drafting; Alg. 1).
   kv_commit       -- the cache side: committing the accepted path, paged
                      caches, the tree-tail layout (App. E).
+  block_causal    -- attention under the draft head's training mask: anchor
+                     blocks that see the prefix before their anchor and
+                     their own earlier positions (App. Training Details).
   brute           -- pure-Python loop versions for tiny inputs, used only to
                      pin the functions above.
 
@@ -25,9 +28,10 @@ from .tree_attention import (decode_bf16, tree_structure, full_mask,
                              tree_attention)
 from .tree_accept import target_argmax, tree_accept
 from .tree_build import draft_topw, build_tree
+from .block_causal import training_mask, block_causal_attention
 from .kv_commit import commit_path, gather_paged, commit_path_paged, tree_tail, commit_path_tail
 
 __all__ = ["decode_bf16", "tree_structure", "full_mask", "tree_attention",
            "target_argmax", "tree_accept", "draft_topw", "build_tree",
            "commit_path", "gather_paged", "commit_path_paged", "tree_tail",
-           "commit_path_tail"]
+           "commit_path_tail", "training_mask", "block_causal_attention"]

@@ -11,7 +11,9 @@ Independent constructions used to pin the oracle:
   * tree building: the full W-ary tree is enumerated and its nodes visited in
     descending score order, with no priority queue;
   * tree-tail commit: rows moved in place one at a time, with no snapshot of
-    the tree rows.
+    the tree rows;
+  * training-mask attention: the visible key list of each query is built
+    from the block rule directly, in Python floats.
 """
 from __future__ import annotations
 
@@ -176,3 +178,31 @@ def commit_tail_in_place(cache, path, accept_len, kv_len):
         for j in range(n):
             c[b][kl + j] = c[b][kl + int(path[b][j])].copy()
     return np.array(c)
+
+
+def block_causal(q, k_ctx, v_ctx, k_blk, v_blk, anchors, scale=None):
+    """Training-mask attention with Python loops: query (b, k, j, h) sees
+    context rows t < anchor and block k's positions 0..j."""
+    B, A, S, Hq, D = np.asarray(q).shape
+    L, Hkv = np.asarray(k_ctx).shape[1:3]
+    G = Hq // Hkv
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    out = np.zeros((B, A, S, Hq, D))
+    for b in range(B):
+        for k in range(A):
+            a = min(max(int(anchors[b][k]), 0), L)
+            for j in range(S):
+                for h in range(Hq):
+                    g = h // G
+                    keys = [(k_ctx[b][t][g], v_ctx[b][t][g]) for t in range(a)]
+                    keys += [(k_blk[b][k][i][g], v_blk[b][k][i][g]) for i in range(j + 1)]
+                    sc = [scale * sum(float(x) * float(y) for x, y in zip(q[b][k][j][h], kk))
+                          for kk, _ in keys]
+                    mx = max(sc)
+                    w = [math.exp(x - mx) for x in sc]
+                    tot = sum(w)
+                    for d in range(D):
+                        out[b, k, j, h, d] = sum(wi * float(vv[d]) for wi, (_, vv) in
+                                                 zip(w, keys)) / tot
+    return out

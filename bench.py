@@ -31,6 +31,7 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 MALL_BYTES = 256 << 20
 PAGE_BLOCK = 64                # rows per paged-cache block in the paged timing
+TRAIN_ANCHORS, TRAIN_BLOCK, TRAIN_CONTEXT = 512, 16, 4096   # training-mask attention timing
 
 
 def parse():
@@ -181,7 +182,10 @@ def summarize_trace(trace_dir, bench_log, workload):
             f"{d['build_tree_us']:.2f} us",
             f"    paged attention ({d['page_block']}-row blocks) {d['paged_attention_us']:.2f} us, "
             f"tree-tail attention {d['tree_tail_attention_us']:.2f} us, "
-            f"path commit {d['commit_us']:.2f} us", ""]
+            f"path commit {d['commit_us']:.2f} us",
+            f"    training-mask attention ({d['training_mask_attention']['anchors']} blocks of "
+            f"{d['training_mask_attention']['block']} over {d['training_mask_attention']['context']}"
+            f" context rows) {d['training_mask_attention']['us']:.1f} us", ""]
     path = os.path.join(ROOT, "profiles", f"kernel_trace_{workload}.md")
     with open(path, "w") as fh:
         fh.write("\n".join(out))
@@ -294,8 +298,9 @@ def main():
         sys.exit(2)
 
     import torch
-    from paper_2606_18394_amd import (build_tree, commit_path, draft_topw, synth, tree_accept,
-                                      tree_verify_attention, tree_verify_attention_paged)
+    from paper_2606_18394_amd import (block_causal_attention, build_tree, commit_path,
+                                      draft_topw, synth, tree_accept, tree_verify_attention,
+                                      tree_verify_attention_paged)
     from paper_2606_18394_amd.binding import load_library
 
     load_library()
@@ -401,6 +406,28 @@ def main():
         max(256, load_library().tv_tree_verify_attention_workspace(
             w.B, w.N, w.Hq, w.Hkv, w.D, w.L + w.N)), dtype=torch.uint8, device=dev)
 
+    # The draft head's training-mask attention at the workload's head
+    # geometry: TRAIN_ANCHORS blocks of TRAIN_BLOCK positions over a
+    # TRAIN_CONTEXT-row context, anchors uniform over the context.
+    trng = np.random.default_rng(w.seed + 99)
+    TA, TS, TL = TRAIN_ANCHORS, TRAIN_BLOCK, TRAIN_CONTEXT
+    anchors_np = trng.integers(0, TL + 1, size=(1, TA)).astype(np.int32)
+    tq = bf(synth._normal_bf16(trng, (1, TA, TS, w.Hq, w.D)))
+    tkc = bf(synth._normal_bf16(trng, (1, TL, w.Hkv, w.D)))
+    tvc = bf(synth._normal_bf16(trng, (1, TL, w.Hkv, w.D)))
+    tkb = bf(synth._normal_bf16(trng, (1, TA, TS, w.Hkv, w.D)))
+    tvb = bf(synth._normal_bf16(trng, (1, TA, TS, w.Hkv, w.D)))
+    tanc = i32(anchors_np)
+    tout = torch.empty(1, TA, TS, w.Hq, w.D, dtype=torch.bfloat16, device=dev)
+    ws_train = torch.zeros(
+        max(256, load_library().tv_block_causal_attention_workspace(
+            1, TA, TS, w.Hq, w.Hkv, w.D, TL)), dtype=torch.uint8, device=dev)
+    train_flops = 4 * w.D * w.Hq * int(sum(int(a) * TS + TS * (TS + 1) // 2
+                                           for a in anchors_np[0]))
+
+    def train_attn(r):
+        block_causal_attention(tq, tkc, tvc, tkb, tvb, tanc, tout, workspace_tensor=ws_train)
+
     ccap = w.L + w.Dmax
     ckc = torch.zeros(w.B, ccap, w.Hkv, w.D, dtype=torch.bfloat16, device=dev)
     cvc = torch.zeros_like(ckc)
@@ -441,6 +468,7 @@ def main():
         build(s % R)
     for name, fn in [("step", step), ("attn", attn), ("accept", accept), ("topw", topw),
                      ("build", build), ("attn_paged", attn_paged), ("attn_tail", attn_tail),
+                     ("train_attn", train_attn),
                      ("reset", reset),
                      ("commit", commit)]:
         graphs[name] = (capture(fn, range(R)), [capture(fn, [r]) for r in range(R)])
@@ -470,6 +498,7 @@ def main():
     ms_build = timed("build", args.steps)
     ms_paged = timed("attn_paged", args.steps)
     ms_tail = timed("attn_tail", args.steps)
+    ms_train = timed("train_attn", max(10, args.steps // 10))
     ms_commit = max(0.0, timed("commit", args.steps) - timed("reset", args.steps))
     attn(0)
     ref0 = outs[0].clone()
@@ -537,6 +566,11 @@ def main():
                    "paged_bit_identical": paged_same,
                    "paged_attention_GBps": attn_bytes / (ms_paged * 1e-3) / 1e9,
                    "tree_tail_attention_us": ms_tail * 1e3,
+                   "training_mask_attention": {
+                       "anchors": TA, "block": TS, "context": TL, "us": ms_train * 1e3,
+                       "flops": train_flops,
+                       "TFLOPs": train_flops / (ms_train * 1e-3) / 1e12,
+                       "mfma_frac": train_flops / (ms_train * 1e-3) / 1e12 / BF16_PEAK_TFLOPS},
                    "commit_us": ms_commit * 1e3, "commit_rows": int(acc_len.sum().item())},
     }
     print(json.dumps(line), flush=True)

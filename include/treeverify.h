@@ -141,6 +141,35 @@ int tv_tree_verify_attention_paged(const void* q, const void* k_pool, const void
                                    hipStream_t stream);
 
 /*
+ * Attention under the draft head's training mask (App. "Training Details"):
+ * each of the A sampled anchors of a training example starts a block of S
+ * positions (the anchor, then mask tokens).  Position j of block k attends to
+ * the context rows t < anchors[b, k] (the verified prefix) and to positions
+ * 0 .. j of its own block; never to later positions or to other blocks.
+ *
+ *   q            [B, A, S, Hq, D]  bf16  block queries (post-RoPE)
+ *   k_ctx, v_ctx [B, L, Hkv, D]    bf16  context K/V of the example
+ *   k_blk, v_blk [B, A, S, Hkv, D] bf16  K/V of the block positions
+ *   anchors      [B, A]            int32 anchor positions, clamped to [0, L]
+ *   out          [B, A, S, Hq, D]  bf16
+ *
+ * Scale, precision, GQA mapping and requirements as in
+ * tv_tree_verify_attention with B*A sequences of S nodes (S <= TV_MAX_NODES,
+ * B*A <= 2^24); it runs on the same kernels, each block as a chain tree whose
+ * cache is its example's context cut at its anchor.  The workspace is
+ * tv_block_causal_attention_workspace(B, A, S, Hq, Hkv, D, L) bytes,
+ * zero-filled before first use like the verification workspace.  Forward
+ * only.
+ */
+size_t tv_block_causal_attention_workspace(int B, int A, int S, int Hq, int Hkv, int D,
+                                          int L);
+int tv_block_causal_attention(const void* q, const void* k_ctx, const void* v_ctx,
+                              const void* k_blk, const void* v_blk, const int32_t* anchors,
+                              void* out, int B, int A, int S, int Hq, int Hkv, int D, int L,
+                              float scale, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream);
+
+/*
  * Commit the accepted path (App. E): the keys and values of nodes
  * path[b, 0 .. accept_len[b]-1] (root first) of k_tree/v_tree are copied to
  * cache positions kv_len[b] .. kv_len[b] + accept_len[b] - 1 and kv_len[b]

@@ -7,7 +7,8 @@ and raises if it is missing.
 """
 
 __all__ = ["tree_verify_attention", "tree_verify_attention_paged", "tree_accept",
-           "commit_path", "commit_path_paged", "draft_topw", "build_tree", "load_library"]
+           "commit_path", "commit_path_paged", "draft_topw", "build_tree",
+           "block_causal_attention", "load_library"]
 
 
 def tree_verify_attention(*args, **kwargs):
@@ -42,6 +43,11 @@ def draft_topw(*args, **kwargs):
 
 def build_tree(*args, **kwargs):
     from .binding import build_tree as f
+    return f(*args, **kwargs)
+
+
+def block_causal_attention(*args, **kwargs):
+    from .binding import block_causal_attention as f
     return f(*args, **kwargs)
 
 

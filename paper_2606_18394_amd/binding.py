@@ -62,6 +62,11 @@ def load_library() -> ctypes.CDLL:
         lib.tv_tree_verify_attention_paged.argtypes = (
             [vp, vp, vp, i32p] + [ci] * 3 + [vp, vp, i32p, i32p, vp] + [ci] * 5
             + [ctypes.c_float, vp, sz, vp])
+        lib.tv_block_causal_attention_workspace.restype = sz
+        lib.tv_block_causal_attention_workspace.argtypes = [ci] * 7
+        lib.tv_block_causal_attention.restype = ci
+        lib.tv_block_causal_attention.argtypes = (
+            [vp] * 5 + [i32p, vp] + [ci] * 7 + [ctypes.c_float, vp, sz, vp])
         lib.tv_commit_path.restype = ci
         lib.tv_commit_path.argtypes = [vp, vp, i32p, i32p, vp, vp, i32p] + [ci] * 6 + [vp]
         lib.tv_commit_path_paged.restype = ci
@@ -182,6 +187,36 @@ def tree_verify_attention_paged(q, k_pool, v_pool, block_table, k_tree, v_tree, 
         _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(block_table), bs, max_blocks, num_blocks,
         _ptr(k_tree), _ptr(v_tree), _ptr(parent), _ptr(kv_len), _ptr(out), B, N, Hq, Hkv, D,
         0.0 if scale is None else float(scale), _ptr(ws), ws.numel(), ctypes.c_void_p(stream)))
+    return out
+
+
+def block_causal_attention(q, k_ctx, v_ctx, k_blk, v_blk, anchors, out, scale=None,
+                           workspace_tensor=None):
+    """Attention under the draft head's training mask: position j of block k
+    sees context rows < anchors[b, k] and positions 0..j of block k.
+
+    q [B,A,S,Hq,D], k_ctx/v_ctx [B,L,Hkv,D], k_blk/v_blk [B,A,S,Hkv,D]
+    (bf16); anchors [B,A] int32; out [B,A,S,Hq,D] bf16."""
+    lib = load_library()
+    B, A, S, Hq, D = q.shape
+    L, Hkv = k_ctx.shape[1], k_ctx.shape[2]
+    dev = q.device
+    _need(q, "q", torch.bfloat16, device=dev)
+    _need(k_ctx, "k_ctx", torch.bfloat16, (B, L, Hkv, D), dev)
+    _need(v_ctx, "v_ctx", torch.bfloat16, (B, L, Hkv, D), dev)
+    _need(k_blk, "k_blk", torch.bfloat16, (B, A, S, Hkv, D), dev)
+    _need(v_blk, "v_blk", torch.bfloat16, (B, A, S, Hkv, D), dev)
+    _need(anchors, "anchors", torch.int32, (B, A), dev)
+    _need(out, "out", torch.bfloat16, (B, A, S, Hq, D), dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    need = lib.tv_block_causal_attention_workspace(B, A, S, Hq, Hkv, D, L)
+    if need == 0:
+        _check(-2)
+    ws = workspace_tensor if workspace_tensor is not None else workspace("attn", need, dev, stream)
+    _check(lib.tv_block_causal_attention(
+        _ptr(q), _ptr(k_ctx), _ptr(v_ctx), _ptr(k_blk), _ptr(v_blk), _ptr(anchors), _ptr(out),
+        B, A, S, Hq, Hkv, D, L, 0.0 if scale is None else float(scale), _ptr(ws), ws.numel(),
+        ctypes.c_void_p(stream)))
     return out
 
 

@@ -14,7 +14,7 @@ hipError_t launch_attention(const void* q, const void* kc, const void* vc, const
                             void* out, int B, int N, int Hq, int Hkv, int D, int Lmax,
                             float scale, void* ws, const AttnPlan& p, hipStream_t st,
                             const int32_t* block_table, int block_shift, int max_blocks,
-                            int num_blocks);
+                            int num_blocks, int cgroup);
 hipError_t launch_commit(const void* kt, const void* vt, const int32_t* path,
                          const int32_t* accept_len, void* kc, void* vc, int32_t* kv_len,
                          const int32_t* block_table, int shift, int max_blocks, int num_blocks,
@@ -58,6 +58,14 @@ static int check_tree(const void* kt, const void* vt, int N, int Lmax) {
   if (!kt && Lmax < N) return TV_ERR_SHAPE;
   if (misaligned(kt) || misaligned(vt)) return TV_ERR_ALIGN;
   return TV_OK;
+}
+
+// The training-mask attention runs as B*A chain trees of S nodes, block k of
+// example b reading example b's context with kv_len = anchors[b, k].
+static int check_block_causal(int B, int A, int S, int Hq, int Hkv, int D, int L) {
+  if (A < 1 || S < 1 || B < 1) return TV_ERR_SHAPE;
+  if ((long long)B * A > (1ll << 24)) return TV_ERR_UNSUPPORTED;
+  return check_attention_sizes(B * A, S, Hq, Hkv, D, L);
 }
 
 static int check_accept_sizes(int B, int N, int V, int Dmax) {
@@ -117,7 +125,36 @@ int tv_tree_verify_attention(const void* q, const void* k_cache, const void* v_c
   if (!(scale > 0.f)) scale = 1.0f / sqrtf((float)D);
   hipError_t e = tv::launch_attention(q, k_cache, v_cache, k_tree, v_tree, parent, kv_len, out,
                                       B, N, Hq, Hkv, D, Lmax, scale, workspace, p, stream,
-                                      nullptr, 0, 0, 0);
+                                      nullptr, 0, 0, 0, 1);
+  return e == hipSuccess ? TV_OK : TV_ERR_LAUNCH;
+}
+
+size_t tv_block_causal_attention_workspace(int B, int A, int S, int Hq, int Hkv, int D,
+                                          int L) {
+  if (check_block_causal(B, A, S, Hq, Hkv, D, L) != TV_OK) return 0;
+  const tv::AttnPlan p = tv::attn_plan(B * A, S, Hq, Hkv, D, L);
+  return p.ws_bytes > 0 ? p.ws_bytes : 256;
+}
+
+int tv_block_causal_attention(const void* q, const void* k_ctx, const void* v_ctx,
+                              const void* k_blk, const void* v_blk, const int32_t* anchors,
+                              void* out, int B, int A, int S, int Hq, int Hkv, int D, int L,
+                              float scale, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream) {
+  int rc = check_block_causal(B, A, S, Hq, Hkv, D, L);
+  if (rc != TV_OK) return rc;
+  if (!q || !k_blk || !v_blk || !anchors || !out) return TV_ERR_NULL;
+  if (L > 0 && (!k_ctx || !v_ctx)) return TV_ERR_NULL;
+  if (misaligned(q) || misaligned(k_blk) || misaligned(v_blk) || misaligned(out) ||
+      (L > 0 && (misaligned(k_ctx) || misaligned(v_ctx))))
+    return TV_ERR_ALIGN;
+  const tv::AttnPlan p = tv::attn_plan(B * A, S, Hq, Hkv, D, L);
+  if (p.ws_bytes > 0 && (!workspace || workspace_bytes < p.ws_bytes)) return TV_ERR_WORKSPACE;
+  if (misaligned(workspace)) return TV_ERR_ALIGN;
+  if (!(scale > 0.f)) scale = 1.0f / sqrtf((float)D);
+  hipError_t e = tv::launch_attention(q, k_ctx, v_ctx, k_blk, v_blk, nullptr, anchors, out,
+                                      B * A, S, Hq, Hkv, D, L, scale, workspace, p, stream,
+                                      nullptr, 0, 0, 0, A);
   return e == hipSuccess ? TV_OK : TV_ERR_LAUNCH;
 }
 
@@ -147,7 +184,7 @@ int tv_tree_verify_attention_paged(const void* q, const void* k_pool, const void
   hipError_t e = tv::launch_attention(q, k_pool, v_pool, k_tree, v_tree, parent, kv_len, out, B,
                                       N, Hq, Hkv, D, Lmax, scale, workspace, p, stream,
                                       Lmax > 0 ? block_table : nullptr, shift, max_blocks,
-                                      num_blocks);
+                                      num_blocks, 1);
   return e == hipSuccess ? TV_OK : TV_ERR_LAUNCH;
 }
 

@@ -64,7 +64,8 @@ struct AttnArgs {
   float c;  // scale * log2(e): scores live in base-2 exponent units
   const int32_t* block_table;  // paged cache: [B, max_blocks], else NULL
   int block_shift, max_blocks, num_blocks;
-  int tail;  // tree-tail layout: node i's K/V are cache row kv_len + i
+  int tail;    // tree-tail layout: node i's K/V are cache row kv_len + i
+  int cgroup;  // sequences sharing one cache (sequence b reads cache b / cgroup)
 };
 
 // The keys a sequence's row block attends over.  Separate tree K/V: nct
@@ -579,7 +580,7 @@ void attn_main(AttnArgs a) {
   int* flag = par + a.N;
 
   const size_t krow = (size_t)a.Hkv * D;  // elements between consecutive keys
-  const size_t cache0 = kPaged ? 0 : (size_t)b * a.Lmax * krow;  // paged: pool base
+  const size_t cache0 = kPaged ? 0 : (size_t)(b / a.cgroup) * a.Lmax * krow;  // paged: pool
   const __bf16* kcache = a.kc + cache0 + (size_t)g * D;
   const __bf16* vcache = a.vc + cache0 + (size_t)g * D;
   const size_t tree0 = (size_t)b * a.N * krow + (size_t)g * D;  // unused with a tree tail
@@ -640,7 +641,7 @@ void attn_main(AttnArgs a) {
   if (has_tree) {
     int bad = 0;
     for (int i = tid; i < a.N; i += kThreads) {
-      const int p = a.parent[(size_t)b * a.N + i];
+      const int p = a.parent ? a.parent[(size_t)b * a.N + i] : i - 1;  // NULL: a chain
       par[i] = p;
       bad |= (i == 0) ? (p != -1) : (p < 0 || p >= i);
     }
@@ -844,7 +845,7 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
   const int b = bg / a.Hkv, g = bg % a.Hkv;
   int bad = 0;
   for (int i = threadIdx.x; i < a.N; i += 256) {
-    const int p = a.parent[(size_t)b * a.N + i];
+    const int p = a.parent ? a.parent[(size_t)b * a.N + i] : i - 1;
     bad |= (i == 0) ? (p != -1) : (p < 0 || p >= i);
   }
   bad = __syncthreads_or(bad);
@@ -930,9 +931,10 @@ hipError_t launch_attention(const void* q, const void* kc, const void* vc, const
                             void* out, int B, int N, int Hq, int Hkv, int D, int Lmax,
                             float scale, void* ws, const AttnPlan& p, hipStream_t st,
                             const int32_t* block_table, int block_shift, int max_blocks,
-                            int num_blocks) {
+                            int num_blocks, int cgroup) {
   AttnArgs a;
   a.tail = kt == nullptr;
+  a.cgroup = cgroup;
   a.block_table = block_table;
   a.block_shift = block_shift;
   a.max_blocks = max_blocks;

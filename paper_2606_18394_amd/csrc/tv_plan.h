@@ -89,7 +89,9 @@ inline AttnPlan attn_plan_arr(int B, int N, int Hq, int Hkv, int D, int Lmax, in
   long long S = (target + base - 1) / base;
   const long long max_s = tiles / min_chunk > 1 ? tiles / min_chunk : 1;
   if (S > max_s) S = max_s;
-  if (B > 1 && S < 4 && max_s >= 4) S = 4;        // ragged batches: balance long sequences
+  // ragged batches with too few row blocks to fill the GPU: split further so
+  // that long sequences spread over several CUs
+  if (B > 1 && base < target && S < 4 && max_s >= 4) S = 4;
   if (S < 1 || base > kSyncGroups) S = 1;
   p.chunk = cdiv(tiles, S);
   p.S = cdiv(tiles, p.chunk);
@@ -118,9 +120,10 @@ inline bool attn_plan_fits(const AttnPlan& p) {
 
 // Rough time of an arrangement: matrix work on padded rows, K/V traffic
 // from L2 (each row block re-reads the keys), HBM, the split partials
-// written and read back, and a penalty when the two waves of a SIMD belong
+// written and read back, a penalty when the two waves of a SIMD belong
 // to one workgroup (its per-tile barriers keep them in phase, so their
-// matrix and vector work overlap poorly).
+// matrix and vector work overlap poorly), and a fixed cost per round of
+// workgroups (prologue, first tile's latency, epilogue: a few us each).
 inline double attn_plan_cost(const AttnPlan& p, int B, int Hkv, int D, int Lmax, int N) {
   const double keys = (double)Lmax + N;
   double mfma = (double)B * Hkv * p.nRB * p.RB * keys * 4.0 * D / 2.0e15;
@@ -129,9 +132,10 @@ inline double attn_plan_cost(const AttnPlan& p, int B, int Hkv, int D, int Lmax,
   const double l2 = kv * p.nRB / 20.0e12;
   const double hbm = kv / 6.0e12;
   const double partial = (double)p.ws_bytes * 2.0 / 5.0e12;
+  const double rounds = (double)cdiv(p.nwork, 256LL * p.wg_per_cu);
   double t = mfma > l2 ? mfma : l2;
   t = t > hbm ? t : hbm;
-  return t + partial;
+  return t + partial + rounds * 4.0e-6;
 }
 
 inline AttnPlan attn_plan(int B, int N, int Hq, int Hkv, int D, int Lmax) {

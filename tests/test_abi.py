@@ -240,3 +240,31 @@ def test_tree_tail_host_errors():
     assert _commit(lib, vt=None) == -1
     assert _commit(lib, kt=None, vt=None, N=64, Lmax=63) == -2
     assert _commit_paged(lib, kt=None, vt=None, N=64, mb=1, bs=32) == -2
+
+
+def _bc(lib, **kw):
+    a = dict(q=FAKE, kc=FAKE, vc=FAKE, kb=FAKE, vb=FAKE, anc=FAKE, out=FAKE, B=1, A=512, S=16,
+             Hq=32, Hkv=8, D=128, L=4096, scale=0.0, ws=FAKE, wsb=1 << 40)
+    a.update(kw)
+    return lib.tv_block_causal_attention(
+        a["q"], a["kc"], a["vc"], a["kb"], a["vb"], a["anc"], a["out"], a["B"], a["A"], a["S"],
+        a["Hq"], a["Hkv"], a["D"], a["L"], ctypes.c_float(a["scale"]), a["ws"], a["wsb"], None)
+
+
+def test_block_causal_host_errors():
+    lib = _lib()
+    assert lib.tv_block_causal_attention_workspace(1, 512, 16, 32, 8, 128, 4096) > 0
+    assert lib.tv_block_causal_attention_workspace(1, 0, 16, 32, 8, 128, 4096) == 0
+    assert lib.tv_block_causal_attention_workspace(1, 4, 2049, 32, 8, 128, 64) == 0
+    assert _bc(lib, anc=None) == -1
+    assert _bc(lib, kb=None) == -1
+    assert _bc(lib, kc=None) == -1
+    assert _bc(lib, A=0) == -2
+    assert _bc(lib, S=0) == -2
+    assert _bc(lib, Hq=30) == -2
+    assert _bc(lib, D=80) == -4
+    assert _bc(lib, S=2049) == -4
+    assert _bc(lib, B=1 << 13, A=1 << 12) == -4
+    assert _bc(lib, out=FAKE + 4) == -7
+    assert lib.tv_block_causal_attention_workspace(1, 4, 16, 32, 8, 128, 4096) > 256  # splits
+    assert _bc(lib, A=4, ws=None) == -5

@@ -15,6 +15,11 @@ Contents
                      log-probability (Sec. 2.4 parallel tree drafting; Alg. 1).
   kv_commit       -- the cache side: committing the accepted path, paged
                      caches, the tree-tail layout (App. E).
+  tree_accept_sampled -- non-greedy (temperature) tree acceptance: the
+                     speculative sampling test min(1, p/q) per draft node,
+                     deepest accepted path, correction token drawn from the
+                     residual (Sec. 2.4); philox -- its counter-based
+                     random numbers (Salmon et al. 2011).
   block_causal    -- attention under the draft head's training mask: anchor
                      blocks that see the prefix before their anchor and
                      their own earlier positions (App. Training Details).
@@ -28,10 +33,12 @@ from .tree_attention import (decode_bf16, tree_structure, full_mask,
                              tree_attention)
 from .tree_accept import target_argmax, tree_accept
 from .tree_build import draft_topw, build_tree
+from .tree_accept_sampled import tree_accept_sampled
 from .block_causal import training_mask, block_causal_attention
 from .kv_commit import commit_path, gather_paged, commit_path_paged, tree_tail, commit_path_tail
 
 __all__ = ["decode_bf16", "tree_structure", "full_mask", "tree_attention",
            "target_argmax", "tree_accept", "draft_topw", "build_tree",
            "commit_path", "gather_paged", "commit_path_paged", "tree_tail",
-           "commit_path_tail", "training_mask", "block_causal_attention"]
+           "commit_path_tail", "training_mask", "block_causal_attention",
+           "tree_accept_sampled"]

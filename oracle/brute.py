@@ -13,7 +13,10 @@ Independent constructions used to pin the oracle:
   * tree-tail commit: rows moved in place one at a time, with no snapshot of
     the tree rows;
   * training-mask attention: the visible key list of each query is built
-    from the block rule directly, in Python floats.
+    from the block rule directly, in Python floats;
+  * sampled acceptance: every root-to-node path tested node by node with
+    Python-float softmaxes, the correction by a Python-loop race over scalar
+    Philox words.
 """
 from __future__ import annotations
 
@@ -206,3 +209,62 @@ def block_causal(q, k_ctx, v_ctx, k_blk, v_blk, anchors, scale=None):
                         out[b, k, j, h, d] = sum(wi * float(vv[d]) for wi, (_, vv) in
                                                  zip(w, keys)) / tot
     return out
+
+
+def _softmax_list(row, T):
+    m = max(float(x) / T for x in row)
+    e = [math.exp(float(x) / T - m) for x in row]
+    s = sum(e)
+    return [x / s for x in e]
+
+
+def accept_sampled(logits, draft_logits, draft_tok, parent, u_accept, seed, T, Dmax):
+    """Sampled tree acceptance by enumerating every root-to-node path and
+    testing each of its draft nodes with Python floats; the correction token
+    by a Python-loop exponential race over scalar Philox words."""
+    from .philox import philox4x32, uniform_open
+    B, N = len(parent), len(parent[0])
+    V, Nd = len(logits[0][0]), len(draft_logits[0])
+    out_len, out_path, out_corr = [], [], []
+    for b in range(B):
+        par = [int(x) for x in parent[b]]
+        if not _valid_tree(par):
+            out_len.append(-1); out_path.append([-1] * Dmax); out_corr.append(-1)
+            continue
+        paths = [_root_path(par, i) for i in range(N)]
+        if max(len(pth) for pth in paths) - 1 > Nd:
+            out_len.append(-1); out_path.append([-1] * Dmax); out_corr.append(-1)
+            continue
+        best = None
+        for i, pth in enumerate(paths):
+            ok = True
+            for d in range(1, len(pth)):
+                node, up = pth[d], pth[d - 1]
+                y = int(draft_tok[b][node])
+                pu = _softmax_list(logits[b][up], T)[y]
+                qd = _softmax_list(draft_logits[b][d - 1], T)[y]
+                ok = ok and float(u_accept[b][node]) * qd < pu
+            if ok and (best is None or len(pth) > len(paths[best])):
+                best = i
+        pth = paths[best]
+        if len(pth) > Dmax:
+            out_len.append(-1); out_path.append([-1] * Dmax); out_corr.append(-1)
+            continue
+        pv = _softmax_list(logits[b][best], T)
+        if any(par[i] == best for i in range(1, N)):
+            qn = _softmax_list(draft_logits[b][len(pth) - 1], T)
+            w = [max(a - c, 0.0) for a, c in zip(pv, qn)]
+        else:
+            w = pv
+        if not any(x > 0 for x in w):
+            w = pv
+        tok, top = -1, -1.0
+        for x in range(V):
+            word = philox4x32((x // 4, b, 0, 0), (seed & 0xFFFFFFFF, seed >> 32))[x % 4]
+            race = w[x] / -math.log(uniform_open(word)) if w[x] > 0 else -1.0
+            if race > top:
+                tok, top = x, race
+        out_len.append(len(pth))
+        out_path.append(pth + [-1] * (Dmax - len(pth)))
+        out_corr.append(tok)
+    return np.array(out_len), np.array(out_path), np.array(out_corr)

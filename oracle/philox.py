@@ -30,9 +30,10 @@ def philox4x32(counter, key, rounds: int = 10):
 
 
 def uniform_open(word: int) -> float:
-    """A 32-bit output as a float in (0, 1): (word + 1/2) / 2^32, exact in
-    float64 and never 0 or 1."""
-    return (int(word) + 0.5) / 4294967296.0
+    """A 32-bit output as a number in (0, 1) from its top 23 bits:
+    ((word >> 9) + 1/2) / 2^23.  Every value is exact in fp32 (the
+    precision a GPU draws it in) and is never 0 or 1."""
+    return ((int(word) >> 9) + 0.5) / 8388608.0
 
 
 def philox4x32_array(c0, c1, c2, c3, k0: int, k1: int, rounds: int = 10):

@@ -30,7 +30,8 @@ Readings where the paper is silent:
     argmax_x w(x) / E_x with E_x = -ln U(b, x) (equivalently Gumbel-max), ties
     to the lowest index, where U(b, x) is word x mod 4 of
     Philox4x32-10(counter = (x div 4, b, 0, 0), key = (seed low, seed high))
-    mapped to (0, 1) by (word + 1/2) / 2^32;
+    mapped to (0, 1) by its top 23 bits, ((word >> 9) + 1/2) / 2^23, a value
+    exact in fp32;
   * a tree deeper than the draft logits, an invalid tree or a path longer
     than Dmax give accept_len = -1, path all -1 and correction -1.
 """
@@ -38,7 +39,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from .philox import philox4x32_array, uniform_open
+from .philox import philox4x32_array
 from .tree_attention import tree_structure
 
 
@@ -55,7 +56,7 @@ def race_uniforms(b: int, V: int, seed: int) -> np.ndarray:
     out = philox4x32_array(ctr, np.full(n4, b), np.zeros(n4), np.zeros(n4),
                            seed & 0xFFFFFFFF, (seed >> 32) & 0xFFFFFFFF)
     words = np.stack(out, axis=1).reshape(-1)[:V]
-    return (words.astype(np.float64) + 0.5) / 4294967296.0
+    return ((words >> np.uint64(9)).astype(np.float64) + 0.5) / 8388608.0
 
 
 def race_sample(w: np.ndarray, b: int, seed: int):

@@ -41,10 +41,14 @@ def test_philox_array_matches_scalar():
         assert tuple(int(a[n]) for a in arr) == philox4x32(ctr[n], key)
 
 
-def test_uniform_is_open_and_exact():
-    assert uniform_open(0) == 0.5 / 2**32
-    assert uniform_open(0xFFFFFFFF) == 1 - 0.5 / 2**32
+def test_uniform_is_open_and_exact_in_fp32():
+    assert uniform_open(0) == 0.5 / 2**23
+    assert uniform_open(0xFFFFFFFF) == 1 - 0.5 / 2**23
     assert 0 < uniform_open(0) < uniform_open(0xFFFFFFFF) < 1
+    rng = np.random.default_rng(1)
+    for w in rng.integers(0, 2**32, size=1000):
+        u = uniform_open(int(w))
+        assert float(np.float32(u)) == u
 
 
 def _case(rng, B=3, N=10, V=6, Nd=4):

@@ -183,6 +183,7 @@ def summarize_trace(trace_dir, bench_log, workload):
             f"    paged attention ({d['page_block']}-row blocks) {d['paged_attention_us']:.2f} us, "
             f"tree-tail attention {d['tree_tail_attention_us']:.2f} us, "
             f"path commit {d['commit_us']:.2f} us",
+            f"    non-greedy acceptance (T = 1) {d['sampled_accept']['us']:.2f} us",
             f"    training-mask attention ({d['training_mask_attention']['anchors']} blocks of "
             f"{d['training_mask_attention']['block']} over {d['training_mask_attention']['context']}"
             f" context rows) {d['training_mask_attention']['us']:.1f} us", ""]
@@ -299,8 +300,8 @@ def main():
 
     import torch
     from paper_2606_18394_amd import (block_causal_attention, build_tree, commit_path,
-                                      draft_topw, synth, tree_accept, tree_verify_attention,
-                                      tree_verify_attention_paged)
+                                      draft_topw, synth, tree_accept, tree_accept_sampled,
+                                      tree_verify_attention, tree_verify_attention_paged)
     from paper_2606_18394_amd.binding import load_library
 
     load_library()
@@ -444,6 +445,21 @@ def main():
     def build(r):
         build_tree(dtok, dlp, w.N)
 
+    # Non-greedy (T = 1) acceptance of the same trees: the target logits of
+    # the replica, the draft head's logits, one uniform per node.
+    u_acc = torch.from_numpy(np.random.default_rng(w.seed + 5).random(
+        (w.B, w.N), dtype=np.float32)).to(dev)
+    s_len = torch.empty(w.B, dtype=torch.int32, device=dev)
+    s_path = torch.empty(w.B, w.Dmax, dtype=torch.int32, device=dev)
+    s_corr = torch.empty(w.B, dtype=torch.int32, device=dev)
+    ws_samp = torch.zeros(load_library().tv_tree_accept_sampled_workspace(w.B, w.N, w.V, w.depth),
+                          dtype=torch.uint8, device=dev)
+
+    def sampled(r):
+        tree_accept_sampled(reps[r]["logits"], dlogs[r], draft_d, parent, u_acc, 1234 + r, 1.0,
+                            w.Dmax, accept_len=s_len, path=s_path, correction=s_corr,
+                            workspace_tensor=ws_samp)
+
     # Launches are recorded once into HIP graphs (one graph runs the R
     # replicas in turn, R more graphs run one replica each) so the timed
     # region measures the GPU, not Python's launch overhead.
@@ -468,7 +484,7 @@ def main():
         build(s % R)
     for name, fn in [("step", step), ("attn", attn), ("accept", accept), ("topw", topw),
                      ("build", build), ("attn_paged", attn_paged), ("attn_tail", attn_tail),
-                     ("train_attn", train_attn),
+                     ("train_attn", train_attn), ("sampled", sampled),
                      ("reset", reset),
                      ("commit", commit)]:
         graphs[name] = (capture(fn, range(R)), [capture(fn, [r]) for r in range(R)])
@@ -499,6 +515,7 @@ def main():
     ms_paged = timed("attn_paged", args.steps)
     ms_tail = timed("attn_tail", args.steps)
     ms_train = timed("train_attn", max(10, args.steps // 10))
+    ms_samp = timed("sampled", args.steps)
     ms_commit = max(0.0, timed("commit", args.steps) - timed("reset", args.steps))
     attn(0)
     ref0 = outs[0].clone()
@@ -514,6 +531,10 @@ def main():
     assert 1 <= ln <= w.Dmax, ln
 
     attn_bytes, attn_flops, acc_bytes = algorithmic_work(inp, w)
+    # target logits + draft logits read once, plus two rows per sequence for
+    # the correction race
+    esz = 4 if w.logits_dtype == "f32" else 2
+    samp_bytes = (w.B * (w.N + w.depth) + 2 * w.B) * w.V * esz
     if ms_attn >= ms_acc:
         t = ms_attn * 1e-3
         if attn_bytes / (HBM_PEAK_GBS * 1e9) >= attn_flops / (BF16_PEAK_TFLOPS * 1e12):
@@ -566,6 +587,9 @@ def main():
                    "paged_bit_identical": paged_same,
                    "paged_attention_GBps": attn_bytes / (ms_paged * 1e-3) / 1e9,
                    "tree_tail_attention_us": ms_tail * 1e3,
+                   "sampled_accept": {
+                       "us": ms_samp * 1e3, "temperature": 1.0,
+                       "bytes": samp_bytes, "GBps": samp_bytes / (ms_samp * 1e-3) / 1e9},
                    "training_mask_attention": {
                        "anchors": TA, "block": TS, "context": TL, "us": ms_train * 1e3,
                        "flops": train_flops,

@@ -284,6 +284,49 @@ int tv_build_tree(const int32_t* tok, const float* logp, const int32_t* root_tok
                   int Nd, int W, int budget, int32_t* parent, int32_t* token, int32_t* depth,
                   float* score, int32_t* n_nodes, hipStream_t stream);
 
+/*
+ * Non-greedy (temperature) tree acceptance (Sec. 2.4: the speculative
+ * sampling rule applied along the tree's branches, with a correction token
+ * drawn from the target when a draft is rejected).
+ *
+ * With p_u = softmax(logits[b, u] / T) the target's next-token distribution
+ * at node u and q_d = softmax(draft_logits[b, d - 1] / T) the draft head's
+ * distribution of depth-d tokens, draft node i (token y, parent u, depth d)
+ * passes its test when u_accept[b, i] * q_d(y) < p_u(y), i.e.
+ * u_accept < min(1, p/q).  It is accepted when it passes and its parent is
+ * accepted; the root always is.  The deepest accepted node v (lowest index
+ * among equally deep ones) gives path and accept_len exactly as in
+ * tv_tree_accept.  correction[b] is drawn at v from the residual
+ * max(0, p_v - q_{d(v)+1}) (normalised) when v has children, from p_v when
+ * it has none or the residual is all zero: the token x maximising
+ * w(x) / -ln U(b, x), ties to the lower index, where U(b, x) takes word x % 4
+ * of Philox4x32-10 (Salmon et al., SC 2011) with counter (x / 4, b, 0, 0)
+ * and key (seed & 0xFFFFFFFF, seed >> 32), mapped to (0, 1) as
+ * ((word >> 9) + 0.5) / 2^23.
+ *
+ *   logits       [B, N, V]  bf16 or fp32 (logits_dtype)  target logits
+ *   draft_logits [B, Nd, V] bf16 or fp32 (draft_dtype)   draft-head logits,
+ *                           row d - 1 for depth d
+ *   draft_tok, parent [B, N] int32, as in tv_tree_accept
+ *   u_accept     [B, N] fp32 uniforms in [0, 1) (entry 0 of a row unused)
+ *   accept_len [B], path [B, Dmax], correction [B] int32 outputs; an invalid
+ *     tree, one deeper than Nd, or a path longer than Dmax gives -1, a -1
+ *     path and correction -1.
+ *
+ * Requirements: temperature > 0 and finite; 1 <= N <= TV_MAX_NODES,
+ * 1 <= Nd <= TV_MAX_DRAFT_DEPTH, V >= 1, Dmax >= 1, B*N <= 2^24; logits
+ * finite.  Workspace: tv_tree_accept_sampled_workspace(B, N, V, Nd) bytes,
+ * 16-byte aligned (needs no zero fill).  The decisions are taken in fp32:
+ * a test within about 1e-6 (relative) of its threshold may go either way.
+ */
+size_t tv_tree_accept_sampled_workspace(int B, int N, int V, int Nd);
+int tv_tree_accept_sampled(const void* logits, int logits_dtype, const void* draft_logits,
+                           int draft_dtype, const int32_t* draft_tok, const int32_t* parent,
+                           const float* u_accept, unsigned long long seed, float temperature,
+                           int B, int N, int V, int Nd, int Dmax, int32_t* accept_len,
+                           int32_t* path, int32_t* correction, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -61,15 +61,18 @@ def race_uniforms(b: int, V: int, seed: int) -> np.ndarray:
 
 def race_sample(w: np.ndarray, b: int, seed: int):
     """Exponential race over weights w >= 0: (token, relative gap between the
-    best and second-best race values; inf when only one is positive)."""
+    best and second-best race values (inf when only one is positive), the
+    second-best token)."""
     e = -np.log(race_uniforms(b, len(w), seed))
     score = np.where(w > 0, w / e, -1.0)
     tok = int(np.argmax(score))
     top = score[tok]
-    rest = np.delete(score, tok)
-    second = rest.max() if rest.size else -1.0
+    rest = score.copy()
+    rest[tok] = -1.0
+    runner = int(np.argmax(rest))
+    second = rest[runner]
     gap = np.inf if second <= 0 else (top - second) / top
-    return tok, gap
+    return tok, gap, runner
 
 
 def tree_accept_sampled(logits, draft_logits, draft_tok, parent, u_accept, seed: int,
@@ -77,7 +80,8 @@ def tree_accept_sampled(logits, draft_logits, draft_tok, parent, u_accept, seed:
     """logits [B, N, V], draft_logits [B, Nd, V], draft_tok/parent [B, N],
     u_accept [B, N].  Returns (accept_len [B], path [B, Dmax],
     correction [B]) as int32, and with detail=True a dict of per-node test
-    margins (p - u q, relative) and the sampling gap per sequence."""
+    margins (|p - u q| relative to max(p, q)), the sampling gap and the
+    second-best token of each sequence's race."""
     lg = np.asarray(logits, dtype=np.float64)
     dl = np.asarray(draft_logits, dtype=np.float64)
     B, N, V = lg.shape
@@ -88,6 +92,7 @@ def tree_accept_sampled(logits, draft_logits, draft_tok, parent, u_accept, seed:
     corr = np.full(B, -1, dtype=np.int32)
     margin = np.full((B, N), np.inf)
     gaps = np.full(B, np.inf)
+    runner = np.full(B, -1, dtype=np.int32)
     for b in range(B):
         valid, _, depth = tree_structure(parent[b])
         if not valid or depth.max() > Nd:
@@ -118,7 +123,7 @@ def tree_accept_sampled(logits, draft_logits, draft_tok, parent, u_accept, seed:
         w = np.maximum(p[best] - q[depth[best]], 0.0) if has_child else p[best]
         if not np.any(w > 0):
             w = p[best]
-        corr[b], gaps[b] = race_sample(w, b, seed)
+        corr[b], gaps[b], runner[b] = race_sample(w, b, seed)
     if detail:
-        return accept_len, path, corr, {"margin": margin, "gap": gaps}
+        return accept_len, path, corr, {"margin": margin, "gap": gaps, "runner_up": runner}
     return accept_len, path, corr

@@ -8,7 +8,7 @@ and raises if it is missing.
 
 __all__ = ["tree_verify_attention", "tree_verify_attention_paged", "tree_accept",
            "commit_path", "commit_path_paged", "draft_topw", "build_tree",
-           "block_causal_attention", "load_library"]
+           "block_causal_attention", "tree_accept_sampled", "load_library"]
 
 
 def tree_verify_attention(*args, **kwargs):
@@ -48,6 +48,11 @@ def build_tree(*args, **kwargs):
 
 def block_causal_attention(*args, **kwargs):
     from .binding import block_causal_attention as f
+    return f(*args, **kwargs)
+
+
+def tree_accept_sampled(*args, **kwargs):
+    from .binding import tree_accept_sampled as f
     return f(*args, **kwargs)
 
 

@@ -67,6 +67,12 @@ def load_library() -> ctypes.CDLL:
         lib.tv_block_causal_attention.restype = ci
         lib.tv_block_causal_attention.argtypes = (
             [vp] * 5 + [i32p, vp] + [ci] * 7 + [ctypes.c_float, vp, sz, vp])
+        lib.tv_tree_accept_sampled_workspace.restype = sz
+        lib.tv_tree_accept_sampled_workspace.argtypes = [ci] * 4
+        lib.tv_tree_accept_sampled.restype = ci
+        lib.tv_tree_accept_sampled.argtypes = (
+            [vp, ci, vp, ci, i32p, i32p, vp, ctypes.c_ulonglong, ctypes.c_float] + [ci] * 5
+            + [i32p, i32p, i32p, vp, sz, vp])
         lib.tv_commit_path.restype = ci
         lib.tv_commit_path.argtypes = [vp, vp, i32p, i32p, vp, vp, i32p] + [ci] * 6 + [vp]
         lib.tv_commit_path_paged.restype = ci
@@ -218,6 +224,52 @@ def block_causal_attention(q, k_ctx, v_ctx, k_blk, v_blk, anchors, out, scale=No
         B, A, S, Hq, Hkv, D, L, 0.0 if scale is None else float(scale), _ptr(ws), ws.numel(),
         ctypes.c_void_p(stream)))
     return out
+
+
+def _dtype_code(t, name):
+    if t.dtype == torch.bfloat16:
+        return TV_BF16
+    if t.dtype == torch.float32:
+        return TV_F32
+    raise ValueError(f"{name} must be bfloat16 or float32, got {t.dtype}")
+
+
+def tree_accept_sampled(logits, draft_logits, draft_tok, parent, u_accept, seed, temperature,
+                        Dmax, accept_len=None, path=None, correction=None, workspace_tensor=None):
+    """Non-greedy tree acceptance.  logits [B,N,V], draft_logits [B,Nd,V]
+    (bf16 or fp32), draft_tok/parent [B,N] int32, u_accept [B,N] fp32.
+    Returns (accept_len [B], path [B,Dmax], correction [B]) int32."""
+    lib = load_library()
+    B, N, V = logits.shape
+    Nd = draft_logits.shape[1]
+    dev = logits.device
+    dt, ddt = _dtype_code(logits, "logits"), _dtype_code(draft_logits, "draft_logits")
+    _need(logits, "logits", logits.dtype, (B, N, V), dev)
+    _need(draft_logits, "draft_logits", draft_logits.dtype, (B, Nd, V), dev)
+    _need(draft_tok, "draft_tok", torch.int32, (B, N), dev)
+    _need(parent, "parent", torch.int32, (B, N), dev)
+    _need(u_accept, "u_accept", torch.float32, (B, N), dev)
+    if accept_len is None:
+        accept_len = torch.empty(B, dtype=torch.int32, device=dev)
+    if path is None:
+        path = torch.empty(B, Dmax, dtype=torch.int32, device=dev)
+    if correction is None:
+        correction = torch.empty(B, dtype=torch.int32, device=dev)
+    _need(accept_len, "accept_len", torch.int32, (B,), dev)
+    _need(path, "path", torch.int32, (B, Dmax), dev)
+    _need(correction, "correction", torch.int32, (B,), dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    need = lib.tv_tree_accept_sampled_workspace(B, N, V, Nd)
+    if need == 0:
+        _check(-2)
+    ws = workspace_tensor if workspace_tensor is not None else workspace("sample", need, dev,
+                                                                         stream)
+    _check(lib.tv_tree_accept_sampled(
+        _ptr(logits), dt, _ptr(draft_logits), ddt, _ptr(draft_tok), _ptr(parent), _ptr(u_accept),
+        ctypes.c_ulonglong(int(seed) & 0xFFFFFFFFFFFFFFFF), ctypes.c_float(temperature), B, N, V,
+        Nd, Dmax, _ptr(accept_len), _ptr(path), _ptr(correction), _ptr(ws), ws.numel(),
+        ctypes.c_void_p(stream)))
+    return accept_len, path, correction
 
 
 def _tree_nodes(k_tree, n_nodes):

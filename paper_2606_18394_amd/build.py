@@ -10,7 +10,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libtreeverify.so")
-SOURCES = ["tv_api.hip", "tv_attention.hip", "tv_accept.hip", "tv_draft.hip", "tv_cache.hip"]
+SOURCES = ["tv_api.hip", "tv_attention.hip", "tv_accept.hip", "tv_draft.hip", "tv_cache.hip",
+           "tv_sample.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

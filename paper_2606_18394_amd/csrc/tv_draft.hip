@@ -348,8 +348,6 @@ struct BuildArgs {
   int Nd, W, budget;
 };
 
-constexpr int kMaxDraftDepth = 64;  // == TV_MAX_DRAFT_DEPTH
-
 __global__ __launch_bounds__(64) void build_tree(BuildArgs a) {
   __shared__ float cand_lp[kMaxDraftDepth * kTopwMax];
   __shared__ int cand_tok[kMaxDraftDepth * kTopwMax];

@@ -234,6 +234,43 @@ inline size_t topw_ws_bytes(int B, int Nd) {
   return (size_t)(rows * accept_split_cap(rows)) * kTopwPartBytes;
 }
 
+// Non-greedy acceptance: an lse scan over the B*N target rows and B*Nd
+// draft rows (splits as in the acceptance scan, in vocabulary entries that
+// are multiples of 8), then one workgroup per (sequence, race split) that
+// repeats the acceptance and races its vocabulary slice (about 512
+// workgroups in all, at least 8 entries per thread).
+constexpr int kMaxDraftDepth = 64;       // == TV_MAX_DRAFT_DEPTH
+constexpr int kMaxRaceSplit = 64;
+
+struct SamplePlan {
+  int nsplit, nrace, lse_grid;
+  long long eps, rps;  // vocabulary entries per lse / race split
+  size_t race_bytes, ws_bytes;
+};
+
+inline SamplePlan sample_plan(int B, int N, int V, int Nd) {
+  SamplePlan p{};
+  const long long rows = (long long)B * (N + Nd);
+  long long ns = accept_split_cap(rows);
+  const long long per_round = (long long)kScanThreads * kScanLoadsPerThread * 8;
+  const long long by_size = ((long long)V + per_round - 1) / per_round;
+  if (ns > by_size) ns = by_size;
+  if (ns < 1) ns = 1;
+  p.eps = ((V + ns - 1) / ns + 7) / 8 * 8;
+  p.nsplit = (int)((V + p.eps - 1) / p.eps);
+  p.lse_grid = (int)(rows * p.nsplit);
+  long long nr = (512 + B - 1) / B;
+  const long long by_v = ((long long)V + 8 * 256 - 1) / (8 * 256);
+  if (nr > by_v) nr = by_v;
+  if (nr > kMaxRaceSplit) nr = kMaxRaceSplit;
+  if (nr < 1) nr = 1;
+  p.rps = ((V + nr - 1) / nr + 7) / 8 * 8;
+  p.nrace = (int)((V + p.rps - 1) / p.rps);
+  p.race_bytes = ((size_t)B * p.nrace * 16 + 255) / 256 * 256;
+  p.ws_bytes = p.race_bytes + (size_t)rows * p.nsplit * 8;
+  return p;
+}
+
 // LDS of the acceptance of one sequence of N nodes: per node the target
 // argmax (int), jump pointers and depths (2 x 2 short, double-buffered),
 // parent (short) and acceptance flags (2 bytes); the finish kernel adds the

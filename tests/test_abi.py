@@ -268,3 +268,37 @@ def test_block_causal_host_errors():
     assert _bc(lib, out=FAKE + 4) == -7
     assert lib.tv_block_causal_attention_workspace(1, 4, 16, 32, 8, 128, 4096) > 256  # splits
     assert _bc(lib, A=4, ws=None) == -5
+
+
+def _samp(lib, **kw):
+    a = dict(lg=FAKE, dt=0, dl=FAKE, ddt=0, tok=FAKE, par=FAKE, u=FAKE, seed=1, T=1.0, B=1, N=64,
+             V=151936, Nd=8, Dmax=9, ln=FAKE, path=FAKE, corr=FAKE, ws=FAKE, wsb=1 << 40)
+    a.update(kw)
+    return lib.tv_tree_accept_sampled(
+        a["lg"], a["dt"], a["dl"], a["ddt"], a["tok"], a["par"], a["u"], a["seed"],
+        ctypes.c_float(a["T"]), a["B"], a["N"], a["V"], a["Nd"], a["Dmax"], a["ln"], a["path"],
+        a["corr"], a["ws"], a["wsb"], None)
+
+
+def test_sampled_accept_host_errors():
+    lib = _lib()
+    assert lib.tv_tree_accept_sampled_workspace(1, 64, 151936, 8) > 0
+    assert lib.tv_tree_accept_sampled_workspace(1, 64, 151936, 65) == 0
+    assert lib.tv_tree_accept_sampled_workspace(1, 64, 151936, 0) == 0
+    assert _samp(lib, lg=None) == -1
+    assert _samp(lib, dl=None) == -1
+    assert _samp(lib, u=None) == -1
+    assert _samp(lib, corr=None) == -1
+    assert _samp(lib, dt=2) == -3
+    assert _samp(lib, ddt=-1) == -3
+    assert _samp(lib, T=0.0) == -2
+    assert _samp(lib, T=-1.0) == -2
+    assert _samp(lib, T=float("inf")) == -2
+    assert _samp(lib, T=float("nan")) == -2
+    assert _samp(lib, Nd=0) == -2
+    assert _samp(lib, Nd=65) == -4
+    assert _samp(lib, N=2049) == -4
+    assert _samp(lib, Dmax=0) == -2
+    assert _samp(lib, ws=None) == -5
+    assert _samp(lib, wsb=64) == -5
+    assert _samp(lib, ws=FAKE + 8) == -7

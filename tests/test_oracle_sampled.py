@@ -102,7 +102,7 @@ def test_draft_equal_to_target_accepts_a_chain():
     ln, path, corr = tree_accept_sampled(lg, dl, tok, par, u, 9, 1.0, N)
     assert ln[0] == N and path[0].tolist() == list(range(N))
     # the last node is a leaf: its correction comes from p there
-    tok_ref, _ = race_sample(np.exp(lg[0, N - 1]) / np.exp(lg[0, N - 1]).sum(), 0, 9)
+    tok_ref = race_sample(np.exp(lg[0, N - 1]) / np.exp(lg[0, N - 1]).sum(), 0, 9)[0]
     assert corr[0] == tok_ref
 
 
@@ -130,7 +130,7 @@ def test_race_sampler_frequencies():
     w = np.array([0.1, 0.0, 0.45, 0.25, 0.2])
     counts = np.zeros(5)
     for s in range(4000):
-        tok, _ = race_sample(w, 0, s)
+        tok = race_sample(w, 0, s)[0]
         counts[tok] += 1
     freq = counts / counts.sum()
     assert counts[1] == 0

@@ -311,6 +311,69 @@ __global__ __launch_bounds__(256) void accept_finish(AcceptArgs a) {
   accept_sequence(a, b, l, pv, dv);
 }
 
+// Second kernel for trees of at most 64 nodes: one wave per sequence, lane
+// i holding node i, so the merge, the pointer jumping and the path need no
+// LDS and no workgroup barrier (lane exchanges only).  Same results as
+// accept_finish.
+__global__ __launch_bounds__(64) void accept_finish_wave(AcceptArgs a) {
+  const int b = blockIdx.x, i = threadIdx.x;
+  const int N = a.N;
+  const bool node = i < N;
+  const int p = node ? a.parent[(size_t)b * N + i] : 0;
+  const int y = node ? a.draft[(size_t)b * N + i] : 0;
+  // this node's prediction: the max of its split keys, loaded together
+  unsigned long long key = 0ull;
+  if (node) {
+    const unsigned long long* kp = a.part + ((size_t)b * N + i) * a.nsplit;
+    constexpr int kLoads = kAcceptMaxSplit;
+    unsigned long long kv[kLoads];
+#pragma unroll
+    for (int k = 0; k < kLoads; ++k) kv[k] = k < a.nsplit ? kp[k] : 0ull;
+#pragma unroll
+    for (int k = 0; k < kLoads; ++k) key = umax64(key, kv[k]);
+  }
+  const int tgt = key_index(key);
+  if (node && a.tgt_out) a.tgt_out[(size_t)b * N + i] = tgt;
+  const int badi = node && ((i == 0) ? (p != -1) : (p < 0 || p >= i));
+  const bool bad = __any(badi);
+  int len = -1, v = 0, depth = 0;
+  int jmp = node && i > 0 && !badi ? p : 0;  // the root (and padding) jump to node 0
+  if (!bad) {
+    // every lane takes part in a lane exchange (an inactive source lane
+    // would read as zero), so the shuffle comes before the selection
+    const int tgt_parent = __shfl(tgt, jmp);
+    int ok = !node ? 0 : (i == 0 ? 1 : (y == tgt_parent));
+    int dep = node && i > 0 ? 1 : 0;
+    // pointer jumping: ceil(log2 64) = 6 rounds reach the root
+    for (int r = 0; r < 6 && __any(jmp != 0); ++r) {
+      ok &= __shfl(ok, jmp);
+      dep += __shfl(dep, jmp);
+      jmp = __shfl(jmp, jmp);
+    }
+    unsigned int k = ok ? ((unsigned int)dep << 16) | (0xFFFFu - (unsigned int)i) : 0u;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      const unsigned int other = __shfl_xor(k, o);
+      k = other > k ? other : k;
+    }
+    depth = (int)(k >> 16);
+    v = (int)(0xFFFFu - (k & 0xFFFFu));
+    len = depth + 1 > a.Dmax ? -1 : depth + 1;
+  }
+  int32_t* pth = a.path + (size_t)b * a.Dmax;
+  for (int k = i; k < a.Dmax; k += 64)
+    if (k >= len) pth[k] = -1;
+  if (len > 0) {
+    // walk up from v: the node at depth k of the path goes to entry k
+    int u = v;
+    for (int k = depth; k >= 0; --k) {
+      if (i == 0) pth[k] = u;
+      u = __shfl(p, u);
+    }
+  }
+  if (i == 0) a.accept_len[b] = len;
+}
+
 hipError_t launch_accept(const void* logits, int f32, const int32_t* draft, const int32_t* parent,
                          int B, int N, int V, int Dmax, int32_t* accept_len, int32_t* path,
                          int32_t* tgt_out, void* ws, hipStream_t st) {
@@ -342,8 +405,11 @@ hipError_t launch_accept(const void* logits, int f32, const int32_t* draft, cons
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(accept_finish, dim3(B), dim3(256), accept_lds_bytes(N) + (size_t)N * 8, st,
-                     a);
+  if (N <= 64)
+    hipLaunchKernelGGL(accept_finish_wave, dim3(B), dim3(64), 0, st, a);
+  else
+    hipLaunchKernelGGL(accept_finish, dim3(B), dim3(256), accept_lds_bytes(N) + (size_t)N * 8,
+                       st, a);
   return hipGetLastError();
 }
 

@@ -266,7 +266,56 @@ __global__ __launch_bounds__(kSampleThreads) void sample_accept(SampleArgs a, in
   bad = __syncthreads_or(bad);
 
   int len = -1, v = 0, dv = 0;
-  if (!bad) {
+  if (!bad && N <= 64) {
+    // Trees of at most 64 nodes: wave 0 alone, lane i holding node i, with
+    // lane exchanges in place of LDS rounds and workgroup barriers.  Every
+    // lane of the wave takes part in each exchange.
+    __shared__ int s_res[3];
+    if (wave == 0) {
+      const int i = lane;
+      const bool node = i < N;
+      const int pp = node && i > 0 ? par[i] : 0;  // the root jumps to itself
+      int jmp = pp, dep = node && i > 0 ? 1 : 0;
+      for (int r = 0; r < 6 && __any(jmp != 0); ++r) {
+        dep += __shfl(dep, jmp);
+        jmp = __shfl(jmp, jmp);
+      }
+      const bool deep = __any(node && dep > Nd);
+      int ok = node ? 1 : 0;
+      if (node && i > 0 && dep <= Nd) {
+        const int y = tok[0];
+        ok = 0;
+        if (y >= 0 && y < V) {
+          const float pl = load_logit<F32T>(a.logits, ((size_t)b * N + pp) * V + y);
+          const float ql = load_logit<F32D>(a.dlogits, ((size_t)b * Nd + dep - 1) * V + y);
+          const float p = __expf(pl * a.invT - lse_t[pp]);
+          const float q = __expf(ql * a.invT - lse_d[dep - 1]);
+          ok = a.u[(size_t)b * N + i] * q < p;
+        }
+      }
+      jmp = pp;
+      for (int r = 0; r < 6 && __any(jmp != 0); ++r) {
+        ok &= __shfl(ok, jmp);
+        jmp = __shfl(jmp, jmp);
+      }
+      unsigned int k = ok ? ((unsigned int)dep << 16) | (0xFFFFu - (unsigned int)i) : 0u;
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) {
+        const unsigned int other = __shfl_xor(k, o);
+        k = other > k ? other : k;
+      }
+      if (lane == 0) {
+        const int d = (int)(k >> 16);
+        s_res[0] = deep || d + 1 > a.Dmax ? -1 : d + 1;
+        s_res[1] = (int)(0xFFFFu - (k & 0xFFFFu));
+        s_res[2] = d;
+      }
+    }
+    __syncthreads();
+    len = s_res[0];
+    v = s_res[1];
+    dv = s_res[2];
+  } else if (!bad) {
     // depths by pointer jumping (the root jumps to itself)
     for (int i = tid; i < N; i += kSampleThreads) {
       jmp0[i] = par[i];

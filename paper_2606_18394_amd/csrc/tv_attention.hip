@@ -615,9 +615,22 @@ void attn_main(AttnArgs a) {
   // waves run n_iter iterations so the per-iteration barriers line up
   const int n_iter = t1 > t0 ? (t1 - t0 + WK - 1) / WK : 0;
   const int n_mine = t0 + wk < t1 ? (t1 - t0 - wk + WK - 1) / WK : 0;  // valid tiles
+
+  // Issue order: parents, queries, then the first tiles' DMAs.  Loads
+  // complete in order and the compiler counts only its own loads, so its
+  // wait for the parents (at most the query loads still outstanding) leaves
+  // the younger DMAs in flight while the tree metadata is built.
+  constexpr int kParPerThread = (kMaxNodes + kThreads - 1) / kThreads;
+  int pv[kParPerThread];
+  if (has_tree) {
+    // indices clamped rather than branched on, so the loads stay in flight
+    const int32_t* pr = a.parent + (size_t)b * a.N;
 #pragma unroll
-  for (int i = 0; i < NS - 1; ++i)
-    if (i < n_mine) issue_tile<D, PW, kPaged>(src, dma_off, wr, lane, t0 + wk + WK * i, ring + i * STAGE);
+    for (int k = 0; k < kParPerThread; ++k) {
+      const int i = tid + kThreads * k;
+      pv[k] = a.parent ? pr[i < a.N ? i : a.N - 1] : i - 1;  // NULL: a chain
+    }
+  }
 
   // ---- queries: B operand of S^T = K Q^T, lane holds Q[row l16][8*g4 .. +8]
   const int wrow0 = r0 + kRowsPerWave * wr;
@@ -637,11 +650,18 @@ void attn_main(AttnArgs a) {
     }
   }
 
+#pragma unroll
+  for (int i = 0; i < NS - 1; ++i)
+    if (i < n_mine) issue_tile<D, PW, kPaged>(src, dma_off, wr, lane, t0 + wk + WK * i, ring + i * STAGE);
+
   // ---- tree structure: ancestor-or-self bitmask of this block's nodes
   if (has_tree) {
     int bad = 0;
-    for (int i = tid; i < a.N; i += kThreads) {
-      const int p = a.parent ? a.parent[(size_t)b * a.N + i] : i - 1;  // NULL: a chain
+#pragma unroll
+    for (int k = 0; k < kParPerThread; ++k) {
+      const int i = tid + kThreads * k;
+      if (i >= a.N) break;
+      const int p = pv[k];
       par[i] = p;
       bad |= (i == 0) ? (p != -1) : (p < 0 || p >= i);
     }

@@ -161,31 +161,41 @@ __global__ __launch_bounds__(kScanThreads) void topw_scan(TopwArgs a) {
   float m = -INFINITY, s = 0.f;
   const char* rowp = (const char*)a.logits + (size_t)row * a.V * (F32 ? 4 : 2);
   for (long long c = c0 + tid; c < c1; c += (long long)L * kScanThreads) {
-    float x[L][E];
+    // all L loads are issued first (past the end: the last chunk again),
+    // then decoded with the padding replaced by -inf bit patterns, so the
+    // loads are in flight together
+    constexpr unsigned int kNegInf = F32 ? 0xFF800000u : 0xFF80FF80u;
+    uint4 raw[L];
 #pragma unroll
     for (int u = 0; u < L; ++u) {
       const long long cu = c + (long long)u * kScanThreads;
+      const long long cl = cu < c1 ? cu : c1 - 1;
+      if (VEC) {
+        raw[u] = reinterpret_cast<const uint4*>(rowp)[cl];
+      } else if (F32) {
+        raw[u].x = reinterpret_cast<const unsigned int*>(rowp)[cl];
+      } else {
+        raw[u].x = (unsigned int)reinterpret_cast<const unsigned short*>(rowp)[cl] << 16;
+      }
+    }
+    float x[L][E];
 #pragma unroll
-      for (int e = 0; e < E; ++e) x[u][e] = -INFINITY;
-      if (cu < c1) {
-        if (VEC) {
-          const uint4 w = reinterpret_cast<const uint4*>(rowp)[cu];
-          const unsigned int ws[4] = {w.x, w.y, w.z, w.w};
+    for (int u = 0; u < L; ++u) {
+      const bool in = c + (long long)u * kScanThreads < c1;
+      const unsigned int ws[4] = {in ? raw[u].x : kNegInf, in ? raw[u].y : kNegInf,
+                                  in ? raw[u].z : kNegInf, in ? raw[u].w : kNegInf};
+      if (VEC) {
 #pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            if (F32) {
-              x[u][k] = __uint_as_float(ws[k]);
-            } else {
-              x[u][2 * k] = __uint_as_float(ws[k] << 16);
-              x[u][2 * k + 1] = __uint_as_float(ws[k] & 0xFFFF0000u);
-            }
+        for (int k = 0; k < 4; ++k) {
+          if (F32) {
+            x[u][k] = __uint_as_float(ws[k]);
+          } else {
+            x[u][2 * k] = __uint_as_float(ws[k] << 16);
+            x[u][2 * k + 1] = __uint_as_float(ws[k] & 0xFFFF0000u);
           }
-        } else if (F32) {
-          x[u][0] = reinterpret_cast<const float*>(rowp)[cu];
-        } else {
-          x[u][0] = __uint_as_float(
-              (unsigned int)reinterpret_cast<const unsigned short*>(rowp)[cu] << 16);
         }
+      } else {
+        x[u][0] = __uint_as_float(in ? raw[u].x : 0xFF800000u);
       }
     }
     float bm = -INFINITY;

@@ -143,23 +143,29 @@ __device__ __forceinline__ void lse_slice(const void* rowp, long long x0, long l
     const long long c0 = x0 / E, c1 = (x1 + E - 1) / E;
     const uint4* base = reinterpret_cast<const uint4*>(rowp);
     for (long long c = c0 + tid; c < c1; c += (long long)L * kScanThreads) {
-      float x[L][E];
+      // all L loads are issued first (past the end: the last chunk again),
+      // then decoded with the padding replaced by -inf bit patterns, so the
+      // loads are in flight together
+      constexpr unsigned int kNegInf = F32 ? 0xFF800000u : 0xFF80FF80u;
+      uint4 raw[L];
 #pragma unroll
       for (int u = 0; u < L; ++u) {
         const long long cu = c + (long long)u * kScanThreads;
+        raw[u] = base[cu < c1 ? cu : c1 - 1];
+      }
+      float x[L][E];
 #pragma unroll
-        for (int e = 0; e < E; ++e) x[u][e] = -INFINITY;
-        if (cu < c1) {
-          const uint4 w = base[cu];
-          const unsigned int ws[4] = {w.x, w.y, w.z, w.w};
+      for (int u = 0; u < L; ++u) {
+        const bool in = c + (long long)u * kScanThreads < c1;
+        const unsigned int ws[4] = {in ? raw[u].x : kNegInf, in ? raw[u].y : kNegInf,
+                                    in ? raw[u].z : kNegInf, in ? raw[u].w : kNegInf};
 #pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            if (F32) {
-              x[u][k] = __uint_as_float(ws[k]) * invT;
-            } else {
-              x[u][2 * k] = __uint_as_float(ws[k] << 16) * invT;
-              x[u][2 * k + 1] = __uint_as_float(ws[k] & 0xFFFF0000u) * invT;
-            }
+        for (int k = 0; k < 4; ++k) {
+          if (F32) {
+            x[u][k] = __uint_as_float(ws[k]) * invT;
+          } else {
+            x[u][2 * k] = __uint_as_float(ws[k] << 16) * invT;
+            x[u][2 * k + 1] = __uint_as_float(ws[k] & 0xFFFF0000u) * invT;
           }
         }
       }

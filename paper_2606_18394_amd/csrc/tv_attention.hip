@@ -447,7 +447,13 @@ __device__ __forceinline__ void attend_tile(const unsigned char* kt_lds, const b
                                             float c, float inv_c, const MaskInfo& mk,
                                             const int (&node_rel)[NT], int g4, int l16) {
   f32x4 sc[2][NT];
+  // The score products run at raised wave priority: the SIMD's other wave
+  // is then mostly in its softmax (vector work) while these matrix
+  // instructions issue back to back (measured 5-8% faster on matrix-bound
+  // shapes than equal priority or raising it for the value products too).
+  __builtin_amdgcn_s_setprio(1);
   tile_scores<D, NT>(kt_lds, qf, sc, g4, l16);
+  __builtin_amdgcn_s_setprio(0);
   if (kMasked) tile_mask<NT>(sc, mk, node_rel);
   tile_reference<D / 16, NT>(sc, m, thr, o, lacc, c, inv_c);
   bf16x8 pf[NT];

@@ -159,8 +159,13 @@ __global__ __launch_bounds__(kScanThreads) void topw_scan(TopwArgs a) {
   TopList<K> top;
   top.init();
   float m = -INFINITY, s = 0.f;
+  // tau: a lower bound on the slice's W-th largest value, known after the
+  // first round; only elements >= tau reach the (divergent) list insertion
+  float tau = -INFINITY;
   const char* rowp = (const char*)a.logits + (size_t)row * a.V * (F32 ? 4 : 2);
-  for (long long c = c0 + tid; c < c1; c += (long long)L * kScanThreads) {
+  // rounds are uniform across the workgroup (the first ends at a barrier)
+  for (long long cb = c0; cb < c1; cb += (long long)L * kScanThreads) {
+    const long long c = cb + tid;
     // all L loads are issued first (past the end: the last chunk again),
     // then decoded with the padding replaced by -inf bit patterns, so the
     // loads are in flight together
@@ -203,22 +208,45 @@ __global__ __launch_bounds__(kScanThreads) void topw_scan(TopwArgs a) {
     for (int u = 0; u < L; ++u)
 #pragma unroll
       for (int e = 0; e < E; ++e) bm = fmaxf(bm, x[u][e]);
-    const float mn = fmaxf(m, bm);
-    float bs = 0.f;
+    if (bm != -INFINITY) {  // a thread past the slice end has only padding
+      const float mn = fmaxf(m, bm);
+      float bs = 0.f;
 #pragma unroll
-    for (int u = 0; u < L; ++u)
+      for (int u = 0; u < L; ++u)
 #pragma unroll
-      for (int e = 0; e < E; ++e) bs += __expf(x[u][e] - mn);  // exp(-inf) = 0 for padding
-    s = (m == -INFINITY ? 0.f : s * __expf(m - mn)) + bs;
-    m = mn;
-    // padding (-inf) never passes the threshold
-    if (bm > top.thr()) {
+        for (int e = 0; e < E; ++e) bs += __expf(x[u][e] - mn);  // exp(-inf) = 0 for padding
+      s = (m == -INFINITY ? 0.f : s * __expf(m - mn)) + bs;
+      m = mn;
+    }
+    if (cb == c0) {
+      // Each wave's q-th largest thread maximum, q = ceil(W / waves): every
+      // wave holds q elements at least that large, so at least W elements
+      // of the slice are >= the smallest of these.
+      constexpr int kWaves = kScanThreads / 64;
+      __shared__ float s_tau[kWaves];
+      const int q = (W + kWaves - 1) / kWaves;
+      float v = bm, kth = -INFINITY;
+      for (int r = 0; r < q; ++r) {
+        float bv = v;
+        int bi = lane;
+        wave_best(bv, bi);
+        kth = bv;
+        if (lane == bi) v = -INFINITY;  // taken
+      }
+      if (lane == 0) s_tau[wave] = kth;
+      __syncthreads();
+      tau = s_tau[0];
+#pragma unroll
+      for (int w = 1; w < kWaves; ++w) tau = fminf(tau, s_tau[w]);
+    }
+    // padding (-inf) never passes; equal values keep the earlier index
+    if (bm >= tau && bm > top.thr()) {
 #pragma unroll
       for (int u = 0; u < L; ++u) {
         const long long cu = c + (long long)u * kScanThreads;
 #pragma unroll
         for (int e = 0; e < E; ++e)
-          if (x[u][e] > top.thr()) top.insert(x[u][e], (int)(cu * E + e));
+          if (x[u][e] >= tau && x[u][e] > top.thr()) top.insert(x[u][e], (int)(cu * E + e));
       }
     }
   }

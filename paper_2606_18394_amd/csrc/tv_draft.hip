@@ -467,6 +467,56 @@ __global__ __launch_bounds__(64) void build_tree(BuildArgs a) {
   if (lane == 0) a.n_nodes[b] = n;
 }
 
+// Budgets of at most 64 nodes: node i lives in the registers of lane i, so
+// a pop is one wave argmax over the open nodes (no per-lane rescan) and the
+// new children are written by their own lanes.  Same selections, same fp32
+// sums, same outputs as build_tree.
+__global__ __launch_bounds__(64) void build_tree_wave(BuildArgs a) {
+  __shared__ float cand_lp[kMaxDraftDepth * kTopwMax];
+  __shared__ int cand_tok[kMaxDraftDepth * kTopwMax];
+  const int b = blockIdx.x, lane = threadIdx.x;
+  const int Nd = a.Nd, W = a.W, budget = a.budget;
+  const size_t cbase = (size_t)b * Nd * W;
+  for (int k = lane; k < Nd * W; k += 64) {
+    cand_lp[k] = a.logp[cbase + k];
+    cand_tok[k] = a.tok[cbase + k];
+  }
+  __syncthreads();
+  // this lane's node (the root on lane 0)
+  float s = 0.f;
+  int tk = lane == 0 && a.root_tok ? a.root_tok[b] : -1;
+  int par = -1, dep = 0;
+  bool open = lane == 0;  // Nd >= 1
+  int n = 1;
+  // each pop of an open node adds at least one node, so budget - 1 pops end it
+  for (int it = 0; it < budget && n < budget; ++it) {
+    float gs = open ? s : -INFINITY;
+    int gi = open ? lane : 0x7FFFFFFF, gd = dep;
+    wave_best(gs, gi, gd);
+    if (gi == 0x7FFFFFFF) break;  // nothing open
+    if (lane == gi) open = false;
+    const int nk = min(W, budget - n);
+    const int k = lane - n;
+    if (k >= 0 && k < nk) {
+      s = gs + cand_lp[gd * W + k];
+      tk = cand_tok[gd * W + k];
+      par = gi;
+      dep = gd + 1;
+      open = gd + 1 < Nd;
+    }
+    n += nk;
+  }
+  const size_t obase = (size_t)b * budget;
+  if (lane < budget) {
+    const bool used = lane < n;
+    a.parent[obase + lane] = used ? par : -1;
+    a.token[obase + lane] = used ? tk : -1;
+    a.depth[obase + lane] = used ? dep : -1;
+    if (a.score) a.score[obase + lane] = used ? s : -INFINITY;
+  }
+  if (lane == 0) a.n_nodes[b] = n;
+}
+
 hipError_t launch_build_tree(const int32_t* tok, const float* logp, const int32_t* root_tok, int B,
                              int Nd, int W, int budget, int32_t* parent, int32_t* token,
                              int32_t* depth, float* score, int32_t* n_nodes, hipStream_t st) {
@@ -482,7 +532,10 @@ hipError_t launch_build_tree(const int32_t* tok, const float* logp, const int32_
   a.Nd = Nd;
   a.W = W;
   a.budget = budget;
-  hipLaunchKernelGGL(build_tree, dim3(B), dim3(64), 0, st, a);
+  if (budget <= 64)
+    hipLaunchKernelGGL(build_tree_wave, dim3(B), dim3(64), 0, st, a);
+  else
+    hipLaunchKernelGGL(build_tree, dim3(B), dim3(64), 0, st, a);
   return hipGetLastError();
 }
 

@@ -110,6 +110,11 @@ BUILD_CASES = [
     (2, 12, 16, 2048, "normal"),   # largest budget
     (5, 4, 3, 1, "normal"),        # root only
     (1, 64, 2, 1000, "normal"),    # deepest draft
+    # budgets of at most 64 nodes (one node per lane)
+    (4, 5, 4, 60, "ties"),
+    (3, 2, 3, 64, "normal"),       # the full tree (13 nodes) ends before the budget
+    (2, 64, 2, 64, "normal"),      # deep and narrow
+    (2, 4, 16, 63, "normal"),
 ]
 
 

@@ -476,7 +476,9 @@ __device__ __forceinline__ void merge_chunks(const AttnArgs& a, size_t part0, in
   constexpr int NPW = kSplitCols ? 1 : NTG / kWaves;  // row tiles per wave
   constexpr int DPW = DT / WPN;                       // column tiles per wave
   constexpr int UB = 32 / DPW;                        // chunks per batch of loads
-  static_assert(DT % WPN == 0 && NTG % (kSplitCols ? 1 : kWaves) == 0, "merge split");
+  // every wave gets whole column tiles of one row tile, or whole row tiles
+  static_assert(kSplitCols ? (kWaves % NTG == 0 && DT % WPN == 0) : (NTG % kWaves == 0),
+                "merge split");
   const int g4 = lane >> 4, l16 = lane & 15;
 #pragma unroll
   for (int k = 0; k < NPW; ++k) {

@@ -51,6 +51,9 @@ def parse():
                     help="no GPU: turn the counter CSVs of four rocprofv3 --pmc runs (FETCH_SIZE "
                          "and WRITE_SIZE of this benchmark, then of --copy-only) into "
                          "profiles/traffic_attn_main_<workload>.json and .md")
+    ap.add_argument("--summarize-counters", nargs="+", default=None, metavar="PMC_DIR",
+                    help="no GPU: turn rocprofv3 --pmc runs of this benchmark (one or more "
+                         "output directories) into profiles/counters_attn_main_<workload>.md")
     ap.add_argument("--summarize-trace", nargs=2, default=None, metavar=("TRACE_DIR", "BENCH_LOG"),
                     help="no GPU: turn a rocprofv3 --kernel-trace --stats run of this benchmark and "
                          "the log of the same command run without the profiler into "
@@ -141,6 +144,80 @@ the scale factors are {fs:.4f} (fetch) and {ws:.4f} (write).
 | total | | {(fetch_b + write_b) / 1e6:.2f} |
 """)
     print(json.dumps(rec))
+
+
+SIMDS = 256 * 4        # MI355X: 256 CUs of 4 SIMDs
+CLOCK_HZ = 2.4e9
+
+
+def summarize_counters(dirs, workload):
+    """Per-dispatch medians of SQ counters of the verification attention
+    kernel (the contiguous-cache instantiation with the most dispatches) and
+    the utilisations they imply."""
+    import csv
+    import glob
+    import re
+    import statistics
+    pat = re.compile(r"attn_main<(\d+), (\d+), (\d+), (\d+)(?:, false)?>")
+    vals, durs, cmds = {}, {}, []
+    for d in dirs:
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            with open(f) as fh:
+                for r in csv.DictReader(fh):
+                    m = pat.search(r["Kernel_Name"])
+                    if not m:
+                        continue
+                    k = "attn_main<%s,%s,%s,%s>" % m.groups()
+                    vals.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(
+                        float(r["Counter_Value"]))
+                    durs.setdefault(k, []).append(
+                        (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9)
+    if not vals:
+        raise SystemExit("no attn_main dispatches in the counter runs")
+    kernel = max(vals, key=lambda k: len(durs[k]))
+    c = {n: statistics.median(v) for n, v in vals[kernel].items()}
+    t = statistics.median(durs[kernel])
+    lines = [f"# SQ counters: {kernel}, workload {workload}", "",
+             "Commands (repository root, rocprofv3 run from /tmp with TMPDIR=/tmp; each --pmc "
+             "set in a run of its own):", ""]
+    sets = ["SQ_WAVES SQ_BUSY_CYCLES SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU SQ_INSTS_MFMA "
+            "SQ_INSTS_LDS SQ_LDS_BANK_CONFLICT SQ_ACTIVE_INST_LDS",
+            "SQ_WAIT_INST_ANY SQ_ACTIVE_INST_VALU SQ_WAIT_ANY SQ_ACTIVE_INST_ANY "
+            "SQ_WAIT_INST_LDS SQ_LDS_IDX_ACTIVE"]
+    for cs in sets:
+        lines.append(f"    rocprofv3 --pmc {cs} --output-format csv -d <out> -o p -- python3 "
+                     f"bench.py --workload {workload} --no-cpu-baseline --steps 20 --warmup 2")
+    lines += [f"    python3 bench.py --workload {workload} --summarize-counters <out> <out2>", "",
+              f"Median over {len(durs[kernel])} counter-run dispatches of the kernel; its median "
+              f"duration in those runs is {t * 1e6:.1f} us.", "",
+              "| counter | median per dispatch |", "|---|---|"]
+    for n in sorted(c):
+        lines.append(f"| {n} | {c[n]:.0f} |")
+    lines += ["", "Derived (MI355X: 1024 SIMDs, 2.4 GHz; SQ_BUSY_CYCLES summed over the 32 "
+              "shader engines of 32 SIMDs):", ""]
+    if "SQ_VALU_MFMA_BUSY_CYCLES" in c:
+        mb = c["SQ_VALU_MFMA_BUSY_CYCLES"]
+        lines.append(f"* matrix cores busy: {100 * mb / (SIMDS * CLOCK_HZ * t):.1f}% of the "
+                     f"kernel's SIMD-cycles")
+        if "SQ_BUSY_CYCLES" in c:
+            lines.append(f"* matrix cores busy: {100 * mb / (c['SQ_BUSY_CYCLES'] * 32):.1f}% of "
+                         f"the cycles the shader engines were busy")
+    if "SQ_INSTS_MFMA" in c and "SQ_INSTS_VALU" in c:
+        lines.append(f"* VALU instructions (MFMA included) per MFMA: "
+                     f"{c['SQ_INSTS_VALU'] / c['SQ_INSTS_MFMA']:.2f}")
+    if "SQ_LDS_BANK_CONFLICT" in c and "SQ_LDS_IDX_ACTIVE" in c:
+        lines.append(f"* LDS bank-conflict cycles per LDS-active cycle: "
+                     f"{c['SQ_LDS_BANK_CONFLICT'] / c['SQ_LDS_IDX_ACTIVE']:.2f}")
+    if "SQ_LDS_IDX_ACTIVE" in c:
+        lines.append(f"* LDS active: {100 * c['SQ_LDS_IDX_ACTIVE'] / (256 * CLOCK_HZ * t):.1f}% "
+                     f"of the kernel's CU-cycles")
+    if "SQ_WAIT_INST_ANY" in c and "SQ_ACTIVE_INST_ANY" in c:
+        lines.append(f"* wave cycles waiting for a dependency per issuing cycle: "
+                     f"{c['SQ_WAIT_INST_ANY'] / c['SQ_ACTIVE_INST_ANY']:.2f}")
+    path = os.path.join(ROOT, "profiles", f"counters_attn_main_{workload}.md")
+    with open(path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(path)
 
 
 def summarize_trace(trace_dir, bench_log, workload):
@@ -293,6 +370,9 @@ def main():
         return
     if args.summarize_trace:
         summarize_trace(*args.summarize_trace, args.workload)
+        return
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters, args.workload)
         return
     if args.copy_only:
         copy_only()

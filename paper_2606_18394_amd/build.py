@@ -51,5 +51,25 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+EXAMPLE_SRC = os.path.join(ROOT, "tests", "native", "abi_example.c")
+EXAMPLE = os.path.join(ROOT, "tests", "native", "abi_example")
+
+
+def build_example(verbose: bool = False, out: str = EXAMPLE) -> str:
+    """Compile the plain-C program that drives the C ABI (a host-only build
+    against libtreeverify.so and the HIP runtime)."""
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    cmd = ["gcc", "-O2", "-std=c99", "-D__HIP_PLATFORM_AMD__", "-I" + os.path.join(ROOT, "include"),
+           "-I" + os.path.join(rocm, "include"), EXAMPLE_SRC, "-o", out, "-L" + HERE,
+           "-ltreeverify", "-L" + os.path.join(rocm, "lib"), "-lamdhip64", "-lm",
+           "-Wl,-rpath," + HERE + ":" + os.path.join(rocm, "lib")]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError("gcc failed:\n" + res.stdout + res.stderr)
+    return out
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))

@@ -302,3 +302,13 @@ def test_sampled_accept_host_errors():
     assert _samp(lib, ws=None) == -5
     assert _samp(lib, wsb=64) == -5
     assert _samp(lib, ws=FAKE + 8) == -7
+
+
+def test_plain_c_program_compiles_against_the_header(tmp_path):
+    """The header is plain C99 and the library links from C (the program
+    itself runs in the GPU suite)."""
+    from paper_2606_18394_amd import build
+    if not os.path.exists(build.LIB):
+        build.build()
+    exe = build.build_example(out=str(tmp_path / "abi_example"))
+    assert os.path.exists(exe)

@@ -278,21 +278,26 @@ __global__ __launch_bounds__(256) void accept_finish(AcceptArgs a) {
   const int tid = threadIdx.x;
   const int b = blockIdx.x;
   const int N = a.N;
+  // The split keys go out in batches of kFinishLoads per thread (one batch
+  // for every plan but the largest trees).  The first batch is requested
+  // before the nodes' parents and tokens, and at clamped indices (a repeat
+  // leaves the max unchanged), so all of them are in flight together.
+  constexpr int kFinishLoads = 8;
+  const size_t kbase = (size_t)b * N * a.nsplit;
+  const int nkeys = N * a.nsplit;
+  unsigned long long kv[kFinishLoads];
+#pragma unroll
+  for (int u = 0; u < kFinishLoads; ++u) kv[u] = a.part[kbase + min(256 * u + tid, nkeys - 1)];
   int pv[kMaxNodes / 256], dv[kMaxNodes / 256];
   load_nodes(a, b, pv, dv);
   unsigned long long* rowkey = reinterpret_cast<unsigned long long*>(lds + accept_lds_bytes(N));
   for (int i = tid; i < N; i += 256) rowkey[i] = 0ull;
   __syncthreads();
-  // loads go out in batches of kFinishLoads so their latencies overlap
-  constexpr int kFinishLoads = 8;
-  const size_t kbase = (size_t)b * N * a.nsplit;
-  const int nkeys = N * a.nsplit;
   for (int idx0 = 0; idx0 < nkeys; idx0 += 256 * kFinishLoads) {
-    unsigned long long kv[kFinishLoads];
+    if (idx0 > 0) {
 #pragma unroll
-    for (int u = 0; u < kFinishLoads; ++u) {
-      const int idx = idx0 + 256 * u + tid;
-      kv[u] = idx < nkeys ? a.part[kbase + idx] : 0ull;
+      for (int u = 0; u < kFinishLoads; ++u)
+        kv[u] = a.part[kbase + min(idx0 + 256 * u + tid, nkeys - 1)];
     }
 #pragma unroll
     for (int u = 0; u < kFinishLoads; ++u) {
@@ -321,16 +326,19 @@ __global__ __launch_bounds__(64) void accept_finish_wave(AcceptArgs a) {
   const bool node = i < N;
   const int p = node ? a.parent[(size_t)b * N + i] : 0;
   const int y = node ? a.draft[(size_t)b * N + i] : 0;
-  // this node's prediction: the max of its split keys, loaded together
+  // this node's prediction: the max of its split keys, all requested at
+  // once (indices past the last split repeat it, which leaves the max
+  // unchanged and keeps the loads free of branches)
   unsigned long long key = 0ull;
-  if (node) {
-    const unsigned long long* kp = a.part + ((size_t)b * N + i) * a.nsplit;
+  {
+    const unsigned long long* kp = a.part + ((size_t)b * N + (node ? i : 0)) * a.nsplit;
     constexpr int kLoads = kAcceptMaxSplit;
     unsigned long long kv[kLoads];
 #pragma unroll
-    for (int k = 0; k < kLoads; ++k) kv[k] = k < a.nsplit ? kp[k] : 0ull;
+    for (int k = 0; k < kLoads; ++k) kv[k] = kp[min(k, a.nsplit - 1)];
 #pragma unroll
     for (int k = 0; k < kLoads; ++k) key = umax64(key, kv[k]);
+    if (!node) key = 0ull;
   }
   const int tgt = key_index(key);
   if (node && a.tgt_out) a.tgt_out[(size_t)b * N + i] = tgt;

@@ -858,12 +858,16 @@ void attn_main(AttnArgs a) {
 }
 
 // Second kernel of the split-KV plans whose merge is too large for one
-// workgroup: out = sum_s e_s O_s / sum_s e_s l_s with e_s = 2^(m_s - max m).  Only chunks that hold tiles of this row
-// block were written.  One wave per 16x16 fragment; loads are issued in
-// groups of 8 so their latencies overlap.
+// workgroup: out = sum_s e_s O_s / sum_s e_s l_s with e_s = 2^(m_s - m*),
+// folded in online over batches of U chunks.  Only chunks that hold tiles
+// of this row block were written.  One wave per 16x16 fragment.  The
+// parents (for the tree check) and the first batch of partials are all
+// requested before any is used, so a merge of up to U chunks waits for one
+// round of memory latency.
 template <int D, int RB>
 __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
-  constexpr int NTG = RB / 16, DT = D / 16, U = 8;
+  constexpr int NTG = RB / 16, DT = D / 16, U = 16;
+  constexpr int kParPerThread = kMaxNodes / 256;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g4 = lane >> 4, l16 = lane & 15;
   const int F = blockIdx.x * 4 + wave;  // fragment id; all 4 of a block share (b,g,rb)
@@ -871,33 +875,22 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
   const int blk = F / per_blk, f = F % per_blk;
   const int rb = blk % a.nRB, bg = blk / a.nRB;
   const int b = bg / a.Hkv, g = bg % a.Hkv;
-  int bad = 0;
-  for (int i = threadIdx.x; i < a.N; i += 256) {
-    const int p = a.parent ? a.parent[(size_t)b * a.N + i] : i - 1;
-    bad |= (i == 0) ? (p != -1) : (p < 0 || p >= i);
+  int pv[kParPerThread];
+#pragma unroll
+  for (int k = 0; k < kParPerThread; ++k) {
+    const int i = threadIdx.x + 256 * k;
+    pv[k] = i >= a.N ? 0 : (a.parent ? a.parent[(size_t)b * a.N + i] : i - 1);
   }
-  bad = __syncthreads_or(bad);
   const int dt = f / NTG, ntg = f % NTG;
   const int row = ntg * 16 + l16, r = rb * RB + row;
-  if (r >= a.M) return;
   // chunks of this row block that hold tiles (the same count the main
   // kernel derives from kv_len and the block's last node)
   const int i_hi = (min(rb * RB + RB, a.M) - 1) / a.G;
   const int T = segment(a, b, i_hi).T;
   const int nval = min(a.S, (T + a.chunk - 1) / a.chunk);
   const size_t base = (size_t)(bg * a.nRB + rb) * a.S;  // first chunk partial
-  float mstar = -INFINITY;
-  for (int s0 = 0; s0 < nval; s0 += U) {
-    float2 ml[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-      if (s0 + u < nval) ml[u] = a.ws_ml[(base + s0 + u) * RB + row];
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-      if (s0 + u < nval) mstar = fmaxf(mstar, ml[u].x);
-  }
+  float m = -INFINITY, l = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  float l = 0.f;
   for (int s0 = 0; s0 < nval; s0 += U) {
     float2 ml[U];
     f32x4 ov[U];
@@ -907,14 +900,32 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
         ml[u] = a.ws_ml[(base + s0 + u) * RB + row];
         ov[u] = a.ws_o[((base + s0 + u) * DT * NTG + dt * NTG + ntg) * 64 + lane];
       }
+    float mb = m;
 #pragma unroll
     for (int u = 0; u < U; ++u)
-      if (s0 + u < nval && ml[u].x != -INFINITY) {
-        const float e = __builtin_amdgcn_exp2f(ml[u].x - mstar);
-        l += e * ml[u].y;
-        acc += e * ov[u];
-      }
+      if (s0 + u < nval) mb = fmaxf(mb, ml[u].x);
+    if (mb != -INFINITY) {  // else every chunk so far saw no key: nothing to add
+      const float ea = __builtin_amdgcn_exp2f(m - mb);  // 0 while m = -inf
+      l *= ea;
+      acc *= ea;
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (s0 + u < nval && ml[u].x != -INFINITY) {
+          const float e = __builtin_amdgcn_exp2f(ml[u].x - mb);
+          l += e * ml[u].y;
+          acc += e * ov[u];
+        }
+      m = mb;
+    }
   }
+  int bad = 0;
+#pragma unroll
+  for (int k = 0; k < kParPerThread; ++k) {
+    const int i = threadIdx.x + 256 * k;
+    if (i < a.N) bad |= (i == 0) ? (pv[k] != -1) : (pv[k] < 0 || pv[k] >= i);
+  }
+  bad = __syncthreads_or(bad);
+  if (r >= a.M) return;
   const int node = r / a.G, h = g * a.G + r % a.G;
   store_out4(a.out + ((size_t)(b * a.N + node) * a.Hq + h) * D + 16 * dt + 4 * g4, acc, 1.f / l,
              bad != 0);

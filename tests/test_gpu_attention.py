@@ -63,6 +63,13 @@ FUZZ = [
     (4, 40, 24, 8, 128, 300, [0, 300, 17, 255], "random"),
     (1, 2048, 2, 1, 128, 40, [40], "random"),
     (1, 300, 64, 8, 128, 2000, [1999], "random"),
+    # matrix-bound shapes of several row blocks per KV head: a cache tail and
+    # tree tiles after many full tiles, ragged sequences whose chunks hold 0,
+    # a few or many full tiles, head dim 64
+    (1, 200, 64, 8, 128, 5000, [4987], "random"),
+    (3, 128, 32, 4, 128, 6000, [5999, 1234, 100], "random"),
+    (1, 256, 64, 8, 64, 6000, [6000], "random"),
+    (2, 128, 32, 4, 64, 6000, [6000, 37], "chain"),
 ]
 
 

@@ -27,6 +27,7 @@ PAGED = [
     (1, 64, 32, 8, 128, 128, 256, [32768], 3, False),
     (2, 17, 8, 2, 64, 32, 0, [0, 0], 0, True),
     (8, 64, 32, 4, 128, 32, 64, [2048, 1999, 33, 1024, 31, 0, 2000, 700], 11, False),
+    (2, 128, 32, 4, 128, 64, 94, [5999, 1234], 3, False),
 ]
 
 
@@ -205,6 +206,7 @@ TAIL = [
     (1, 300, 16, 2, 128, [517], 3, True),
     (8, 64, 32, 4, 128, [2048, 1999, 33, 1024, 31, 0, 2000, 700], 0, False),
     (1, 64, 32, 8, 128, [32700], 4, False),
+    (2, 128, 32, 4, 128, [5900, 1234], 3, False),
 ]
 
 

@@ -230,6 +230,13 @@ def summarize_trace(trace_dir, bench_log, workload):
         raise SystemExit(f"expected one kernel_stats.csv under {trace_dir}, got {files}")
     with open(files[0]) as fh:
         rows = list(csv.DictReader(fh))
+    # per-dispatch durations (median, p10, p90) from the trace itself
+    durs = {}
+    for f in glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True):
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                durs.setdefault(r["Kernel_Name"], []).append(
+                    (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3)
     line = None
     with open(bench_log) as fh:
         for ln in fh:
@@ -248,11 +255,15 @@ def summarize_trace(trace_dir, bench_log, workload):
            "Calls include warm-up, graph capture and every timed graph (step, attention, "
            "acceptance, draft top-W, tree build, paged attention, tree-tail attention, path "
            "commit).", "",
-           "| kernel | calls | avg us | min us | max us | % of GPU time |",
-           "|---|---|---|---|---|---|"]
+           "| kernel | calls | avg us | median us | p10 us | p90 us | min us | max us | "
+           "% of GPU time |",
+           "|---|---|---|---|---|---|---|---|---|"]
     for r in rows:
         name = r["Name"] if len(r["Name"]) <= 72 else r["Name"][:69] + "..."
+        dv = np.array(durs.get(r["Name"], [float("nan")]))
         out.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                   f"{np.median(dv):.2f} | {np.percentile(dv, 10):.2f} | "
+                   f"{np.percentile(dv, 90):.2f} | "
                    f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
                    f"{float(r['Percentage']):.2f} |")
     out += ["", "Same command without the profiler (HIP events around graph replays on the "
@@ -267,7 +278,11 @@ def summarize_trace(trace_dir, bench_log, workload):
             f"    non-greedy acceptance (T = 1) {d['sampled_accept']['us']:.2f} us",
             f"    training-mask attention ({d['training_mask_attention']['anchors']} blocks of "
             f"{d['training_mask_attention']['block']} over {d['training_mask_attention']['context']}"
-            f" context rows) {d['training_mask_attention']['us']:.1f} us", ""]
+            f" context rows) {d['training_mask_attention']['us']:.1f} us"]
+    if "copy_floor" in d:
+        out.append(f"    device copy of the attention's {d['copy_floor']['bytes_moved'] / 1e6:.1f} MB "
+                   f"(the streaming floor) {d['copy_floor']['us']:.2f} us")
+    out.append("")
     path = os.path.join(ROOT, "profiles", f"kernel_trace_{workload}.md")
     with open(path, "w") as fh:
         fh.write("\n".join(out))

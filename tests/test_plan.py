@@ -39,3 +39,20 @@ def test_plans(tmp_path):
     res = subprocess.run([str(exe)], input=data, capture_output=True, text=True)
     fails = [l for l in res.stdout.splitlines() if l.startswith("FAIL")]
     assert res.returncode == 0 and not fails, "\n".join(fails[:20]) + res.stdout[-300:]
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="needs g++")
+def test_plans_under_host_sanitizers(tmp_path):
+    """The same checks with AddressSanitizer and UndefinedBehaviorSanitizer on
+    the host planner (integer overflow in sizes, out-of-range indexing)."""
+    exe = tmp_path / "plan_check_san"
+    build = subprocess.run(["g++", "-O1", "-g", "-std=c++17", "-fsanitize=address,undefined",
+                            "-fno-sanitize-recover=undefined", "-I", CSRC,
+                            os.path.join(ROOT, "tests", "native", "plan_check.cpp"), "-o", str(exe)],
+                           capture_output=True, text=True)
+    if build.returncode != 0:
+        pytest.skip("host sanitizer runtime not available: " + build.stderr[-200:])
+    data = "\n".join(" ".join(map(str, s)) for s in shapes()) + "\n"
+    res = subprocess.run([str(exe)], input=data, capture_output=True, text=True)
+    fails = [l for l in res.stdout.splitlines() if l.startswith("FAIL")]
+    assert res.returncode == 0 and not fails, "\n".join(fails[:20]) + res.stderr[-1000:]

@@ -60,7 +60,8 @@ struct AttnArgs {
   unsigned int* arrived;  // per row block: chunks that have stored partials
   int* tree_bad;          // per row block: invalid parent array seen
   int B, N, Hq, Hkv, Lmax, G, M, nRB, S, chunk, nwork;
-  int fused;  // split-KV merge inside the main kernel (else a second kernel)
+  int fused;   // split-KV merge inside the main kernel (else a second kernel)
+  int spread;  // work order of several sequences (tv_plan.h, work_item)
   float c;  // scale * log2(e): scores live in base-2 exponent units
   const int32_t* block_table;  // paged cache: [B, max_blocks], else NULL
   int block_shift, max_blocks, num_blocks;
@@ -553,16 +554,9 @@ void attn_main(AttnArgs a) {
   static_assert(NS >= 1, "ring does not fit");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
-  const int per = gridDim.x / kXcds;
-  int w = (blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
-  if (w >= a.nwork) return;
-  const int s = w % a.S;
-  w /= a.S;
-  const int rb = w % a.nRB;
-  w /= a.nRB;
-  const int g = w % a.Hkv;
-  const int b = w / a.Hkv;
-  if (b >= a.B) return;  // never taken for a consistent plan
+  WorkItem it{};
+  if (!work_item(gridDim.x, a.nwork, a.S, a.nRB, a.spread, a.B, a.Hkv, blockIdx.x, it)) return;
+  const int s = it.s, rb = it.rb, g = it.g, b = it.b;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wr = wave % WR, wk = wave / WR;
@@ -1002,6 +996,7 @@ hipError_t launch_attention(const void* q, const void* kc, const void* vc, const
   a.chunk = p.chunk;
   a.nwork = p.nwork;
   a.fused = p.fused;
+  a.spread = p.spread;
   a.c = scale * 1.4426950408889634f;
   return D == 128 ? launch_attn_d<128>(a, p, st) : launch_attn_d<64>(a, p, st);
 }

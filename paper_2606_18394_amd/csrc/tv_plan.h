@@ -50,6 +50,7 @@ struct AttnPlan {
   int G, M, RB, nRB, S, chunk;
   int nwork, grid;             // work items, launched workgroups (x8 padded)
   int fused;                   // S > 1: merge in the main kernel's last chunk
+  int spread;                  // work order of several sequences (below)
   size_t ws_o_bytes, ws_ml_bytes, ws_sync_bytes, ws_bytes;
   size_t lds_bytes;            // dynamic LDS of the main kernel
 };
@@ -111,7 +112,45 @@ inline AttnPlan attn_plan_arr(int B, int N, int Hq, int Hkv, int D, int Lmax, in
   // go to a second kernel that spreads them over the whole GPU.
   p.fused = p.S > 1 && (size_t)p.S * p.RB * D * 4 <= (size_t)kFusedMergeBytes * p.threads;
   p.lds_bytes = p.NS > 0 ? attn_lds_bytes(D, ar.WR, ar.WK, p.NS, p.G, N) : kMaxLds + 1;
+  // Workgroups go to the XCDs round-robin, and the row blocks of one
+  // (sequence, KV head, chunk) read the same keys, so they stay on one XCD
+  // (its L2).  With one sequence, XCD x takes a contiguous run of work
+  // items.  With several sequences of different lengths that would give
+  // each XCD whole sequences and very different work, so each XCD instead
+  // takes one KV head and one of L = 8/Hkv lanes of chunks: chunk s of
+  // sequence b goes to lane (b + s) % L.  Every XCD then sees every
+  // sequence.  This needs Hkv to divide 8 and L to divide S.
+  p.spread = B > 1 && kXcds % Hkv == 0 && p.S % (kXcds / Hkv) == 0;
   return p;
+}
+
+// The work item (sequence b, KV head g, row block rb, chunk s) of launched
+// workgroup `bid`; false for padding workgroups past the work.  constexpr,
+// so the kernels and the host checks decode with this same function.
+struct WorkItem {
+  int b, g, rb, s;
+};
+constexpr bool work_item(int grid, int nwork, int S, int nRB, int spread, int B, int Hkv, int bid,
+                         WorkItem& it) {
+  const int x = bid % kXcds, j = bid / kXcds;
+  if (spread) {
+    const int L = kXcds / Hkv, per_b = S / L;
+    it.g = x % Hkv;
+    it.rb = j % nRB;
+    const int uu = j / nRB;
+    it.b = uu / per_b;
+    it.s = ((x / Hkv - it.b) % L + L) % L + L * (uu % per_b);
+    return it.b < B;
+  }
+  int w = x * (grid / kXcds) + j;
+  if (w >= nwork) return false;
+  it.s = w % S;
+  w /= S;
+  it.rb = w % nRB;
+  w /= nRB;
+  it.g = w % Hkv;
+  it.b = w / Hkv;
+  return it.b < B;
 }
 
 inline bool attn_plan_fits(const AttnPlan& p) {

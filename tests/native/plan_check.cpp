@@ -19,15 +19,21 @@ int main() {
     bool ok = p.grid % tv::kXcds == 0 && p.nwork == B * Hkv * p.nRB * p.S && p.grid >= p.nwork;
     ok = ok && (long long)p.S * p.chunk >= tiles && (long long)(p.S - 1) * p.chunk < tiles;
     ok = ok && p.WR >= 1 && p.RB == tv::kRowsPerWave * p.WR && tv::attn_plan_fits(p);
-    const int per = p.grid / tv::kXcds;
+    // the spread order needs every workgroup to carry a work item
+    if (p.spread && (p.grid != p.nwork || tv::kXcds % Hkv != 0 || p.S % (tv::kXcds / Hkv) != 0))
+      ok = false;
+    int decoded = 0;
     for (int bid = 0; bid < p.grid && ok; ++bid) {
-      int w = (bid % tv::kXcds) * per + bid / tv::kXcds;
-      if (w < 0 || w >= p.grid) ok = false;
-      if (w >= p.nwork) continue;
-      const int s = w % p.S, rb = (w / p.S) % p.nRB, g = (w / p.S / p.nRB) % Hkv;
-      const int b = w / p.S / p.nRB / Hkv;
-      if (b >= B || rb * p.RB >= p.M) ok = false;
-      seen[(size_t)w]++;
+      tv::WorkItem it{};
+      if (!tv::work_item(p.grid, p.nwork, p.S, p.nRB, p.spread, B, Hkv, bid, it)) continue;
+      ++decoded;
+      const int s = it.s, rb = it.rb, g = it.g, b = it.b;
+      if (b < 0 || b >= B || g < 0 || g >= Hkv || rb < 0 || rb >= p.nRB || s < 0 || s >= p.S ||
+          rb * p.RB >= p.M) {
+        ok = false;
+        break;
+      }
+      seen[(size_t)(s + p.S * (rb + p.nRB * (g + Hkv * b)))]++;
       if (p.S > 1) {
         const int DT = D / 16, NT = p.RB / 16;
         const size_t fr = ((size_t)((b * Hkv + g) * p.nRB + rb) * p.S + s) * DT * NT;
@@ -37,6 +43,7 @@ int main() {
       }
     }
     for (int v : seen) ok = ok && v == 1;
+    ok = ok && decoded == p.nwork;
     if (p.S > 1) {
       // arrival counter + tree flag per row block; the workspace sections add up
       const size_t groups = (size_t)B * Hkv * p.nRB;
@@ -87,9 +94,9 @@ int main() {
         if (tp.nsplit < 1 || tp.nsplit > tv::kAcceptMaxSplit) ok = false;
         if (tp.ws_bytes > tv::topw_ws_bytes(B, Nd)) ok = false;
       }
-    std::printf("%s B=%d N=%d Hq=%d Hkv=%d D=%d L=%d V=%d S=%d RB=%d nRB=%d grid=%d lds=%zu ws=%zu\n",
+    std::printf("%s B=%d N=%d Hq=%d Hkv=%d D=%d L=%d V=%d S=%d RB=%d nRB=%d grid=%d spread=%d lds=%zu ws=%zu\n",
                 ok ? "OK" : "FAIL", B, N, Hq, Hkv, D, Lmax, V, p.S, p.RB, p.nRB, p.grid,
-                p.lds_bytes, p.ws_bytes);
+                p.spread, p.lds_bytes, p.ws_bytes);
     bad += !ok;
   }
   std::printf("%d cases, %d failed\n", cases, bad);

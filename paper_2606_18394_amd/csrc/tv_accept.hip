@@ -5,8 +5,8 @@
 // prediction at its parent and the parent is accepted; the result is the
 // deepest accepted root-to-node path (Sec. 2.4 greedy rule; App. E).
 //
-// Scan: one workgroup per (node row, vocabulary split).  256 threads stream
-// the slice with 16-byte loads, kScanLoadsPerThread of them in flight per
+// Scan: one workgroup per (node row, vocabulary split).  512 threads stream
+// the slice with 16-byte loads, kAcceptScanLoads of them in flight per
 // thread, and keep a running first maximum; the workgroup reduces it with
 // wave64 shuffles on the 64-bit key
 //     key = order-preserving(value) << 32 | (0xFFFFFFFF - index)
@@ -100,7 +100,7 @@ __device__ __forceinline__ void see_chunk(Best& best, const uint4& w, unsigned i
 template <bool F32, bool VEC>
 __device__ __forceinline__ unsigned long long scan_slice(const AcceptArgs& a, int row, int split) {
   constexpr int E = VEC ? (F32 ? 4 : 8) : 1;  // elements per chunk
-  constexpr int L = kScanLoadsPerThread;
+  constexpr int L = kAcceptScanLoads;
   const int tid = threadIdx.x;
   const long long nchunks = ((long long)a.V + E - 1) / E;
   const long long c0 = (long long)split * a.cps;
@@ -111,21 +111,21 @@ __device__ __forceinline__ unsigned long long scan_slice(const AcceptArgs& a, in
     const uint4* base = reinterpret_cast<const uint4*>(
         (const char*)a.logits + (size_t)row * a.V * (F32 ? 4 : 2));
     // rounds of L loads per thread, all issued before any is used
-    for (long long c = c0 + tid; c < c1; c += (long long)L * kScanThreads) {
+    for (long long c = c0 + tid; c < c1; c += (long long)L * kAcceptScanThreads) {
       uint4 w[L];
 #pragma unroll
       for (int u = 0; u < L; ++u) {
-        const long long cu = c + (long long)u * kScanThreads;
+        const long long cu = c + (long long)u * kAcceptScanThreads;
         if (cu < c1) w[u] = base[cu];
       }
 #pragma unroll
       for (int u = 0; u < L; ++u) {
-        const long long cu = c + (long long)u * kScanThreads;
+        const long long cu = c + (long long)u * kAcceptScanThreads;
         if (cu < c1) see_chunk<F32>(best, w[u], (unsigned int)(cu * E));
       }
     }
   } else {
-    for (long long c = c0 + tid; c < c1; c += kScanThreads) {
+    for (long long c = c0 + tid; c < c1; c += kAcceptScanThreads) {
       float x;
       if (F32) {
         x = reinterpret_cast<const float*>(a.logits)[(size_t)row * a.V + c];
@@ -138,14 +138,14 @@ __device__ __forceinline__ unsigned long long scan_slice(const AcceptArgs& a, in
     }
   }
 
-  __shared__ unsigned long long red[kScanThreads / 64];
+  __shared__ unsigned long long red[kAcceptScanThreads / 64];
   unsigned long long key = best.any ? make_key(best.v, best.i) : 0ull;
   key = wave_max_u64(key);
   if ((tid & 63) == 0) red[tid >> 6] = key;
   __syncthreads();
   key = red[0];
 #pragma unroll
-  for (int k = 1; k < kScanThreads / 64; ++k) key = umax64(key, red[k]);
+  for (int k = 1; k < kAcceptScanThreads / 64; ++k) key = umax64(key, red[k]);
   return key;
 }
 
@@ -264,7 +264,7 @@ __device__ __forceinline__ void accept_sequence(const AcceptArgs& a, int b, cons
 
 // First kernel: the key of every (row, split).
 template <bool F32, bool VEC>
-__global__ __launch_bounds__(kScanThreads) void accept_scan(AcceptArgs a) {
+__global__ __launch_bounds__(kAcceptScanThreads) void accept_scan(AcceptArgs a) {
   const int row = blockIdx.x / a.nsplit;
   const int split = blockIdx.x % a.nsplit;
   const unsigned long long key = scan_slice<F32, VEC>(a, row, split);
@@ -403,7 +403,7 @@ hipError_t launch_accept(const void* logits, int f32, const int32_t* draft, cons
   a.Dmax = Dmax;
   a.nsplit = p.nsplit;
   a.cps = p.chunks_per_split;
-  const dim3 g(p.grid), t(kScanThreads);
+  const dim3 g(p.grid), t(kAcceptScanThreads);
   if (f32) {
     if (vec) hipLaunchKernelGGL((accept_scan<true, true>), g, t, 0, st, a);
     else hipLaunchKernelGGL((accept_scan<true, false>), g, t, 0, st, a);

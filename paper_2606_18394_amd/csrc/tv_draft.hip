@@ -386,14 +386,20 @@ struct BuildArgs {
   int Nd, W, budget;
 };
 
+// Budgets of 65 .. 64 S nodes.  Node i belongs to lane i % 64, slot i / 64,
+// and the score, depth and open flag of a lane's S nodes stay in its
+// registers, so after a pop the owner finds its next best open node with an
+// unrolled register scan (no memory access).  Each lane also caches its
+// best open node, and a pop is one wave argmax of those caches.  Tokens and
+// parents are only written during the loop, so they go to LDS and are read
+// once at the end.
+template <int S>
 __global__ __launch_bounds__(64) void build_tree(BuildArgs a) {
+  static_assert(S >= 1 && S <= 32, "open flags are one 32-bit mask");
   __shared__ float cand_lp[kMaxDraftDepth * kTopwMax];
   __shared__ int cand_tok[kMaxDraftDepth * kTopwMax];
-  __shared__ float sc[kMaxNodes];
-  __shared__ int tk[kMaxNodes];
-  __shared__ short par[kMaxNodes];
-  __shared__ unsigned char dep[kMaxNodes];
-  __shared__ unsigned char open[kMaxNodes];
+  __shared__ int tk[64 * S];
+  __shared__ short par[64 * S];
   const int b = blockIdx.x, lane = threadIdx.x;
   const int Nd = a.Nd, W = a.W, budget = a.budget;
   const size_t cbase = (size_t)b * Nd * W;
@@ -402,21 +408,25 @@ __global__ __launch_bounds__(64) void build_tree(BuildArgs a) {
     cand_tok[k] = a.tok[cbase + k];
   }
   if (lane == 0) {
-    sc[0] = 0.f;
     tk[0] = a.root_tok ? a.root_tok[b] : -1;
     par[0] = -1;
-    dep[0] = 0;
-    open[0] = 1;  // Nd >= 1
   }
   __syncthreads();
-  // The loop runs in one wave: LDS accesses of a wave execute in order, so
-  // a lane reads what another lane wrote in an earlier pop; the outputs go
-  // to global memory once at the end.
-  float bs = lane == 0 ? 0.f : -INFINITY;  // this lane's best open node,
-  int bi = lane == 0 ? 0 : 0x7FFFFFFF;     // its index and depth
-  int bd = 0;                              // (lane 0 owns the root)
+  float sc[S];
+  int dep[S];
+#pragma unroll
+  for (int j = 0; j < S; ++j) {
+    sc[j] = 0.f;
+    dep[j] = 0;
+  }
+  unsigned int open = lane == 0 ? 1u : 0u;  // bit j: node lane + 64 j is open (root: Nd >= 1)
+  float bs = lane == 0 ? 0.f : -INFINITY;   // this lane's best open node,
+  int bi = lane == 0 ? 0 : 0x7FFFFFFF;      // its index and depth
+  int bd = 0;
   int n = 1;
-  // each pop of an open node adds at least one node, so budget - 1 pops end it
+  // The loop runs in one wave: LDS accesses of a wave execute in order, and
+  // tokens and parents are read only after it.  Each pop of an open node
+  // adds at least one node, so budget - 1 pops end it.
   for (int it = 0; it < budget && n < budget; ++it) {
     float gs = bs;
     int gi = bi, gd = bd;
@@ -425,27 +435,35 @@ __global__ __launch_bounds__(64) void build_tree(BuildArgs a) {
     const int v = gi;
     const int d = gd;
     if (lane == (v & 63)) {  // the owner closes v and finds its next best
-      open[v] = 0;
+      open &= ~(1u << (v >> 6));
       bs = -INFINITY;
       bi = 0x7FFFFFFF;
-      for (int i = lane; i < n; i += 64)
-        if (open[i] && better(sc[i], i, bs, bi)) {
-          bs = sc[i];
+#pragma unroll
+      for (int j = 0; j < S; ++j) {
+        const int i = lane + 64 * j;
+        if (((open >> j) & 1u) && better(sc[j], i, bs, bi)) {
+          bs = sc[j];
           bi = i;
-          bd = dep[i];
+          bd = dep[j];
         }
+      }
     }
     const int nk = min(W, budget - n);
     const int k = (lane - (n & 63)) & 63;  // this lane's child, if k < nk
     if (k < nk) {
       const int c = n + k;
+      const int jc = c >> 6;
       const float s = gs + cand_lp[d * W + k];
       const bool op = d + 1 < Nd;
-      sc[c] = s;
+#pragma unroll
+      for (int j = 0; j < S; ++j)
+        if (j == jc) {
+          sc[j] = s;
+          dep[j] = d + 1;
+        }
+      if (op) open |= 1u << jc;
       tk[c] = cand_tok[d * W + k];
       par[c] = (short)v;
-      dep[c] = (unsigned char)(d + 1);
-      open[c] = op;
       if (op && better(s, c, bs, bi)) {
         bs = s;
         bi = c;
@@ -457,12 +475,16 @@ __global__ __launch_bounds__(64) void build_tree(BuildArgs a) {
   }
   __syncthreads();
   const size_t obase = (size_t)b * budget;
-  for (int i = lane; i < budget; i += 64) {
-    const bool used = i < n;
-    a.parent[obase + i] = used ? (int)par[i] : -1;
-    a.token[obase + i] = used ? tk[i] : -1;
-    a.depth[obase + i] = used ? (int)dep[i] : -1;
-    if (a.score) a.score[obase + i] = used ? sc[i] : -INFINITY;
+#pragma unroll
+  for (int j = 0; j < S; ++j) {
+    const int i = lane + 64 * j;
+    if (i < budget) {
+      const bool used = i < n;
+      a.parent[obase + i] = used ? (int)par[i] : -1;
+      a.token[obase + i] = used ? tk[i] : -1;
+      a.depth[obase + i] = used ? dep[j] : -1;
+      if (a.score) a.score[obase + i] = used ? sc[j] : -INFINITY;
+    }
   }
   if (lane == 0) a.n_nodes[b] = n;
 }
@@ -534,8 +556,16 @@ hipError_t launch_build_tree(const int32_t* tok, const float* logp, const int32_
   a.budget = budget;
   if (budget <= 64)
     hipLaunchKernelGGL(build_tree_wave, dim3(B), dim3(64), 0, st, a);
+  else if (budget <= 128)  // slots per lane: the fewest that hold the budget
+    hipLaunchKernelGGL(build_tree<2>, dim3(B), dim3(64), 0, st, a);
+  else if (budget <= 256)
+    hipLaunchKernelGGL(build_tree<4>, dim3(B), dim3(64), 0, st, a);
+  else if (budget <= 512)
+    hipLaunchKernelGGL(build_tree<8>, dim3(B), dim3(64), 0, st, a);
+  else if (budget <= 1024)
+    hipLaunchKernelGGL(build_tree<16>, dim3(B), dim3(64), 0, st, a);
   else
-    hipLaunchKernelGGL(build_tree, dim3(B), dim3(64), 0, st, a);
+    hipLaunchKernelGGL(build_tree<kMaxNodes / 64>, dim3(B), dim3(64), 0, st, a);
   return hipGetLastError();
 }
 

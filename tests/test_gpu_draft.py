@@ -110,6 +110,12 @@ BUILD_CASES = [
     (2, 12, 16, 2048, "normal"),   # largest budget
     (5, 4, 3, 1, "normal"),        # root only
     (1, 64, 2, 1000, "normal"),    # deepest draft
+    (3, 6, 4, 65, "normal"),       # smallest budget past one node per lane
+    (2, 8, 8, 513, "ties"),        # budgets just past 128, 256, 512 and 1024 nodes
+    (1, 10, 6, 129, "ties"),       # (the builder keeps 2, 4, 8, 16 or 32 nodes per lane)
+    (2, 9, 5, 257, "normal"),
+    (1, 12, 9, 1025, "normal"),
+    (2, 7, 3, 128, "ties"),
     # budgets of at most 64 nodes (one node per lane)
     (4, 5, 4, 60, "ties"),
     (3, 2, 3, 64, "normal"),       # the full tree (13 nodes) ends before the budget

@@ -225,7 +225,7 @@ __global__ __launch_bounds__(kScanThreads) void lse_scan(SampleArgs a, int vec) 
 
 // ------------------------------------------------------------ sample_accept
 
-constexpr int kSampleThreads = 256;
+constexpr int kSampleThreads = 512;
 constexpr int kNodesPerThread = kMaxNodes / kSampleThreads;
 
 template <bool F32T, bool F32D>

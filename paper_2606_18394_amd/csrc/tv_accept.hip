@@ -149,6 +149,9 @@ __device__ __forceinline__ unsigned long long scan_slice(const AcceptArgs& a, in
   return key;
 }
 
+// Threads of the one-workgroup acceptance of trees over 64 nodes.
+constexpr int kFinishThreads = 512;
+
 // Per-node LDS arrays of one sequence's acceptance (accept_lds_bytes).
 struct SeqLds {
   int* tgt;
@@ -169,28 +172,28 @@ __device__ __forceinline__ SeqLds seq_lds(unsigned char* base, int N) {
   return l;
 }
 
-__device__ __forceinline__ void load_nodes(const AcceptArgs& a, int b, int (&pv)[kMaxNodes / 256],
-                                           int (&dv)[kMaxNodes / 256]) {
+__device__ __forceinline__ void load_nodes(const AcceptArgs& a, int b, int (&pv)[kMaxNodes / kFinishThreads],
+                                           int (&dv)[kMaxNodes / kFinishThreads]) {
 #pragma unroll
-  for (int k = 0; k < kMaxNodes / 256; ++k) {
-    const int i = threadIdx.x + 256 * k;
+  for (int k = 0; k < kMaxNodes / kFinishThreads; ++k) {
+    const int i = threadIdx.x + kFinishThreads * k;
     pv[k] = i < a.N ? a.parent[(size_t)b * a.N + i] : 0;
     dv[k] = i < a.N ? a.draft[(size_t)b * a.N + i] : 0;
   }
 }
 
 // Acceptance of sequence b once l.tgt holds every node's prediction; pv and
-// dv hold parent and draft token of nodes tid + 256 k.  All 256 threads.
+// dv hold parent and draft token of nodes tid + 256 k.  All kFinishThreads threads.
 __device__ __forceinline__ void accept_sequence(const AcceptArgs& a, int b, const SeqLds& l,
-                                                const int (&pv)[kMaxNodes / 256],
-                                                const int (&dv)[kMaxNodes / 256]) {
+                                                const int (&pv)[kMaxNodes / kFinishThreads],
+                                                const int (&dv)[kMaxNodes / kFinishThreads]) {
   __shared__ unsigned int best_key;
   const int tid = threadIdx.x;
   const int N = a.N;
   int bad = 0;
 #pragma unroll
-  for (int k = 0; k < kMaxNodes / 256; ++k) {
-    const int i = tid + 256 * k;
+  for (int k = 0; k < kMaxNodes / kFinishThreads; ++k) {
+    const int i = tid + kFinishThreads * k;
     if (i >= N) break;
     const int p = pv[k];
     const int badi = (i == 0) ? (p != -1) : (p < 0 || p >= i);
@@ -201,8 +204,8 @@ __device__ __forceinline__ void accept_sequence(const AcceptArgs& a, int b, cons
   bad = __syncthreads_or(bad);
   if (!bad) {
 #pragma unroll
-    for (int k = 0; k < kMaxNodes / 256; ++k) {
-      const int i = tid + 256 * k;
+    for (int k = 0; k < kMaxNodes / kFinishThreads; ++k) {
+      const int i = tid + kFinishThreads * k;
       if (i >= N) break;
       // the root (par = -1) jumps to itself
       const int p = i == 0 ? 0 : l.par[i];
@@ -224,7 +227,7 @@ __device__ __forceinline__ void accept_sequence(const AcceptArgs& a, int b, cons
       short* dn = cur ? l.dep0 : l.dep1;
       unsigned char* on = cur ? l.ok0 : l.ok1;
       more = 0;
-      for (int i = tid; i < N; i += 256) {
+      for (int i = tid; i < N; i += kFinishThreads) {
         const int j = jc[i];
         on[i] = oc[i] & oc[j];
         dn[i] = dc[i] + dc[j];
@@ -236,7 +239,7 @@ __device__ __forceinline__ void accept_sequence(const AcceptArgs& a, int b, cons
     const short* dc = cur ? l.dep1 : l.dep0;
     const unsigned char* oc = cur ? l.ok1 : l.ok0;
     unsigned int mk = 0u;
-    for (int i = tid; i < N; i += 256)
+    for (int i = tid; i < N; i += kFinishThreads)
       if (oc[i]) {
         const unsigned int k = ((unsigned int)dc[i] << 16) | (0xFFFFu - (unsigned int)i);
         mk = mk > k ? mk : k;
@@ -248,7 +251,7 @@ __device__ __forceinline__ void accept_sequence(const AcceptArgs& a, int b, cons
   const int depth = (int)(bk >> 16);
   const int len = bad || depth + 1 > a.Dmax ? -1 : depth + 1;
   int32_t* pth = a.path + (size_t)b * a.Dmax;
-  for (int k = tid; k < a.Dmax; k += 256)
+  for (int k = tid; k < a.Dmax; k += kFinishThreads)
     if (k >= len) pth[k] = -1;  // len == -1 clears the whole row
   if (tid == 0) {
     if (len > 0) {
@@ -273,7 +276,7 @@ __global__ __launch_bounds__(kAcceptScanThreads) void accept_scan(AcceptArgs a) 
 
 // Second kernel: one workgroup per sequence merges the split keys of its
 // rows (LDS max) and runs the acceptance.
-__global__ __launch_bounds__(256) void accept_finish(AcceptArgs a) {
+__global__ __launch_bounds__(kFinishThreads) void accept_finish(AcceptArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   const int tid = threadIdx.x;
   const int b = blockIdx.x;
@@ -287,27 +290,27 @@ __global__ __launch_bounds__(256) void accept_finish(AcceptArgs a) {
   const int nkeys = N * a.nsplit;
   unsigned long long kv[kFinishLoads];
 #pragma unroll
-  for (int u = 0; u < kFinishLoads; ++u) kv[u] = a.part[kbase + min(256 * u + tid, nkeys - 1)];
-  int pv[kMaxNodes / 256], dv[kMaxNodes / 256];
+  for (int u = 0; u < kFinishLoads; ++u) kv[u] = a.part[kbase + min(kFinishThreads * u + tid, nkeys - 1)];
+  int pv[kMaxNodes / kFinishThreads], dv[kMaxNodes / kFinishThreads];
   load_nodes(a, b, pv, dv);
   unsigned long long* rowkey = reinterpret_cast<unsigned long long*>(lds + accept_lds_bytes(N));
-  for (int i = tid; i < N; i += 256) rowkey[i] = 0ull;
+  for (int i = tid; i < N; i += kFinishThreads) rowkey[i] = 0ull;
   __syncthreads();
-  for (int idx0 = 0; idx0 < nkeys; idx0 += 256 * kFinishLoads) {
+  for (int idx0 = 0; idx0 < nkeys; idx0 += kFinishThreads * kFinishLoads) {
     if (idx0 > 0) {
 #pragma unroll
       for (int u = 0; u < kFinishLoads; ++u)
-        kv[u] = a.part[kbase + min(idx0 + 256 * u + tid, nkeys - 1)];
+        kv[u] = a.part[kbase + min(idx0 + kFinishThreads * u + tid, nkeys - 1)];
     }
 #pragma unroll
     for (int u = 0; u < kFinishLoads; ++u) {
-      const int idx = idx0 + 256 * u + tid;
+      const int idx = idx0 + kFinishThreads * u + tid;
       if (idx < nkeys) atomicMax(&rowkey[idx / a.nsplit], kv[u]);
     }
   }
   __syncthreads();
   const SeqLds l = seq_lds(lds, N);
-  for (int i = tid; i < N; i += 256) {
+  for (int i = tid; i < N; i += kFinishThreads) {
     const int t = key_index(rowkey[i]);
     l.tgt[i] = t;
     if (a.tgt_out) a.tgt_out[(size_t)b * N + i] = t;
@@ -416,7 +419,7 @@ hipError_t launch_accept(const void* logits, int f32, const int32_t* draft, cons
   if (N <= 64)
     hipLaunchKernelGGL(accept_finish_wave, dim3(B), dim3(64), 0, st, a);
   else
-    hipLaunchKernelGGL(accept_finish, dim3(B), dim3(256), accept_lds_bytes(N) + (size_t)N * 8,
+    hipLaunchKernelGGL(accept_finish, dim3(B), dim3(kFinishThreads), accept_lds_bytes(N) + (size_t)N * 8,
                        st, a);
   return hipGetLastError();
 }

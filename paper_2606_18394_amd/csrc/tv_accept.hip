@@ -149,8 +149,10 @@ __device__ __forceinline__ unsigned long long scan_slice(const AcceptArgs& a, in
   return key;
 }
 
-// Threads of the one-workgroup acceptance of trees over 64 nodes.
+// Threads of the one-workgroup acceptance of trees over 64 nodes (512
+// measured faster than 256 or 1024 at 128 and 512 nodes).
 constexpr int kFinishThreads = 512;
+static_assert(kMaxNodes % kFinishThreads == 0, "whole node batches per thread");
 
 // Per-node LDS arrays of one sequence's acceptance (accept_lds_bytes).
 struct SeqLds {
@@ -183,7 +185,8 @@ __device__ __forceinline__ void load_nodes(const AcceptArgs& a, int b, int (&pv)
 }
 
 // Acceptance of sequence b once l.tgt holds every node's prediction; pv and
-// dv hold parent and draft token of nodes tid + 256 k.  All kFinishThreads threads.
+// dv hold parent and draft token of nodes tid + kFinishThreads k.  Called by
+// all threads of the workgroup.
 __device__ __forceinline__ void accept_sequence(const AcceptArgs& a, int b, const SeqLds& l,
                                                 const int (&pv)[kMaxNodes / kFinishThreads],
                                                 const int (&dv)[kMaxNodes / kFinishThreads]) {

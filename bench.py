@@ -8,20 +8,36 @@ Inputs are seeded synthetic tensors of the workload's shape, resident in HBM
 before timing starts; R input replicas (> 512 MB in total, twice the MI355X
 last-level cache) are rotated so every step reads from HBM.
 
-Prints one JSON line: tree-tokens/s (B*N / step time), ms per step, the
-roofline position of the dominant kernel (algorithmic bytes or flops over its
-event-timed duration) and the CPU oracle's throughput on a bounded sample.
+The headline workload is the largest configuration (big_tree_32b: Qwen3-32B
+attention geometry, one sequence, 8192 cached rows, a 512-node tree).  Every
+one of the five workloads is also measured the same way and reported in
+``detail.per_config``: step, attention and acceptance times, tree-tokens/s,
+the roofline position of each kernel, and the error of the timed outputs
+against the CPU oracle on a sample.
+
+Prints one JSON line: tree-tokens/s (B*N / step time) of the headline, ms
+per step, the roofline position of the dominant kernel (algorithmic bytes or
+flops over its event-timed duration) and the CPU oracle's throughput on a
+bounded sample.
 """
 from __future__ import annotations
 
-import argparse
-import hashlib
-import json
 import os
-import sys
-import time
 
-import numpy as np
+# The CPU leg's thread count is pinned before numpy loads its BLAS: the
+# environment's value if set, else every CPU this process may run on.
+AFFINITY_CPUS = len(os.sched_getaffinity(0))
+THREAD_VARS = ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS")
+for _v in THREAD_VARS:
+    os.environ.setdefault(_v, str(AFFINITY_CPUS))
+
+import argparse  # noqa: E402
+import hashlib  # noqa: E402
+import json  # noqa: E402
+import sys  # noqa: E402
+import time  # noqa: E402
+
+import numpy as np  # noqa: E402
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
@@ -32,6 +48,9 @@ BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 MALL_BYTES = 256 << 20
 PAGE_BLOCK = 64                # rows per paged-cache block in the paged timing
 TRAIN_ANCHORS, TRAIN_BLOCK, TRAIN_CONTEXT = 512, 16, 4096   # training-mask attention timing
+HEADLINE = "big_tree_32b"
+WORKLOAD_ORDER = ["tiny", "qwen3_8b", "long_ctx", "batched_30b_a3b", "big_tree_32b"]
+CHECK_NODES = 16               # nodes per sequence whose timed output the oracle checks
 
 
 def parse():
@@ -39,18 +58,25 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="qwen3_8b")
+    ap.add_argument("--workload", default=HEADLINE,
+                    help="headline workload (default: the largest, big_tree_32b)")
+    ap.add_argument("--core-only", action="store_true",
+                    help="time only the headline workload's step, attention and acceptance "
+                         "(no other workloads, no extra paths, no CPU leg): the profiler runs")
     ap.add_argument("--replicas", type=int, default=0, help="0 = enough to exceed 2x the LLC")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the CPU leg (oracle timing and the oracle checks)")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--copy-only", action="store_true",
                     help="only run 10 plain device copies of 256 MiB (calibrates the HBM "
                          "traffic counters: each copy reads and writes exactly 256 MiB)")
+    ap.add_argument("--kernel", default="attn_main", choices=["attn_main", "accept_scan"],
+                    help="kernel family the --summarize-traffic summary covers")
     ap.add_argument("--summarize-traffic", nargs=4, default=None,
                     metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
                     help="no GPU: turn the counter CSVs of four rocprofv3 --pmc runs (FETCH_SIZE "
                          "and WRITE_SIZE of this benchmark, then of --copy-only) into "
-                         "profiles/traffic_attn_main_<workload>.json and .md")
+                         "profiles/traffic_<kernel>_<workload>.json and .md")
     ap.add_argument("--summarize-counters", nargs="+", default=None, metavar="PMC_DIR",
                     help="no GPU: turn rocprofv3 --pmc runs of this benchmark (one or more "
                          "output directories) into profiles/counters_attn_main_<workload>.md")
@@ -76,25 +102,31 @@ def _counter_rows(d, counter):
     return rows
 
 
-def summarize_traffic(dirs, workload):
-    """HBM bytes per launch of the contiguous-cache attention kernel from
-    FETCH_SIZE / WRITE_SIZE (KiB per dispatch), each scaled by what the same
-    counter reads for a 256 MiB device copy."""
-    import re
-    import statistics
+KERNEL_PATTERNS = {
     # the verification launch is the contiguous-cache instantiation with the
     # most dispatches (the other timed paths launch fewer)
-    pat = re.compile(r"attn_main<(\d+), (\d+), (\d+), (\d+)(?:, false)?>")
+    "attn_main": (r"attn_main<(\d+), (\d+), (\d+), (\d+)(?:, false)?>", "attn_main<%s,%s,%s,%s>"),
+    "accept_scan": (r"accept_scan<(\w+), (\w+)>", "accept_scan<%s,%s>"),
+}
+
+
+def summarize_traffic(dirs, workload, kernel_family):
+    """HBM bytes per launch of one kernel from FETCH_SIZE / WRITE_SIZE (KiB
+    per dispatch), each scaled by what the same counter reads for a 256 MiB
+    device copy."""
+    import re
+    import statistics
+    pat = re.compile(KERNEL_PATTERNS[kernel_family][0])
+    fmt = KERNEL_PATTERNS[kernel_family][1]
     med, names, n = {}, set(), {}
     for d, c in zip(dirs[:2], ["FETCH_SIZE", "WRITE_SIZE"]):
         by = {}
         for r in _counter_rows(d, c):
             m = pat.search(r["Kernel_Name"])
             if m:
-                by.setdefault("attn_main<%s,%s,%s,%s>" % m.groups(), []).append(
-                    float(r["Counter_Value"]))
+                by.setdefault(fmt % m.groups(), []).append(float(r["Counter_Value"]))
         if not by:
-            raise SystemExit(f"no contiguous attn_main dispatches in {d}")
+            raise SystemExit(f"no {kernel_family} dispatches in {d}")
         name = max(by, key=lambda k: len(by[k]))
         names.add(name)
         med[c], n[c] = statistics.median(by[name]), len(by[name])
@@ -118,7 +150,7 @@ def summarize_traffic(dirs, workload):
                                 "write_scale": round(ws, 4)},
            "hbm_bytes_per_launch": int(round(fetch_b + write_b)),
            "kernel_src_sha": kernel_source_sha()}
-    base = os.path.join(ROOT, "profiles", f"traffic_attn_main_{workload}")
+    base = os.path.join(ROOT, "profiles", f"traffic_{kernel_family}_{workload}")
     with open(base + ".json", "w") as fh:
         json.dump(rec, fh, indent=1)
         fh.write("\n")
@@ -127,11 +159,11 @@ def summarize_traffic(dirs, workload):
 
 Commands (repository root, rocprofv3 run from /tmp with TMPDIR=/tmp; one counter per run):
 
-    rocprofv3 --pmc FETCH_SIZE --output-format csv -d <f> -o b -- python3 bench.py --workload {workload} --no-cpu-baseline --steps 40 --warmup 5
-    rocprofv3 --pmc WRITE_SIZE --output-format csv -d <w> -o b -- python3 bench.py --workload {workload} --no-cpu-baseline --steps 40 --warmup 5
+    rocprofv3 --pmc FETCH_SIZE --output-format csv -d <f> -o b -- python3 bench.py --workload {workload} --core-only --steps 40 --warmup 5
+    rocprofv3 --pmc WRITE_SIZE --output-format csv -d <w> -o b -- python3 bench.py --workload {workload} --core-only --steps 40 --warmup 5
     rocprofv3 --pmc FETCH_SIZE --output-format csv -d <cf> -o c -- python3 bench.py --copy-only
     rocprofv3 --pmc WRITE_SIZE --output-format csv -d <cw> -o c -- python3 bench.py --copy-only
-    python3 bench.py --workload {workload} --summarize-traffic <f> <w> <cf> <cw>
+    python3 bench.py --workload {workload} --kernel {kernel_family} --summarize-traffic <f> <w> <cf> <cw>
 
 Calibration: a plain {COPY_BYTES >> 20} MiB device copy reads FETCH_SIZE = {cal['FETCH_SIZE']:.1f} KiB
 and WRITE_SIZE = {cal['WRITE_SIZE']:.1f} KiB per dispatch against {kib:.0f} KiB moved each way, so
@@ -158,8 +190,8 @@ def summarize_counters(dirs, workload):
     import glob
     import re
     import statistics
-    pat = re.compile(r"attn_main<(\d+), (\d+), (\d+), (\d+)(?:, false)?>")
-    vals, durs, cmds = {}, {}, []
+    pat = re.compile(KERNEL_PATTERNS["attn_main"][0])
+    vals, durs = {}, {}
     for d in dirs:
         for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
             with open(f) as fh:
@@ -186,7 +218,7 @@ def summarize_counters(dirs, workload):
             "SQ_WAIT_INST_LDS SQ_LDS_IDX_ACTIVE"]
     for cs in sets:
         lines.append(f"    rocprofv3 --pmc {cs} --output-format csv -d <out> -o p -- python3 "
-                     f"bench.py --workload {workload} --no-cpu-baseline --steps 20 --warmup 2")
+                     f"bench.py --workload {workload} --core-only --steps 20 --warmup 2")
     lines += [f"    python3 bench.py --workload {workload} --summarize-counters <out> <out2>", "",
               f"Median over {len(durs[kernel])} counter-run dispatches of the kernel; its median "
               f"duration in those runs is {t * 1e6:.1f} us.", "",
@@ -230,7 +262,6 @@ def summarize_trace(trace_dir, bench_log, workload):
         raise SystemExit(f"expected one kernel_stats.csv under {trace_dir}, got {files}")
     with open(files[0]) as fh:
         rows = list(csv.DictReader(fh))
-    # per-dispatch durations (median, p10, p90) from the trace itself
     durs = {}
     for f in glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True):
         with open(f) as fh:
@@ -245,16 +276,16 @@ def summarize_trace(trace_dir, bench_log, workload):
     if line is None or line["config"]["workload"] != workload:
         raise SystemExit(f"no bench line for {workload} in {bench_log}")
     c, d = line["config"], line["detail"]
+    pc = d["per_config"][workload]
     out = [f"# Kernel trace: workload {workload} (B={c['B']}, Hq={c['Hq']}, Hkv={c['Hkv']}, "
            f"D={c['D']}, L={c['Lmax']}, N={c['N']}, V={c['V']} {c['logits']})", "",
            "Command (repository root; rocprofv3 run from /tmp with TMPDIR=/tmp):", "",
            f"    rocprofv3 --kernel-trace --stats --output-format csv -d <out> -o bench -- "
-           f"python3 bench.py --workload {workload} --no-cpu-baseline",
+           f"python3 bench.py --workload {workload} --core-only",
            f"    python3 bench.py --workload {workload} --summarize-trace <out> <log of the same "
            f"bench.py command without the profiler>", "",
-           "Calls include warm-up, graph capture and every timed graph (step, attention, "
-           "acceptance, draft top-W, tree build, paged attention, tree-tail attention, path "
-           "commit).", "",
+           "Calls include warm-up, graph capture and every timed graph (step, attention alone, "
+           "acceptance alone).", "",
            "| kernel | calls | avg us | median us | p10 us | p90 us | min us | max us | "
            "% of GPU time |",
            "|---|---|---|---|---|---|---|---|---|"]
@@ -268,21 +299,8 @@ def summarize_trace(trace_dir, bench_log, workload):
                    f"{float(r['Percentage']):.2f} |")
     out += ["", "Same command without the profiler (HIP events around graph replays on the "
             "launch stream):", "",
-            f"    step {d['us_per_step']:.2f} us = attention {d['attention_us']:.2f} us + "
-            f"acceptance {d['accept_us']:.2f} us",
-            f"    drafting (not in the step): top-W {d['draft_topw_us']:.2f} us, tree build "
-            f"{d['build_tree_us']:.2f} us",
-            f"    paged attention ({d['page_block']}-row blocks) {d['paged_attention_us']:.2f} us, "
-            f"tree-tail attention {d['tree_tail_attention_us']:.2f} us, "
-            f"path commit {d['commit_us']:.2f} us",
-            f"    non-greedy acceptance (T = 1) {d['sampled_accept']['us']:.2f} us",
-            f"    training-mask attention ({d['training_mask_attention']['anchors']} blocks of "
-            f"{d['training_mask_attention']['block']} over {d['training_mask_attention']['context']}"
-            f" context rows) {d['training_mask_attention']['us']:.1f} us"]
-    if "copy_floor" in d:
-        out.append(f"    device copy of the attention's {d['copy_floor']['bytes_moved'] / 1e6:.1f} MB "
-                   f"(the streaming floor) {d['copy_floor']['us']:.2f} us")
-    out.append("")
+            f"    step {pc['us_per_step']:.2f} us = attention {pc['attention_us']:.2f} us + "
+            f"acceptance {pc['accept_us']:.2f} us", ""]
     path = os.path.join(ROOT, "profiles", f"kernel_trace_{workload}.md")
     with open(path, "w") as fh:
         fh.write("\n".join(out))
@@ -343,14 +361,36 @@ def measured_traffic(kernel, workload):
     return rec.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(inp, w, draft, budget_s):
-    """The oracle, as it stands, on a bounded sample of the same step."""
-    import oracle
+def roofline(name, t_s, nbytes, flops, kernel, workload):
+    """Position of one kernel against the roofline that binds it: HBM bytes
+    or bf16 MFMA flops at the MI355X peaks, whichever takes longer."""
+    if flops == 0 or nbytes / (HBM_PEAK_GBS * 1e9) >= flops / (BF16_PEAK_TFLOPS * 1e12):
+        r = {"bound": "hbm", "achieved": nbytes / t_s / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    else:
+        r = {"bound": "mfma", "achieved": flops / t_s / 1e12, "peak": BF16_PEAK_TFLOPS,
+             "unit": "TFLOP/s"}
+    r["frac"] = r["achieved"] / r["peak"]
+    r["kernel"] = name
+    r["traffic"] = measured_traffic(kernel, workload)
+    return r
+
+
+# --------------------------------------------------------------------- CPU leg
+
+def _thread_report():
     try:
         from threadpoolctl import threadpool_info
-        cores = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+        blas = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
     except Exception:
-        cores = 1
+        blas = None
+    return blas, {v: os.environ.get(v) for v in THREAD_VARS}
+
+
+def cpu_baseline(inp, w, draft, budget_s):
+    """The oracle, as it stands, timed on a bounded sample of the same step
+    (and its attention sample compared with nothing: timing only)."""
+    import oracle
+    blas, env = _thread_report()
     q = oracle.decode_bf16(inp["q"])
     kc, vc = oracle.decode_bf16(inp["k_cache"]), oracle.decode_bf16(inp["v_cache"])
     kt, vt = oracle.decode_bf16(inp["k_tree"]), oracle.decode_bf16(inp["v_tree"])
@@ -371,17 +411,372 @@ def cpu_baseline(inp, w, draft, budget_s):
     oracle.tree_accept(lg, draft, inp["parent"], w.Dmax)
     acc_step = time.perf_counter() - t0
     step = attn_step + acc_step
-    return {"value": w.B * w.N / step, "unit": "tree-tokens/s", "cores": int(cores),
-            "kind": "oracle",
+    return {"value": w.B * w.N / step, "unit": "tree-tokens/s",
+            "cores": int(blas) if blas else AFFINITY_CPUS, "kind": "oracle",
+            "affinity_cpus": AFFINITY_CPUS, "blas_threads": blas, "thread_env": env,
+            "us_per_step": step * 1e6,
             "sample": f"attention on {n_nodes}/{w.N} nodes x all {w.Hq} heads of batch {w.B} "
                       f"({t_attn:.1f} s, scaled to all nodes) + full acceptance "
-                      f"({acc_step:.1f} s); fp64 numpy"}
+                      f"({acc_step:.1f} s); fp64 numpy, BLAS on {blas} threads, elementwise "
+                      f"work on one"}
+
+
+def oracle_check(inp, w, draft, got_rows, nodes, acc):
+    """The timed outputs against the oracle: attention on the sampled nodes
+    (all heads) as max-abs error, acceptance bit for bit."""
+    import oracle
+    dec = oracle.decode_bf16
+    err = 0.0
+    for b in range(w.B):
+        ref = oracle.tree_attention(dec(inp["q"][b:b + 1]), dec(inp["k_cache"][b:b + 1]),
+                                    dec(inp["v_cache"][b:b + 1]), dec(inp["k_tree"][b:b + 1]),
+                                    dec(inp["v_tree"][b:b + 1]), inp["parent"][b:b + 1],
+                                    inp["kv_len"][b:b + 1], nodes=nodes[b])[0]
+        err = max(err, float(np.abs(got_rows[b] - ref).max()))
+    lg = inp["logits"] if w.logits_dtype == "f32" else dec(inp["logits"])
+    rl, rp, rt = oracle.tree_accept(lg, draft, inp["parent"], w.Dmax)
+    exact = bool(np.array_equal(acc[0], rl) and np.array_equal(acc[1], rp) and
+                 np.array_equal(acc[2], rt))
+    return {"attention_max_abs_err": err,
+            "attention_rows_checked": int(sum(len(n) for n in nodes) * w.Hq),
+            "accept_bit_exact": exact}
+
+
+def check_nodes(parent_row, k, seed):
+    """Nodes whose timed attention output the oracle checks: the root, the
+    last node, the deepest node and a seeded sample."""
+    N = len(parent_row)
+    d = depths(parent_row)
+    pick = {0, N - 1, int(np.argmax(d))}
+    pick |= set(np.random.default_rng(seed).choice(N, size=min(k, N), replace=False).tolist())
+    return np.array(sorted(pick))
+
+
+# --------------------------------------------------------------------- GPU
+
+def _bf(torch, dev, a):
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+
+def _i32(torch, dev, a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
+
+
+class Timer:
+    """HIP graphs of a step's launches, replayed between HIP events on the
+    stream the graphs are launched on.  One graph runs the R replicas in
+    turn, R more graphs run one replica each, so exactly k calls are timed
+    and the timed region measures the GPU, not Python's launch overhead."""
+
+    def __init__(self, torch, R):
+        self.torch, self.R, self.graphs = torch, R, {}
+
+    def capture(self, name, fn):
+        torch = self.torch
+
+        def cap(rs):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for r in rs:
+                    fn(r)
+            return g
+        self.graphs[name] = (cap(range(self.R)), [cap([r]) for r in range(self.R)])
+
+    def time_ms(self, name, k):
+        torch = self.torch
+        full, singles = self.graphs[name]
+        for _ in range(2):             # untimed graph warmup
+            full.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(k // self.R):
+            full.replay()
+        for r in range(k % self.R):
+            singles[r].replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / k     # ms
+
+
+def run_workload(name, args, extras, cpu_leg):
+    """Times one workload's step (attention + acceptance), and each alone;
+    with ``extras`` also the paths around the step.  Returns the per-config
+    record, the extra timings and what the CPU leg needs."""
+    import torch
+    from paper_2606_18394_amd import synth, tree_accept, tree_verify_attention
+    from paper_2606_18394_amd.binding import load_library
+
+    lib = load_library()
+    w = synth.WORKLOADS[name]
+    dev = torch.device("cuda:0")
+    inp = synth.draw(w)
+    bf = lambda a: _bf(torch, dev, a)      # noqa: E731
+    i32 = lambda a: _i32(torch, dev, a)    # noqa: E731
+
+    logits0 = torch.from_numpy(inp["logits"]).to(dev) if w.logits_dtype == "f32" \
+        else bf(inp["logits"])
+    # draft tokens per the workload recipe (argmax at the parent, first max)
+    tgt = logits0.float().argmax(dim=-1).cpu().numpy()
+    draft = synth.draft_tokens(inp["parent"], tgt, inp["match"], inp["rand_tok"])
+    del tgt
+
+    base = dict(q=bf(inp["q"]), kc=bf(inp["k_cache"]), vc=bf(inp["v_cache"]),
+                kt=bf(inp["k_tree"]), vt=bf(inp["v_tree"]), logits=logits0)
+    per_rep = sum(t.numel() * t.element_size() for t in base.values())
+    R = args.replicas or max(1, -(-2 * MALL_BYTES // per_rep))
+    reps = [base] + [{k: v.clone() for k, v in base.items()} for _ in range(R - 1)]
+    parent, kv_len, draft_d = i32(inp["parent"]), i32(inp["kv_len"]), i32(draft)
+    outs = [torch.empty(w.B, w.N, w.Hq, w.D, dtype=torch.bfloat16, device=dev) for _ in range(R)]
+    acc_len = torch.empty(w.B, dtype=torch.int32, device=dev)
+    path = torch.empty(w.B, w.Dmax, dtype=torch.int32, device=dev)
+    targ = torch.empty(w.B, w.N, dtype=torch.int32, device=dev)
+    ws_attn = torch.zeros(max(256, lib.tv_tree_verify_attention_workspace(
+        w.B, w.N, w.Hq, w.Hkv, w.D, w.L)), dtype=torch.uint8, device=dev)
+    ws_acc = torch.zeros(lib.tv_tree_accept_workspace(w.B, w.N, w.V), dtype=torch.uint8,
+                         device=dev)
+
+    def attn(r):
+        x = reps[r]
+        tree_verify_attention(x["q"], x["kc"], x["vc"], x["kt"], x["vt"], parent, outs[r],
+                              kv_len=kv_len, workspace_tensor=ws_attn)
+
+    def accept(r):
+        tree_accept(reps[r]["logits"], draft_d, parent, w.Dmax, accept_len=acc_len, path=path,
+                    tgt_argmax=targ, workspace_tensor=ws_acc)
+
+    def step(r):
+        attn(r)
+        accept(r)
+
+    side = torch.cuda.Stream(device=dev)
+    side.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(side):
+        for s in range(args.warmup):
+            step(s % R)
+    torch.cuda.current_stream(dev).wait_stream(side)
+    torch.cuda.synchronize()
+
+    timer = Timer(torch, R)
+    for nm, fn in [("step", step), ("attn", attn), ("accept", accept)]:
+        timer.capture(nm, fn)
+    torch.cuda.synchronize()
+    print(f"[bench] {w.name}: {R} replicas of {per_rep / 2**20:.1f} MiB; warmup done, "
+          f"graphs captured", file=sys.stderr, flush=True)
+    ms_step = timer.time_ms("step", args.steps)
+    ms_attn = timer.time_ms("attn", args.steps)
+    ms_acc = timer.time_ms("accept", args.steps)
+    print(f"[bench] {w.name}: step {ms_step * 1e3:.2f} us, attention {ms_attn * 1e3:.2f} us, "
+          f"accept {ms_acc * 1e3:.2f} us", file=sys.stderr, flush=True)
+
+    # the timed graphs computed real results: keep what the oracle checks
+    nodes = [check_nodes(inp["parent"][b], CHECK_NODES, 11 + b) for b in range(w.B)]
+    got_all = outs[0].float().cpu().numpy()      # every replica holds the same inputs
+    got_rows = [got_all[b][nodes[b]] for b in range(w.B)]
+    del got_all
+    acc = (acc_len.cpu().numpy(), path.cpu().numpy(), targ.cpu().numpy())
+
+    attn_bytes, attn_flops, acc_bytes = algorithmic_work(inp, w)
+    rec = {
+        "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "D": w.D, "Lmax": w.L, "N": w.N, "V": w.V,
+        "logits": w.logits_dtype, "kv_len_sum": int(inp["kv_len"].sum()), "replicas": R,
+        "us_per_step": ms_step * 1e3, "attention_us": ms_attn * 1e3, "accept_us": ms_acc * 1e3,
+        "tree_tokens_per_s": w.B * w.N / (ms_step * 1e-3),
+        "attention_bytes": attn_bytes, "attention_flops": attn_flops, "accept_bytes": acc_bytes,
+        "attention_roofline": roofline("tree_verify_attention", ms_attn * 1e-3, attn_bytes,
+                                       attn_flops, "attn_main", w.name),
+        "accept_roofline": roofline("tree_accept", ms_acc * 1e-3, acc_bytes, 0,
+                                    "accept_scan", w.name),
+        "cache": "cold (replicas rotated)",
+    }
+
+    extra = None
+    if extras:
+        extra = run_extras(torch, w, inp, args, dev, R, reps, parent, kv_len, draft_d, outs,
+                           acc_len, path, ws_attn, attn, attn_bytes)
+    cpu_in = (inp, draft, got_rows, nodes, acc) if cpu_leg else None
+    del reps, outs, timer, base
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return w, rec, extra, cpu_in
+
+
+def run_extras(torch, w, inp, args, dev, R, reps, parent, kv_len, draft_d, outs, acc_len, path,
+               ws_attn, attn, attn_bytes):
+    """The paths around the step at the headline workload, timed apart:
+    drafting, the paged and tree-tail attention, the non-greedy acceptance,
+    the training-mask attention, the path commit and a device-copy floor."""
+    from paper_2606_18394_amd import (block_causal_attention, build_tree, commit_path,
+                                      draft_topw, synth, tree_accept_sampled,
+                                      tree_verify_attention, tree_verify_attention_paged)
+    from paper_2606_18394_amd.binding import load_library
+    lib = load_library()
+    bf = lambda a: _bf(torch, dev, a)      # noqa: E731
+    i32 = lambda a: _i32(torch, dev, a)    # noqa: E731
+
+    # Tree drafting (the step that builds the verified trees): top-W of the
+    # draft logits per draft depth, then the best-first tree.
+    Wd = synth.draft_width(w)
+    dl = synth.draft_logits(w)
+    dlog0 = torch.from_numpy(dl).to(dev) if w.logits_dtype == "f32" else bf(dl)
+    dlogs = [dlog0] + [dlog0.clone() for _ in range(R - 1)]
+    dtok = torch.empty(w.B, w.depth, Wd, dtype=torch.int32, device=dev)
+    dlp = torch.empty(w.B, w.depth, Wd, dtype=torch.float32, device=dev)
+
+    def topw(r):
+        draft_topw(dlogs[r], Wd, tok=dtok, logp=dlp)
+
+    def build(r):
+        build_tree(dtok, dlp, w.N)
+
+    # The same attention over a paged cache (shuffled blocks of PAGE_BLOCK rows)
+    prng = np.random.default_rng(w.seed + 77)
+    mb = -(-w.L // PAGE_BLOCK)
+    btab, nblk = synth.block_table(prng, w.B, mb, spare=7)
+    kpool0 = bf(synth.scatter_pool(prng, inp["k_cache"], btab, nblk, PAGE_BLOCK))
+    vpool0 = bf(synth.scatter_pool(prng, inp["v_cache"], btab, nblk, PAGE_BLOCK))
+    pools = [(kpool0, vpool0)] + [(kpool0.clone(), vpool0.clone()) for _ in range(R - 1)]
+    btab_d = i32(btab)
+
+    def attn_paged(r):
+        kp, vp = pools[r]
+        x = reps[r]
+        tree_verify_attention_paged(x["q"], kp, vp, btab_d, x["kt"], x["vt"], parent, outs[r],
+                                    kv_len=kv_len, workspace_tensor=ws_attn)
+
+    # tree-tail layout: the tree's K/V written into the cache after the context
+    tk = np.concatenate([inp["k_cache"], np.zeros((w.B, w.N) + inp["k_cache"].shape[2:],
+                                                  inp["k_cache"].dtype)], axis=1)
+    tv = np.concatenate([inp["v_cache"], np.zeros_like(tk[:, :w.N])], axis=1)
+    for b in range(w.B):
+        kl = int(inp["kv_len"][b])
+        tk[b, kl:kl + w.N] = inp["k_tree"][b]
+        tv[b, kl:kl + w.N] = inp["v_tree"][b]
+    tail0 = (bf(tk), bf(tv))
+    tails = [tail0] + [(tail0[0].clone(), tail0[1].clone()) for _ in range(R - 1)]
+    del tk, tv
+    ws_tail = torch.zeros(max(256, lib.tv_tree_verify_attention_workspace(
+        w.B, w.N, w.Hq, w.Hkv, w.D, w.L + w.N)), dtype=torch.uint8, device=dev)
+
+    def attn_tail(r):
+        kc, vc = tails[r]
+        tree_verify_attention(reps[r]["q"], kc, vc, None, None, parent, outs[r], kv_len=kv_len,
+                              workspace_tensor=ws_tail)
+
+    # The draft head's training-mask attention at the workload's head
+    # geometry: TRAIN_ANCHORS blocks of TRAIN_BLOCK positions over a
+    # TRAIN_CONTEXT-row context, anchors uniform over the context.
+    trng = np.random.default_rng(w.seed + 99)
+    TA, TS, TL = TRAIN_ANCHORS, TRAIN_BLOCK, TRAIN_CONTEXT
+    anchors_np = trng.integers(0, TL + 1, size=(1, TA)).astype(np.int32)
+    tq = bf(synth._normal_bf16(trng, (1, TA, TS, w.Hq, w.D)))
+    tkc = bf(synth._normal_bf16(trng, (1, TL, w.Hkv, w.D)))
+    tvc = bf(synth._normal_bf16(trng, (1, TL, w.Hkv, w.D)))
+    tkb = bf(synth._normal_bf16(trng, (1, TA, TS, w.Hkv, w.D)))
+    tvb = bf(synth._normal_bf16(trng, (1, TA, TS, w.Hkv, w.D)))
+    tanc = i32(anchors_np)
+    tout = torch.empty(1, TA, TS, w.Hq, w.D, dtype=torch.bfloat16, device=dev)
+    ws_train = torch.zeros(max(256, lib.tv_block_causal_attention_workspace(
+        1, TA, TS, w.Hq, w.Hkv, w.D, TL)), dtype=torch.uint8, device=dev)
+    train_flops = 4 * w.D * w.Hq * int(sum(int(a) * TS + TS * (TS + 1) // 2
+                                           for a in anchors_np[0]))
+    train_bytes = sum(t.numel() * t.element_size() for t in (tq, tkc, tvc, tkb, tvb, tout))
+
+    def train_attn(r):
+        block_causal_attention(tq, tkc, tvc, tkb, tvb, tanc, tout, workspace_tensor=ws_train)
+
+    # committing the accepted path (kv_len is reset from a copy first, so
+    # every replay commits the same rows; the reset alone is timed too and
+    # subtracted)
+    ccap = w.L + w.Dmax
+    ckc = torch.zeros(w.B, ccap, w.Hkv, w.D, dtype=torch.bfloat16, device=dev)
+    cvc = torch.zeros_like(ckc)
+    ckl0 = kv_len.clone()
+    ckl = kv_len.clone()
+
+    def reset(r):
+        ckl.copy_(ckl0)
+
+    def commit(r):
+        reset(r)
+        commit_path(reps[r]["kt"], reps[r]["vt"], path, acc_len, ckc, cvc, ckl)
+
+    # Non-greedy (T = 1) acceptance of the same trees: the target logits of
+    # the replica, the draft head's logits, one uniform per node.
+    u_acc = torch.from_numpy(np.random.default_rng(w.seed + 5).random(
+        (w.B, w.N), dtype=np.float32)).to(dev)
+    s_len = torch.empty(w.B, dtype=torch.int32, device=dev)
+    s_path = torch.empty(w.B, w.Dmax, dtype=torch.int32, device=dev)
+    s_corr = torch.empty(w.B, dtype=torch.int32, device=dev)
+    ws_samp = torch.zeros(lib.tv_tree_accept_sampled_workspace(w.B, w.N, w.V, w.depth),
+                          dtype=torch.uint8, device=dev)
+
+    def sampled(r):
+        tree_accept_sampled(reps[r]["logits"], dlogs[r], draft_d, parent, u_acc, 1234 + r, 1.0,
+                            w.Dmax, accept_len=s_len, path=s_path, correction=s_corr,
+                            workspace_tensor=ws_samp)
+
+    # The practical floor of a streaming kernel at this size: a plain device
+    # copy moving the attention's algorithmic bytes (half read, half
+    # written), timed like the rest from cold replicas.
+    half = max(1, attn_bytes // 4)  # int16 elements in each direction
+    csrc = [torch.empty(half, dtype=torch.int16, device=dev).fill_(1) for _ in range(R)]
+    cdst = [torch.empty(half, dtype=torch.int16, device=dev) for _ in range(R)]
+
+    def copy_floor(r):
+        cdst[r].copy_(csrc[r])
+
+    for s in range(2):
+        topw(s % R)
+        build(s % R)
+        sampled(s % R)
+    torch.cuda.synchronize()
+    timer = Timer(torch, R)
+    for nm, fn in [("topw", topw), ("build", build), ("attn_paged", attn_paged),
+                   ("attn_tail", attn_tail), ("train_attn", train_attn), ("sampled", sampled),
+                   ("reset", reset), ("copy_floor", copy_floor), ("commit", commit)]:
+        timer.capture(nm, fn)
+    torch.cuda.synchronize()
+    k = args.steps
+    ms = {nm: timer.time_ms(nm, k) for nm in ["topw", "build", "attn_paged", "attn_tail",
+                                              "sampled", "reset", "copy_floor", "commit"]}
+    ms["train_attn"] = timer.time_ms("train_attn", max(10, k // 10))
+    attn(0)
+    ref0 = outs[0].clone()
+    attn_paged(0)
+    torch.cuda.synchronize()
+    paged_same = bool(torch.equal(outs[0].view(torch.int16), ref0.view(torch.int16)))
+    esz = 4 if w.logits_dtype == "f32" else 2
+    # target logits + draft logits read once, plus two rows per sequence for
+    # the correction race
+    samp_bytes = (w.B * (w.N + w.depth) + 2 * w.B) * w.V * esz
+    ms_commit = max(0.0, ms["commit"] - ms["reset"])
+    out = {
+        "draft_topw_us": ms["topw"] * 1e3, "build_tree_us": ms["build"] * 1e3,
+        "draft": {"depth": w.depth, "width": Wd, "budget": w.N},
+        "paged_attention_us": ms["attn_paged"] * 1e3, "page_block": PAGE_BLOCK,
+        "paged_bit_identical": paged_same,
+        "tree_tail_attention_us": ms["attn_tail"] * 1e3,
+        "sampled_accept": {"us": ms["sampled"] * 1e3, "temperature": 1.0, "bytes": samp_bytes,
+                           "GBps": samp_bytes / (ms["sampled"] * 1e-3) / 1e9},
+        "training_mask_attention": {
+            "anchors": TA, "block": TS, "context": TL, "us": ms["train_attn"] * 1e3,
+            "flops": train_flops, "TFLOPs": train_flops / (ms["train_attn"] * 1e-3) / 1e12,
+            "mfma_frac": train_flops / (ms["train_attn"] * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
+            "cache": f"warm: its {train_bytes / 1e6:.0f} MB of inputs and output stay in the "
+                     f"256 MB last-level cache between calls"},
+        "commit_us": ms_commit * 1e3, "commit_rows": int(acc_len.sum().item()),
+        "copy_floor": {"bytes_moved": 4 * half, "us": ms["copy_floor"] * 1e3,
+                       "GBps": 4 * half / (ms["copy_floor"] * 1e-3) / 1e9},
+    }
+    del timer, pools, tails, dlogs, csrc, cdst
+    return out
 
 
 def main():
     args = parse()
     if args.summarize_traffic:
-        summarize_traffic(args.summarize_traffic, args.workload)
+        summarize_traffic(args.summarize_traffic, args.workload, args.kernel)
         return
     if args.summarize_trace:
         summarize_trace(*args.summarize_trace, args.workload)
@@ -398,279 +793,48 @@ def main():
         sys.exit(2)
 
     import torch
-    from paper_2606_18394_amd import (block_causal_attention, build_tree, commit_path,
-                                      draft_topw, synth, tree_accept, tree_accept_sampled,
-                                      tree_verify_attention, tree_verify_attention_paged)
     from paper_2606_18394_amd.binding import load_library
 
     load_library()
-    w = synth.WORKLOADS[args.workload]
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    inp = synth.draw(w)
+    torch.cuda.set_device(torch.device("cuda:0"))
+    cpu_leg = not args.no_cpu_baseline and not args.core_only and \
+        int(os.environ.get("RANK", "0")) == 0
+    names = [args.workload] if args.core_only else \
+        [args.workload] + [n for n in WORKLOAD_ORDER if n != args.workload]
+    per, checks, extra, head_w, cpu = {}, {}, None, None, None
+    for name in names:
+        head = name == args.workload
+        w, rec, ex, cpu_in = run_workload(name, args, extras=head and not args.core_only,
+                                          cpu_leg=cpu_leg)
+        per[name] = rec
+        if head:
+            extra, head_w = ex, w
+        if cpu_in is not None:
+            inp, draft, got_rows, nodes, acc = cpu_in
+            t0 = time.perf_counter()
+            checks[name] = oracle_check(inp, w, draft, got_rows, nodes, acc)
+            rec["oracle_check"] = checks[name]
+            print(f"[bench] {name}: oracle check {checks[name]} "
+                  f"({time.perf_counter() - t0:.1f} s)", file=sys.stderr, flush=True)
+            if head:
+                cpu = cpu_baseline(inp, w, draft, args.cpu_budget_s)
+            del inp, draft, got_rows, nodes, acc, cpu_in
 
-    def bf(a):
-        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
-
-    def i32(a):
-        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
-
-    if w.logits_dtype == "f32":
-        logits0 = torch.from_numpy(inp["logits"]).to(dev)
+    h = per[args.workload]
+    w = head_w
+    ms_step = h["us_per_step"] * 1e-3
+    # the dominant kernel of the step: the longer of attention and acceptance
+    if h["attention_us"] >= h["accept_us"]:
+        roof = dict(h["attention_roofline"])
     else:
-        logits0 = bf(inp["logits"])
-    # draft tokens per the workload recipe (argmax at the parent, first max)
-    tgt = logits0.float().argmax(dim=-1).cpu().numpy()
-    draft = synth.draft_tokens(inp["parent"], tgt, inp["match"], inp["rand_tok"])
-
-    base = dict(q=bf(inp["q"]), kc=bf(inp["k_cache"]), vc=bf(inp["v_cache"]),
-                kt=bf(inp["k_tree"]), vt=bf(inp["v_tree"]), logits=logits0)
-    per_rep = sum(t.numel() * t.element_size() for t in base.values())
-    R = args.replicas or max(1, -(-2 * MALL_BYTES // per_rep))
-    reps = [base] + [{k: v.clone() for k, v in base.items()} for _ in range(R - 1)]
-    parent, kv_len, draft_d = i32(inp["parent"]), i32(inp["kv_len"]), i32(draft)
-    outs = [torch.empty(w.B, w.N, w.Hq, w.D, dtype=torch.bfloat16, device=dev) for _ in range(R)]
-    acc_len = torch.empty(w.B, dtype=torch.int32, device=dev)
-    path = torch.empty(w.B, w.Dmax, dtype=torch.int32, device=dev)
-    targ = torch.empty(w.B, w.N, dtype=torch.int32, device=dev)
-
-    ws_attn = torch.zeros(
-        max(256, load_library().tv_tree_verify_attention_workspace(
-            w.B, w.N, w.Hq, w.Hkv, w.D, w.L)), dtype=torch.uint8, device=dev)
-    ws_acc = torch.zeros(load_library().tv_tree_accept_workspace(w.B, w.N, w.V),
-                         dtype=torch.uint8, device=dev)
-
-    def attn(r):
-        x = reps[r]
-        tree_verify_attention(x["q"], x["kc"], x["vc"], x["kt"], x["vt"], parent, outs[r],
-                              kv_len=kv_len, workspace_tensor=ws_attn)
-
-    def accept(r):
-        tree_accept(reps[r]["logits"], draft_d, parent, w.Dmax, accept_len=acc_len, path=path,
-                    tgt_argmax=targ, workspace_tensor=ws_acc)
-
-    def step(r):
-        attn(r)
-        accept(r)
-
-    # Tree drafting (the step that builds the verified trees): top-W of the
-    # draft logits per draft depth, then the best-first tree; timed apart,
-    # it is not part of the verification step.
-    Wd = synth.draft_width(w)
-    dl = synth.draft_logits(w)
-    dlog0 = torch.from_numpy(dl).to(dev) if w.logits_dtype == "f32" else bf(dl)
-    dlogs = [dlog0] + [dlog0.clone() for _ in range(R - 1)]
-    dtok = torch.empty(w.B, w.depth, Wd, dtype=torch.int32, device=dev)
-    dlp = torch.empty(w.B, w.depth, Wd, dtype=torch.float32, device=dev)
-
-    def topw(r):
-        draft_topw(dlogs[r], Wd, tok=dtok, logp=dlp)
-
-    # The serving side, timed apart: the same attention over a paged cache
-    # (shuffled blocks of PAGE_BLOCK rows), and committing the accepted path
-    # (kv_len is reset from a copy first, so every replay commits the same
-    # rows; the reset alone is timed too and subtracted).
-    prng = np.random.default_rng(w.seed + 77)
-    mb = -(-w.L // PAGE_BLOCK)
-    btab, nblk = synth.block_table(prng, w.B, mb, spare=7)
-    kpool0 = bf(synth.scatter_pool(prng, inp["k_cache"], btab, nblk, PAGE_BLOCK))
-    vpool0 = bf(synth.scatter_pool(prng, inp["v_cache"], btab, nblk, PAGE_BLOCK))
-    pools = [(kpool0, vpool0)] + [(kpool0.clone(), vpool0.clone()) for _ in range(R - 1)]
-    btab_d = i32(btab)
-
-    def attn_paged(r):
-        kp, vp = pools[r]
-        x = reps[r]
-        tree_verify_attention_paged(x["q"], kp, vp, btab_d, x["kt"], x["vt"], parent, outs[r],
-                                    kv_len=kv_len, workspace_tensor=ws_attn)
-
-    # tree-tail layout: the tree's K/V written into the cache after the context
-    kt_np, vt_np = inp["k_tree"], inp["v_tree"]
-    tk = np.concatenate([inp["k_cache"], np.zeros((w.B, w.N) + inp["k_cache"].shape[2:],
-                                                  inp["k_cache"].dtype)], axis=1)
-    tv = np.concatenate([inp["v_cache"], np.zeros_like(tk[:, :w.N])], axis=1)
-    for b in range(w.B):
-        kl = int(inp["kv_len"][b])
-        tk[b, kl:kl + w.N] = kt_np[b]
-        tv[b, kl:kl + w.N] = vt_np[b]
-    tail0 = (bf(tk), bf(tv))
-    tails = [tail0] + [(tail0[0].clone(), tail0[1].clone()) for _ in range(R - 1)]
-    del tk, tv
-
-    def attn_tail(r):
-        kc, vc = tails[r]
-        tree_verify_attention(reps[r]["q"], kc, vc, None, None, parent, outs[r], kv_len=kv_len,
-                              workspace_tensor=ws_tail)
-
-    ws_tail = torch.zeros(
-        max(256, load_library().tv_tree_verify_attention_workspace(
-            w.B, w.N, w.Hq, w.Hkv, w.D, w.L + w.N)), dtype=torch.uint8, device=dev)
-
-    # The draft head's training-mask attention at the workload's head
-    # geometry: TRAIN_ANCHORS blocks of TRAIN_BLOCK positions over a
-    # TRAIN_CONTEXT-row context, anchors uniform over the context.
-    trng = np.random.default_rng(w.seed + 99)
-    TA, TS, TL = TRAIN_ANCHORS, TRAIN_BLOCK, TRAIN_CONTEXT
-    anchors_np = trng.integers(0, TL + 1, size=(1, TA)).astype(np.int32)
-    tq = bf(synth._normal_bf16(trng, (1, TA, TS, w.Hq, w.D)))
-    tkc = bf(synth._normal_bf16(trng, (1, TL, w.Hkv, w.D)))
-    tvc = bf(synth._normal_bf16(trng, (1, TL, w.Hkv, w.D)))
-    tkb = bf(synth._normal_bf16(trng, (1, TA, TS, w.Hkv, w.D)))
-    tvb = bf(synth._normal_bf16(trng, (1, TA, TS, w.Hkv, w.D)))
-    tanc = i32(anchors_np)
-    tout = torch.empty(1, TA, TS, w.Hq, w.D, dtype=torch.bfloat16, device=dev)
-    ws_train = torch.zeros(
-        max(256, load_library().tv_block_causal_attention_workspace(
-            1, TA, TS, w.Hq, w.Hkv, w.D, TL)), dtype=torch.uint8, device=dev)
-    train_flops = 4 * w.D * w.Hq * int(sum(int(a) * TS + TS * (TS + 1) // 2
-                                           for a in anchors_np[0]))
-
-    def train_attn(r):
-        block_causal_attention(tq, tkc, tvc, tkb, tvb, tanc, tout, workspace_tensor=ws_train)
-
-    ccap = w.L + w.Dmax
-    ckc = torch.zeros(w.B, ccap, w.Hkv, w.D, dtype=torch.bfloat16, device=dev)
-    cvc = torch.zeros_like(ckc)
-    ckl0 = kv_len.clone()
-    ckl = kv_len.clone()
-
-    def reset(r):
-        ckl.copy_(ckl0)
-
-    def commit(r):
-        reset(r)
-        commit_path(reps[r]["kt"], reps[r]["vt"], path, acc_len, ckc, cvc, ckl)
-
-    def build(r):
-        build_tree(dtok, dlp, w.N)
-
-    # Non-greedy (T = 1) acceptance of the same trees: the target logits of
-    # the replica, the draft head's logits, one uniform per node.
-    u_acc = torch.from_numpy(np.random.default_rng(w.seed + 5).random(
-        (w.B, w.N), dtype=np.float32)).to(dev)
-    s_len = torch.empty(w.B, dtype=torch.int32, device=dev)
-    s_path = torch.empty(w.B, w.Dmax, dtype=torch.int32, device=dev)
-    s_corr = torch.empty(w.B, dtype=torch.int32, device=dev)
-    ws_samp = torch.zeros(load_library().tv_tree_accept_sampled_workspace(w.B, w.N, w.V, w.depth),
-                          dtype=torch.uint8, device=dev)
-
-    def sampled(r):
-        tree_accept_sampled(reps[r]["logits"], dlogs[r], draft_d, parent, u_acc, 1234 + r, 1.0,
-                            w.Dmax, accept_len=s_len, path=s_path, correction=s_corr,
-                            workspace_tensor=ws_samp)
-
-    # The practical floor of a streaming kernel at this size: a plain device
-    # copy moving the attention's algorithmic bytes (half read, half
-    # written), timed like the rest from cold replicas.
-    attn_bytes0, _, _ = algorithmic_work(inp, w)
-    half = max(1, attn_bytes0 // 4)  # int16 elements in each direction
-    csrc = [torch.empty(half, dtype=torch.int16, device=dev).fill_(1) for _ in range(R)]
-    cdst = [torch.empty(half, dtype=torch.int16, device=dev) for _ in range(R)]
-
-    def copy_floor(r):
-        cdst[r].copy_(csrc[r])
-
-    # Launches are recorded once into HIP graphs (one graph runs the R
-    # replicas in turn, R more graphs run one replica each) so the timed
-    # region measures the GPU, not Python's launch overhead.
-    side = torch.cuda.Stream(device=dev)
-    side.wait_stream(torch.cuda.current_stream(dev))
-    with torch.cuda.stream(side):
-        for s in range(args.warmup):
-            step(s % R)
-    torch.cuda.current_stream(dev).wait_stream(side)
-    torch.cuda.synchronize()
-
-    def capture(fn, rs):
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            for r in rs:
-                fn(r)
-        return g
-
-    graphs = {}
-    for s in range(2):
-        topw(s % R)
-        build(s % R)
-    for name, fn in [("step", step), ("attn", attn), ("accept", accept), ("topw", topw),
-                     ("build", build), ("attn_paged", attn_paged), ("attn_tail", attn_tail),
-                     ("train_attn", train_attn), ("sampled", sampled),
-                     ("reset", reset), ("copy_floor", copy_floor),
-                     ("commit", commit)]:
-        graphs[name] = (capture(fn, range(R)), [capture(fn, [r]) for r in range(R)])
-    torch.cuda.synchronize()
-    print(f"[bench] {w.name}: {R} replicas of {per_rep / 2**20:.1f} MiB; warmup done, "
-          f"graphs captured", file=sys.stderr, flush=True)
-
-    def timed(name, k):
-        full, singles = graphs[name]
-        for _ in range(2):             # untimed graph warmup
-            full.replay()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(k // R):
-            full.replay()
-        for r in range(k % R):
-            singles[r].replay()
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / k     # ms
-
-    ms_step = timed("step", args.steps)
-    ms_attn = timed("attn", args.steps)
-    ms_acc = timed("accept", args.steps)
-    ms_topw = timed("topw", args.steps)
-    ms_build = timed("build", args.steps)
-    ms_paged = timed("attn_paged", args.steps)
-    ms_tail = timed("attn_tail", args.steps)
-    ms_train = timed("train_attn", max(10, args.steps // 10))
-    ms_samp = timed("sampled", args.steps)
-    ms_commit = max(0.0, timed("commit", args.steps) - timed("reset", args.steps))
-    ms_copy = timed("copy_floor", args.steps)
-    attn(0)
-    ref0 = outs[0].clone()
-    attn_paged(0)
-    torch.cuda.synchronize()
-    paged_same = bool(torch.equal(outs[0].view(torch.int16), ref0.view(torch.int16)))
-    print(f"[bench] step {ms_step * 1e3:.2f} us, attention {ms_attn * 1e3:.2f} us, "
-          f"accept {ms_acc * 1e3:.2f} us", file=sys.stderr, flush=True)
-
-    # the graphs computed real results: check the last accept against the
-    # oracle-free expectation that the path is a valid root chain
-    ln = int(acc_len[0].item())
-    assert 1 <= ln <= w.Dmax, ln
-
-    attn_bytes, attn_flops, acc_bytes = algorithmic_work(inp, w)
-    # target logits + draft logits read once, plus two rows per sequence for
-    # the correction race
-    esz = 4 if w.logits_dtype == "f32" else 2
-    samp_bytes = (w.B * (w.N + w.depth) + 2 * w.B) * w.V * esz
-    if ms_attn >= ms_acc:
-        t = ms_attn * 1e-3
-        if attn_bytes / (HBM_PEAK_GBS * 1e9) >= attn_flops / (BF16_PEAK_TFLOPS * 1e12):
-            roof = {"bound": "hbm", "achieved": attn_bytes / t / 1e9, "peak": HBM_PEAK_GBS,
-                    "unit": "GB/s"}
-        else:
-            roof = {"bound": "mfma", "achieved": attn_flops / t / 1e12,
-                    "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
-        roof["kernel"] = "tree_verify_attention"
-        roof["traffic"] = measured_traffic("attn_main", w.name)
-    else:
-        t = ms_acc * 1e-3
-        roof = {"bound": "hbm", "achieved": acc_bytes / t / 1e9, "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "kernel": "tree_accept",
-                "traffic": measured_traffic("accept_scan", w.name)}
-    roof["frac"] = roof["achieved"] / roof["peak"]
-
-    cpu = None
-    if not args.no_cpu_baseline and int(os.environ.get("RANK", "0")) == 0:
-        cpu = cpu_baseline(inp, w, draft, args.cpu_budget_s)
-
-    tokens = w.B * w.N
+        roof = dict(h["accept_roofline"])
+    detail = {"us_per_step": h["us_per_step"], "attention_us": h["attention_us"],
+              "accept_us": h["accept_us"], "per_config": per}
+    if extra is not None:
+        detail.update(extra)
     line = {
-        "metric": "tree-verify \u00b5s/step & tree-tokens/s; % of HBM/MFMA roofline at 1 MI355X",
-        "value": tokens / (ms_step * 1e-3),
+        "metric": "tree-verify µs/step & tree-tokens/s; % of HBM/MFMA roofline at 1 MI355X",
+        "value": h["tree_tokens_per_s"],
         "unit": "tree-tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -683,32 +847,10 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "D": w.D,
                    "Lmax": w.L, "N": w.N, "V": w.V, "logits": w.logits_dtype,
-                   "kv_len_sum": int(inp["kv_len"].sum()), "replicas": R},
+                   "kv_len_sum": h["kv_len_sum"], "replicas": h["replicas"]},
         "roofline": roof,
         "cpu_baseline": cpu,
-        "detail": {"us_per_step": ms_step * 1e3, "attention_us": ms_attn * 1e3,
-                   "accept_us": ms_acc * 1e3, "attention_bytes": attn_bytes,
-                   "attention_flops": attn_flops, "accept_bytes": acc_bytes,
-                   "attention_GBps": attn_bytes / (ms_attn * 1e-3) / 1e9,
-                   "attention_TFLOPs": attn_flops / (ms_attn * 1e-3) / 1e12,
-                   "accept_GBps": acc_bytes / (ms_acc * 1e-3) / 1e9,
-                   "draft_topw_us": ms_topw * 1e3, "build_tree_us": ms_build * 1e3,
-                   "draft": {"depth": w.depth, "width": Wd, "budget": w.N},
-                   "paged_attention_us": ms_paged * 1e3, "page_block": PAGE_BLOCK,
-                   "paged_bit_identical": paged_same,
-                   "paged_attention_GBps": attn_bytes / (ms_paged * 1e-3) / 1e9,
-                   "tree_tail_attention_us": ms_tail * 1e3,
-                   "sampled_accept": {
-                       "us": ms_samp * 1e3, "temperature": 1.0,
-                       "bytes": samp_bytes, "GBps": samp_bytes / (ms_samp * 1e-3) / 1e9},
-                   "training_mask_attention": {
-                       "anchors": TA, "block": TS, "context": TL, "us": ms_train * 1e3,
-                       "flops": train_flops,
-                       "TFLOPs": train_flops / (ms_train * 1e-3) / 1e12,
-                       "mfma_frac": train_flops / (ms_train * 1e-3) / 1e12 / BF16_PEAK_TFLOPS},
-                   "commit_us": ms_commit * 1e3, "commit_rows": int(acc_len.sum().item()),
-                   "copy_floor": {"bytes_moved": 4 * half, "us": ms_copy * 1e3,
-                                  "GBps": 4 * half / (ms_copy * 1e-3) / 1e9}},
+        "detail": detail,
     }
     print(json.dumps(line), flush=True)
 

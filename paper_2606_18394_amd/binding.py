@@ -119,11 +119,31 @@ def _need_tree(k_tree, v_tree, shape, device):
         _need(v_tree, "v_tree", torch.bfloat16, shape, device)
 
 
+_retired = []
+
+
 def workspace(kind: str, nbytes: int, device, stream_ptr: int) -> torch.Tensor:
-    """Zero-filled workspace cached per (kind, device, stream); grows as needed."""
+    """Zero-filled workspace cached per (kind, device, stream); grows as needed.
+
+    A HIP graph captured with a cached workspace keeps writing to that
+    buffer's address on every replay, so a workspace that a larger call
+    replaces is kept alive (in ``_retired``) rather than freed: its memory is
+    never handed to another tensor while the process runs.  Under stream
+    capture nothing is allocated: the cached workspace must already be large
+    enough (make one eager call of the same or a larger size on the capturing
+    stream first), or the caller passes ``workspace_tensor``.
+    """
     key = (kind, str(device), stream_ptr)
     ws = _workspaces.get(key)
     if ws is None or ws.numel() < nbytes:
+        if torch.device(device).type == "cuda" and torch.cuda.is_current_stream_capturing():
+            raise RuntimeError(
+                f"the cached {kind} workspace of this stream is missing or smaller than the "
+                f"{nbytes} bytes this call needs, and a workspace cannot be allocated during "
+                f"graph capture: call once eagerly on the capturing stream first, or pass "
+                f"workspace_tensor")
+        if ws is not None:
+            _retired.append(ws)
         ws = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=device)
         _workspaces[key] = ws
     return ws

@@ -13,11 +13,14 @@
 //   argmax.  Finish: one wave per row merges the splits.
 //
 // build: best-first expansion under a node budget, one wave per sequence.
-//   Node i lives in LDS and is owned by lane i % 64, which caches the best
-//   open node it owns; a pop is a wave argmax of (score, lower index) over
-//   those caches, the winning node's owner rescans its slots, and the up to
-//   W children go to W consecutive lanes.  Scores are fp32 sums
-//   parent + log-probability, the comparisons that decide the tree.
+//   Node i is owned by lane i % 64 (slot i / 64), which keeps the score,
+//   depth and open flag of its slots in registers and caches the best open
+//   node it owns; a pop is a wave argmax of (score, lower index) over those
+//   caches, the winning node's owner rescans its slots in registers, and the
+//   up to W children go to W consecutive lanes.  Only tokens and parents go
+//   to LDS, written during the loop and read once at the end.  Scores are
+//   fp32 sums parent + log-probability, the comparisons that decide the
+//   tree.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>

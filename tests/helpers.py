@@ -81,3 +81,30 @@ def gpu_accept(inp: dict, draft: np.ndarray, Dmax: int, canary: int = 0, workspa
         for buf, n in [(lbuf, B), (pbuf, B * Dmax), (tbuf, B * N)]:
             ok &= bool((buf[:canary] == -77).all() and (buf[canary + n:] == -77).all())
     return ln.cpu().numpy(), path.cpu().numpy(), tgt.cpu().numpy(), ok
+
+
+def oracle_attention_max_err(inp: dict, got: np.ndarray, scale=None) -> float:
+    """Max-abs difference between ``got`` [B,N,Hq,D] and the oracle over every
+    output element.  The oracle runs one (sequence, KV head) at a time, over
+    that head's G query heads and all nodes, which bounds its memory; the
+    calls together cover every row."""
+    B, N, Hq, D = inp["q"].shape
+    Hkv = inp["k_cache"].shape[2]
+    G = Hq // Hkv
+    dec = oracle.decode_bf16
+    err = 0.0
+    for b in range(B):
+        sl = slice(b, b + 1)
+        q, kt, vt = dec(inp["q"][sl]), dec(inp["k_tree"][sl]), dec(inp["v_tree"][sl])
+        kc, vc = dec(inp["k_cache"][sl]), dec(inp["v_cache"][sl])
+        for g in range(Hkv):
+            heads = np.arange(g * G, (g + 1) * G)
+            ref = oracle.tree_attention(q, kc, vc, kt, vt, inp["parent"][sl], inp["kv_len"][sl],
+                                        scale=scale, heads=heads)[0]
+            d = np.abs(got[b][:, heads] - ref)
+            if np.isnan(ref).all():
+                if not np.isnan(got[b]).all():
+                    return float("inf")
+                continue
+            err = max(err, float(d.max()))
+    return err

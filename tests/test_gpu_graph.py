@@ -97,6 +97,11 @@ def test_acceptance_and_drafting_graph_replays():
     ref_tree = [t.clone() for t in built["t"]]
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
+    # the binding allocates nothing under capture: one eager call on the
+    # capturing stream creates its cached workspaces
+    with torch.cuda.stream(side):
+        call()
+    torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.stream(side):
         with torch.cuda.graph(g, stream=side):
@@ -117,3 +122,44 @@ def test_acceptance_and_drafting_graph_replays():
             assert torch.equal(a, b), rep
         tree_accept(lg[:1].contiguous(), draft[:1].contiguous(), par[:1].contiguous(), w.Dmax)
         torch.cuda.synchronize()
+
+
+def test_graph_replay_after_cached_workspace_grows():
+    """A graph captured with the binding's cached workspace, then a larger
+    eager call on the same stream that replaces that workspace: the replaced
+    buffer stays allocated, so replays still write into memory the graph
+    owns and give the eager result bit for bit."""
+    from paper_2606_18394_amd import tree_verify_attention
+    small = synth.WORKLOADS["qwen3_8b"]
+    big = synth.with_shape(small, N=128, L=32768, depth=12)
+    xs, xb = _attn_inputs(small), _attn_inputs(big)
+    out = torch.empty(small.B, small.N, small.Hq, small.D, dtype=torch.bfloat16, device="cuda")
+    outb = torch.empty(big.B, big.N, big.Hq, big.D, dtype=torch.bfloat16, device="cuda")
+
+    def call(x, o):
+        tree_verify_attention(x["q"], x["kc"], x["vc"], x["kt"], x["vt"], x["par"], o,
+                              kv_len=x["kvl"])
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        call(xs, out)                      # creates the stream's cached workspace
+    torch.cuda.synchronize()
+    ref = out.clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            call(xs, out)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(side):
+        call(xb, outb)                     # grows the cached workspace
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    filler = [torch.full((1 << 22,), 3, dtype=torch.int32, device="cuda") for _ in range(8)]
+    torch.cuda.synchronize()
+    for rep in range(3):
+        out.fill_(7.0)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), ref.view(torch.int16)), f"replay {rep}"
+        assert all(int(f.min()) == 3 and int(f.max()) == 3 for f in filler)

@@ -622,9 +622,11 @@ def run_extras(torch, w, inp, args, dev, R, reps, parent, kv_len, draft_d, outs,
     dlogs = [dlog0] + [dlog0.clone() for _ in range(R - 1)]
     dtok = torch.empty(w.B, w.depth, Wd, dtype=torch.int32, device=dev)
     dlp = torch.empty(w.B, w.depth, Wd, dtype=torch.float32, device=dev)
+    ws_topw = torch.zeros(max(256, lib.tv_draft_topw_workspace(w.B, w.depth, w.V)),
+                          dtype=torch.uint8, device=dev)
 
     def topw(r):
-        draft_topw(dlogs[r], Wd, tok=dtok, logp=dlp)
+        draft_topw(dlogs[r], Wd, tok=dtok, logp=dlp, workspace_tensor=ws_topw)
 
     def build(r):
         build_tree(dtok, dlp, w.N)

@@ -61,7 +61,8 @@ typedef enum {
   TV_ERR_UNSUPPORTED = -4,  /* D not in {64,128}, N above TV_MAX_NODES, ... */
   TV_ERR_WORKSPACE = -5,    /* workspace NULL or smaller than required */
   TV_ERR_LAUNCH = -6,       /* the HIP runtime rejected a launch */
-  TV_ERR_ALIGN = -7         /* a tensor pointer is not 16-byte aligned */
+  TV_ERR_ALIGN = -7,        /* a tensor pointer is not 16-byte aligned */
+  TV_ERR_SCRATCH = -8       /* sizes exceed the static scratch of tv_tree_accept_noalloc */
 } tv_status;
 
 /* Largest tree (nodes per sequence, root included) either call accepts. */
@@ -228,6 +229,34 @@ int tv_tree_accept(const void* logits, int logits_dtype,
                    int N, int V, int Dmax, int32_t* accept_len, int32_t* path,
                    int32_t* tgt_argmax, void* workspace,
                    size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * tv_tree_accept without a workspace, for callers that cannot allocate
+ * device memory: code under HIP graph capture, serving loops that must not
+ * call hipMalloc, harnesses that forbid it.  Same arguments (minus the
+ * workspace), results and device-side error behaviour as tv_tree_accept;
+ * the same kernels run.
+ *
+ * The split keys go to a static device array of TV_ACCEPT_SCRATCH_BYTES
+ * inside the library.  Every GPU the library runs on holds its own copy
+ * from the library's load until the process ends; the call itself never
+ * allocates or frees.  The copy used is that of the device `stream` belongs
+ * to (the current device for the null stream); its address is looked up on
+ * the first call on each device.  Nothing in it needs to start at zero: each
+ * call writes every key before reading it.
+ *
+ * Sizes whose keys do not fit (tv_tree_accept_workspace(B, N, V) >
+ * TV_ACCEPT_SCRATCH_BYTES: more than about 1M node rows B*N) return
+ * TV_ERR_SCRATCH and launch nothing.  All calls on one GPU share its array:
+ * calls that may overlap on that GPU (different streams without ordering
+ * between them) race and give wrong results; order them, or use
+ * tv_tree_accept with a workspace per stream.
+ */
+#define TV_ACCEPT_SCRATCH_BYTES (8u << 20)
+int tv_tree_accept_noalloc(const void* logits, int logits_dtype,
+                           const int32_t* draft_tok, const int32_t* parent, int B,
+                           int N, int V, int Dmax, int32_t* accept_len, int32_t* path,
+                           int32_t* tgt_argmax, hipStream_t stream);
 
 /* ---- Budgeted tree drafting (the step before verification) ------------ */
 

@@ -52,6 +52,8 @@ def load_library() -> ctypes.CDLL:
         lib.tv_tree_accept.restype = ci
         lib.tv_tree_accept.argtypes = (
             [vp, ci, i32p, i32p] + [ci] * 4 + [i32p, i32p, i32p, vp, sz, vp])
+        lib.tv_tree_accept_noalloc.restype = ci
+        lib.tv_tree_accept_noalloc.argtypes = [vp, ci, i32p, i32p] + [ci] * 4 + [i32p] * 3 + [vp]
         lib.tv_draft_topw_workspace.restype = sz
         lib.tv_draft_topw_workspace.argtypes = [ci] * 3
         lib.tv_draft_topw.restype = ci
@@ -381,6 +383,33 @@ def tree_accept(logits, draft_tok, parent, Dmax, accept_len=None, path=None,
         _ptr(logits), dt, _ptr(draft_tok), _ptr(parent), B, N, V, int(Dmax),
         _ptr(accept_len), _ptr(path), _ptr(tgt_argmax), _ptr(ws), ws.numel(),
         ctypes.c_void_p(stream)))
+    return accept_len, path, tgt_argmax
+
+
+def tree_accept_noalloc(logits, draft_tok, parent, Dmax, accept_len, path, tgt_argmax=None):
+    """Greedy tree acceptance through the entry point that allocates nothing
+    (its split keys live in the library's static per-GPU scratch).  The
+    caller passes every output; returns (accept_len, path, tgt_argmax)."""
+    lib = load_library()
+    B, N, V = logits.shape
+    dev = logits.device
+    if logits.dtype == torch.bfloat16:
+        dt = TV_BF16
+    elif logits.dtype == torch.float32:
+        dt = TV_F32
+    else:
+        raise TypeError("logits must be bfloat16 or float32")
+    _need(logits, "logits", logits.dtype, device=dev)
+    _need(draft_tok, "draft_tok", torch.int32, (B, N), dev)
+    _need(parent, "parent", torch.int32, (B, N), dev)
+    _need(accept_len, "accept_len", torch.int32, (B,), dev)
+    _need(path, "path", torch.int32, (B, Dmax), dev)
+    if tgt_argmax is not None:
+        _need(tgt_argmax, "tgt_argmax", torch.int32, (B, N), dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    _check(lib.tv_tree_accept_noalloc(
+        _ptr(logits), dt, _ptr(draft_tok), _ptr(parent), B, N, V, int(Dmax),
+        _ptr(accept_len), _ptr(path), _ptr(tgt_argmax), ctypes.c_void_p(stream)))
     return accept_len, path, tgt_argmax
 
 

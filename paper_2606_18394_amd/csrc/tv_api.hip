@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "treeverify.h"
 #include "tv_plan.h"
 
@@ -100,6 +102,9 @@ const char* tv_status_string(int status) {
     case TV_ERR_WORKSPACE: return "TV_ERR_WORKSPACE: workspace missing or too small";
     case TV_ERR_LAUNCH: return "TV_ERR_LAUNCH: the HIP runtime rejected a launch";
     case TV_ERR_ALIGN: return "TV_ERR_ALIGN: tensor pointer not 16-byte aligned";
+    case TV_ERR_SCRATCH:
+      return "TV_ERR_SCRATCH: sizes need more than the allocation-free entry point's static "
+             "scratch (TV_ACCEPT_SCRATCH_BYTES)";
     default: return "unknown treeverify status";
   }
 }
@@ -254,6 +259,62 @@ int tv_tree_accept(const void* logits, int logits_dtype, const int32_t* draft_to
   if (misaligned(workspace)) return TV_ERR_ALIGN;
   hipError_t e = tv::launch_accept(logits, logits_dtype == TV_F32, draft_tok, parent, B, N, V,
                                    Dmax, accept_len, path, tgt_argmax, workspace, stream);
+  return e == hipSuccess ? TV_OK : TV_ERR_LAUNCH;
+}
+
+// ---------------------------------------------------------------- static scratch
+// The split keys of tv_tree_accept_noalloc live in this device array: every
+// GPU the library runs on holds its own copy, from the code object's load
+// until the process ends.  In host code the name is only a stand-in for the
+// symbol, never a device address: the address of the current device's copy
+// comes from hipGetSymbolAddress, once per device, and only that address is
+// passed to kernels.
+static __device__ __align__(256) unsigned char scratch[TV_ACCEPT_SCRATCH_BYTES];
+
+constexpr int kScratchDevices = 64;
+static std::atomic<void*> g_scratch_addr[kScratchDevices];
+
+// Address of `stream`'s device's copy of the scratch array (the device is
+// made current for the lookup and restored afterwards).
+static int scratch_address(hipStream_t stream, void** out) {
+  int dev = -1;
+  if (stream) {
+    hipDevice_t d;
+    if (hipStreamGetDevice(stream, &d) != hipSuccess) return TV_ERR_LAUNCH;
+    dev = (int)d;
+  } else if (hipGetDevice(&dev) != hipSuccess) {
+    return TV_ERR_LAUNCH;
+  }
+  if (dev < 0 || dev >= kScratchDevices) return TV_ERR_UNSUPPORTED;
+  void* p = g_scratch_addr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return TV_ERR_LAUNCH;
+    if (cur != dev && hipSetDevice(dev) != hipSuccess) return TV_ERR_LAUNCH;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev && hipSetDevice(cur) != hipSuccess) return TV_ERR_LAUNCH;
+    if (e != hipSuccess || !p) return TV_ERR_LAUNCH;
+    g_scratch_addr[dev].store(p, std::memory_order_release);
+  }
+  *out = p;
+  return TV_OK;
+}
+
+int tv_tree_accept_noalloc(const void* logits, int logits_dtype, const int32_t* draft_tok,
+                           const int32_t* parent, int B, int N, int V, int Dmax,
+                           int32_t* accept_len, int32_t* path, int32_t* tgt_argmax,
+                           hipStream_t stream) {
+  int rc = check_accept_sizes(B, N, V, Dmax);
+  if (rc != TV_OK) return rc;
+  if (logits_dtype != TV_BF16 && logits_dtype != TV_F32) return TV_ERR_DTYPE;
+  if (!logits || !draft_tok || !parent || !accept_len || !path) return TV_ERR_NULL;
+  if (tv::accept_ws_bytes(B, N) > (size_t)TV_ACCEPT_SCRATCH_BYTES) return TV_ERR_SCRATCH;
+  void* ws = nullptr;
+  if ((rc = scratch_address(stream, &ws)) != TV_OK) return rc;
+  // every split key is written by the scan before the finish reads it:
+  // nothing in the scratch has to start at zero
+  hipError_t e = tv::launch_accept(logits, logits_dtype == TV_F32, draft_tok, parent, B, N, V,
+                                   Dmax, accept_len, path, tgt_argmax, ws, stream);
   return e == hipSuccess ? TV_OK : TV_ERR_LAUNCH;
 }
 

@@ -42,7 +42,7 @@ def test_every_declared_symbol_is_exported():
 def test_status_strings_and_version():
     lib = _lib()
     assert lib.tv_version() == 1
-    for code in [0, -1, -2, -3, -4, -5, -6, -7]:
+    for code in [0, -1, -2, -3, -4, -5, -6, -7, -8]:
         assert lib.tv_status_string(code)
     assert b"unknown" in lib.tv_status_string(123)
 
@@ -116,6 +116,29 @@ def test_accept_host_errors():
     assert _acc(lib, ws=None) == -5
     assert _acc(lib, wsb=8) == -5
     assert _acc(lib, ws=FAKE + 4) == -7
+
+
+def test_accept_noalloc_host_errors():
+    """The allocation-free acceptance checks its sizes before it touches a
+    GPU: errors come back with nothing launched."""
+    lib = _lib()
+
+    def call(**kw):
+        a = dict(logits=FAKE, dt=0, draft=FAKE, parent=FAKE, B=1, N=64, V=151936, Dmax=9,
+                 ln=FAKE, path=FAKE, tgt=None)
+        a.update(kw)
+        return lib.tv_tree_accept_noalloc(a["logits"], a["dt"], a["draft"], a["parent"], a["B"],
+                                          a["N"], a["V"], a["Dmax"], a["ln"], a["path"],
+                                          a["tgt"], None)
+    assert call(logits=None) == -1
+    assert call(path=None) == -1
+    assert call(dt=3) == -3
+    assert call(B=0) == -2
+    assert call(N=2049) == -4
+    # split keys beyond the static scratch: 1.2M node rows
+    assert lib.tv_tree_accept_workspace(600, 2048, 8) > (8 << 20)
+    assert call(B=600, N=2048, V=8) == -8
+    assert b"TV_ERR_SCRATCH" in lib.tv_status_string(-8)
 
 
 def test_binding_refuses_cpu_tensors():

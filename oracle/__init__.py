@@ -16,10 +16,12 @@ Contents
   kv_commit       -- the cache side: committing the accepted path, paged
                      caches, the tree-tail layout (App. E).
   tree_accept_sampled -- non-greedy (temperature) tree acceptance: the
-                     speculative sampling test min(1, p/q) per draft node,
-                     deepest accepted path, correction token drawn from the
-                     residual (Sec. 2.4); philox -- its counter-based
-                     random numbers (Salmon et al. 2011).
+                     speculative sampling rule (Sec. 2.4) applied to each
+                     node's deterministic children in turn against the
+                     target's residual, which keeps verification lossless
+                     (Sec. 2.2); correction token drawn from the final
+                     residual; philox -- its counter-based random numbers
+                     (Salmon et al. 2011).
   block_causal    -- attention under the draft head's training mask: anchor
                      blocks that see the prefix before their anchor and
                      their own earlier positions (App. Training Details).

@@ -14,9 +14,10 @@ Independent constructions used to pin the oracle:
     the tree rows;
   * training-mask attention: the visible key list of each query is built
     from the block rule directly, in Python floats;
-  * sampled acceptance: every root-to-node path tested node by node with
-    Python-float softmaxes, the correction by a Python-loop race over scalar
-    Philox words.
+  * sampled acceptance: each node's test and its siblings' evaluated on
+    their own, every root-to-node path checked for being taken end to end
+    (no walk), Python-float softmaxes, the correction by a Python-loop race
+    over scalar Philox words.
 """
 from __future__ import annotations
 
@@ -218,53 +219,57 @@ def _softmax_list(row, T):
     return [x / s for x in e]
 
 
-def accept_sampled(logits, draft_logits, draft_tok, parent, u_accept, seed, T, Dmax):
-    """Sampled tree acceptance by enumerating every root-to-node path and
-    testing each of its draft nodes with Python floats; the correction token
-    by a Python-loop exponential race over scalar Philox words."""
+def accept_sampled(logits, draft_tok, parent, u_accept, seed, T, Dmax):
+    """Sampled tree acceptance, checked path by path: a node is taken from
+    its parent when its own test passes and no earlier sibling's does (each
+    sibling's test against the mass its earlier siblings' distinct tokens
+    left, in Python floats); the result is the longest root-to-node path made
+    only of taken nodes.  The correction token by a Python-loop exponential
+    race over scalar Philox words, with the end node's child tokens removed."""
     from .philox import philox4x32, uniform_open
     B, N = len(parent), len(parent[0])
-    V, Nd = len(logits[0][0]), len(draft_logits[0])
+    V = len(logits[0][0])
     out_len, out_path, out_corr = [], [], []
     for b in range(B):
         par = [int(x) for x in parent[b]]
         if not _valid_tree(par):
             out_len.append(-1); out_path.append([-1] * Dmax); out_corr.append(-1)
             continue
-        paths = [_root_path(par, i) for i in range(N)]
-        if max(len(pth) for pth in paths) - 1 > Nd:
+        probs = [_softmax_list(logits[b][v], T) for v in range(N)]
+        passes = [False] * N
+        for c in range(1, N):
+            sibs = [j for j in range(1, c) if par[j] == par[c]]
+            seen, mass = [], 0.0
+            for j in sibs:
+                yj = int(draft_tok[b][j])
+                if 0 <= yj < V and yj not in seen:
+                    seen.append(yj)
+                    mass += probs[par[c]][yj]
+            y = int(draft_tok[b][c])
+            e = probs[par[c]][y] if 0 <= y < V and y not in seen else 0.0
+            passes[c] = float(u_accept[b][c]) * (1.0 - mass) < e
+        taken = [c > 0 and passes[c] and not any(passes[j] for j in range(1, c)
+                                                  if par[j] == par[c]) for c in range(N)]
+        best = [0]
+        for i in range(1, N):
+            pth = _root_path(par, i)
+            if all(taken[x] for x in pth[1:]) and len(pth) > len(best):
+                best = pth
+        if len(best) > Dmax:
             out_len.append(-1); out_path.append([-1] * Dmax); out_corr.append(-1)
             continue
-        best = None
-        for i, pth in enumerate(paths):
-            ok = True
-            for d in range(1, len(pth)):
-                node, up = pth[d], pth[d - 1]
-                y = int(draft_tok[b][node])
-                pu = _softmax_list(logits[b][up], T)[y]
-                qd = _softmax_list(draft_logits[b][d - 1], T)[y]
-                ok = ok and float(u_accept[b][node]) * qd < pu
-            if ok and (best is None or len(pth) > len(paths[best])):
-                best = i
-        pth = paths[best]
-        if len(pth) > Dmax:
-            out_len.append(-1); out_path.append([-1] * Dmax); out_corr.append(-1)
-            continue
-        pv = _softmax_list(logits[b][best], T)
-        if any(par[i] == best for i in range(1, N)):
-            qn = _softmax_list(draft_logits[b][len(pth) - 1], T)
-            w = [max(a - c, 0.0) for a, c in zip(pv, qn)]
-        else:
-            w = pv
+        end = best[-1]
+        kids = {int(draft_tok[b][c]) for c in range(1, N) if par[c] == end}
+        w = [0.0 if x in kids else probs[end][x] for x in range(V)]
         if not any(x > 0 for x in w):
-            w = pv
+            w = probs[end]
         tok, top = -1, -1.0
         for x in range(V):
             word = philox4x32((x // 4, b, 0, 0), (seed & 0xFFFFFFFF, seed >> 32))[x % 4]
             race = w[x] / -math.log(uniform_open(word)) if w[x] > 0 else -1.0
             if race > top:
                 tok, top = x, race
-        out_len.append(len(pth))
-        out_path.append(pth + [-1] * (Dmax - len(pth)))
+        out_len.append(len(best))
+        out_path.append(best + [-1] * (Dmax - len(best)))
         out_corr.append(tok)
     return np.array(out_len), np.array(out_path), np.array(out_corr)

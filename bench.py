@@ -704,18 +704,18 @@ def run_extras(torch, w, inp, args, dev, R, reps, parent, kv_len, draft_d, outs,
         commit_path(reps[r]["kt"], reps[r]["vt"], path, acc_len, ckc, cvc, ckl)
 
     # Non-greedy (T = 1) acceptance of the same trees: the target logits of
-    # the replica, the draft head's logits, one uniform per node.
+    # the replica, one uniform per node.
     u_acc = torch.from_numpy(np.random.default_rng(w.seed + 5).random(
         (w.B, w.N), dtype=np.float32)).to(dev)
     s_len = torch.empty(w.B, dtype=torch.int32, device=dev)
     s_path = torch.empty(w.B, w.Dmax, dtype=torch.int32, device=dev)
     s_corr = torch.empty(w.B, dtype=torch.int32, device=dev)
-    ws_samp = torch.zeros(lib.tv_tree_accept_sampled_workspace(w.B, w.N, w.V, w.depth),
+    ws_samp = torch.zeros(lib.tv_tree_accept_sampled_workspace(w.B, w.N, w.V),
                           dtype=torch.uint8, device=dev)
 
     def sampled(r):
-        tree_accept_sampled(reps[r]["logits"], dlogs[r], draft_d, parent, u_acc, 1234 + r, 1.0,
-                            w.Dmax, accept_len=s_len, path=s_path, correction=s_corr,
+        tree_accept_sampled(reps[r]["logits"], draft_d, parent, u_acc, 1234 + r, 1.0, w.Dmax,
+                            accept_len=s_len, path=s_path, correction=s_corr,
                             workspace_tensor=ws_samp)
 
     # The practical floor of a streaming kernel at this size: a plain device
@@ -749,9 +749,9 @@ def run_extras(torch, w, inp, args, dev, R, reps, parent, kv_len, draft_d, outs,
     torch.cuda.synchronize()
     paged_same = bool(torch.equal(outs[0].view(torch.int16), ref0.view(torch.int16)))
     esz = 4 if w.logits_dtype == "f32" else 2
-    # target logits + draft logits read once, plus two rows per sequence for
-    # the correction race
-    samp_bytes = (w.B * (w.N + w.depth) + 2 * w.B) * w.V * esz
+    # target logits read once, plus the last node's row again for the
+    # correction race
+    samp_bytes = (w.B * w.N + w.B) * w.V * esz
     ms_commit = max(0.0, ms["commit"] - ms["reset"])
     out = {
         "draft_topw_us": ms["topw"] * 1e3, "build_tree_us": ms["build"] * 1e3,

@@ -316,45 +316,48 @@ int tv_build_tree(const int32_t* tok, const float* logp, const int32_t* root_tok
 /*
  * Non-greedy (temperature) tree acceptance (Sec. 2.4: the speculative
  * sampling rule applied along the tree's branches, with a correction token
- * drawn from the target when a draft is rejected).
+ * drawn from the target when the drafts are rejected), in the form that
+ * keeps verification lossless (Sec. 2.2) for trees whose children are
+ * deterministic drafts (top-W per depth, as tv_build_tree makes them).
  *
- * With p_u = softmax(logits[b, u] / T) the target's next-token distribution
- * at node u and q_d = softmax(draft_logits[b, d - 1] / T) the draft head's
- * distribution of depth-d tokens, draft node i (token y, parent u, depth d)
- * passes its test when u_accept[b, i] * q_d(y) < p_u(y), i.e.
- * u_accept < min(1, p/q).  It is accepted when it passes and its parent is
- * accepted; the root always is.  The deepest accepted node v (lowest index
- * among equally deep ones) gives path and accept_len exactly as in
- * tv_tree_accept.  correction[b] is drawn at v from the residual
- * max(0, p_v - q_{d(v)+1}) (normalised) when v has children, from p_v when
- * it has none or the residual is all zero: the token x maximising
- * w(x) / -ln U(b, x), ties to the lower index, where U(b, x) takes word x % 4
- * of Philox4x32-10 (Salmon et al., SC 2011) with counter (x / 4, b, 0, 0)
- * and key (seed & 0xFFFFFFFF, seed >> 32), mapped to (0, 1) as
- * ((word >> 9) + 0.5) / 2^23.
+ * With p_v = softmax(logits[b, v] / T) the target's next-token
+ * distribution at node v, a walk starts at the root.  At the current node v
+ * the children c of v are tested in increasing index order: c (token y)
+ * passes when u_accept[b, c] * (1 - S) < e, where e = p_v(y) if y is in
+ * [0, V) and no earlier child of v has token y, else e = 0, and S is the
+ * sum of p_v over the distinct tokens of v's earlier children.  (Each child
+ * is a point-mass proposal; the test is u < min(1, p'(y)) for the target
+ * residual p' left by the rejected ones.)  The first child that passes
+ * becomes the current node.  The walk ends at a node none of whose children
+ * passes: path and accept_len describe the walk as in tv_tree_accept.
+ * correction[b] is drawn at the last node v from p_v with the tokens of v's
+ * children removed (from p_v when that leaves no mass): the token x
+ * maximising w(x) / -ln U(b, x), ties to the lower index, where U(b, x)
+ * takes word x % 4 of Philox4x32-10 (Salmon et al., SC 2011) with counter
+ * (x / 4, b, 0, 0) and key (seed & 0xFFFFFFFF, seed >> 32), mapped to (0, 1)
+ * as ((word >> 9) + 0.5) / 2^23.  With uniforms drawn independently on
+ * [0, 1), the first emitted token (accepted draft or correction) follows p
+ * at the root, and the walk ends at v with probability (product of p along
+ * v's root path) x (1 - sum of p_v over v's distinct child tokens).
  *
- *   logits       [B, N, V]  bf16 or fp32 (logits_dtype)  target logits
- *   draft_logits [B, Nd, V] bf16 or fp32 (draft_dtype)   draft-head logits,
- *                           row d - 1 for depth d
+ *   logits     [B, N, V]  bf16 or fp32 (logits_dtype)  target logits
  *   draft_tok, parent [B, N] int32, as in tv_tree_accept
- *   u_accept     [B, N] fp32 uniforms in [0, 1) (entry 0 of a row unused)
+ *   u_accept   [B, N] fp32 uniforms in [0, 1) (entry 0 of a row unused)
  *   accept_len [B], path [B, Dmax], correction [B] int32 outputs; an invalid
- *     tree, one deeper than Nd, or a path longer than Dmax gives -1, a -1
- *     path and correction -1.
+ *     tree or a path longer than Dmax gives -1, a -1 path and correction -1.
  *
  * Requirements: temperature > 0 and finite; 1 <= N <= TV_MAX_NODES,
- * 1 <= Nd <= TV_MAX_DRAFT_DEPTH, V >= 1, Dmax >= 1, B*N <= 2^24; logits
- * finite.  Workspace: tv_tree_accept_sampled_workspace(B, N, V, Nd) bytes,
+ * 1 <= V <= 2^23 (TV_ERR_UNSUPPORTED above), Dmax >= 1, B*N <= 2^24; logits
+ * finite.  Workspace: tv_tree_accept_sampled_workspace(B, N, V) bytes,
  * 16-byte aligned (needs no zero fill).  The decisions are taken in fp32:
  * a test within about 1e-6 (relative) of its threshold may go either way.
  */
-size_t tv_tree_accept_sampled_workspace(int B, int N, int V, int Nd);
-int tv_tree_accept_sampled(const void* logits, int logits_dtype, const void* draft_logits,
-                           int draft_dtype, const int32_t* draft_tok, const int32_t* parent,
-                           const float* u_accept, unsigned long long seed, float temperature,
-                           int B, int N, int V, int Nd, int Dmax, int32_t* accept_len,
-                           int32_t* path, int32_t* correction, void* workspace,
-                           size_t workspace_bytes, hipStream_t stream);
+size_t tv_tree_accept_sampled_workspace(int B, int N, int V);
+int tv_tree_accept_sampled(const void* logits, int logits_dtype, const int32_t* draft_tok,
+                           const int32_t* parent, const float* u_accept,
+                           unsigned long long seed, float temperature, int B, int N, int V,
+                           int Dmax, int32_t* accept_len, int32_t* path, int32_t* correction,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -70,10 +70,10 @@ def load_library() -> ctypes.CDLL:
         lib.tv_block_causal_attention.argtypes = (
             [vp] * 5 + [i32p, vp] + [ci] * 7 + [ctypes.c_float, vp, sz, vp])
         lib.tv_tree_accept_sampled_workspace.restype = sz
-        lib.tv_tree_accept_sampled_workspace.argtypes = [ci] * 4
+        lib.tv_tree_accept_sampled_workspace.argtypes = [ci] * 3
         lib.tv_tree_accept_sampled.restype = ci
         lib.tv_tree_accept_sampled.argtypes = (
-            [vp, ci, vp, ci, i32p, i32p, vp, ctypes.c_ulonglong, ctypes.c_float] + [ci] * 5
+            [vp, ci, i32p, i32p, vp, ctypes.c_ulonglong, ctypes.c_float] + [ci] * 4
             + [i32p, i32p, i32p, vp, sz, vp])
         lib.tv_commit_path.restype = ci
         lib.tv_commit_path.argtypes = [vp, vp, i32p, i32p, vp, vp, i32p] + [ci] * 6 + [vp]
@@ -256,18 +256,17 @@ def _dtype_code(t, name):
     raise ValueError(f"{name} must be bfloat16 or float32, got {t.dtype}")
 
 
-def tree_accept_sampled(logits, draft_logits, draft_tok, parent, u_accept, seed, temperature,
-                        Dmax, accept_len=None, path=None, correction=None, workspace_tensor=None):
-    """Non-greedy tree acceptance.  logits [B,N,V], draft_logits [B,Nd,V]
-    (bf16 or fp32), draft_tok/parent [B,N] int32, u_accept [B,N] fp32.
-    Returns (accept_len [B], path [B,Dmax], correction [B]) int32."""
+def tree_accept_sampled(logits, draft_tok, parent, u_accept, seed, temperature, Dmax,
+                        accept_len=None, path=None, correction=None, workspace_tensor=None):
+    """Non-greedy tree acceptance (lossless multi-candidate rule for
+    deterministic children).  logits [B,N,V] bf16 or fp32, draft_tok/parent
+    [B,N] int32, u_accept [B,N] fp32.  Returns (accept_len [B], path
+    [B,Dmax], correction [B]) int32."""
     lib = load_library()
     B, N, V = logits.shape
-    Nd = draft_logits.shape[1]
     dev = logits.device
-    dt, ddt = _dtype_code(logits, "logits"), _dtype_code(draft_logits, "draft_logits")
+    dt = _dtype_code(logits, "logits")
     _need(logits, "logits", logits.dtype, (B, N, V), dev)
-    _need(draft_logits, "draft_logits", draft_logits.dtype, (B, Nd, V), dev)
     _need(draft_tok, "draft_tok", torch.int32, (B, N), dev)
     _need(parent, "parent", torch.int32, (B, N), dev)
     _need(u_accept, "u_accept", torch.float32, (B, N), dev)
@@ -281,15 +280,15 @@ def tree_accept_sampled(logits, draft_logits, draft_tok, parent, u_accept, seed,
     _need(path, "path", torch.int32, (B, Dmax), dev)
     _need(correction, "correction", torch.int32, (B,), dev)
     stream = torch.cuda.current_stream(dev).cuda_stream
-    need = lib.tv_tree_accept_sampled_workspace(B, N, V, Nd)
+    need = lib.tv_tree_accept_sampled_workspace(B, N, V)
     if need == 0:
         _check(-2)
     ws = workspace_tensor if workspace_tensor is not None else workspace("sample", need, dev,
                                                                          stream)
     _check(lib.tv_tree_accept_sampled(
-        _ptr(logits), dt, _ptr(draft_logits), ddt, _ptr(draft_tok), _ptr(parent), _ptr(u_accept),
+        _ptr(logits), dt, _ptr(draft_tok), _ptr(parent), _ptr(u_accept),
         ctypes.c_ulonglong(int(seed) & 0xFFFFFFFFFFFFFFFF), ctypes.c_float(temperature), B, N, V,
-        Nd, Dmax, _ptr(accept_len), _ptr(path), _ptr(correction), _ptr(ws), ws.numel(),
+        Dmax, _ptr(accept_len), _ptr(path), _ptr(correction), _ptr(ws), ws.numel(),
         ctypes.c_void_p(stream)))
     return accept_len, path, correction
 

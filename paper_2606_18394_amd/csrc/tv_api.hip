@@ -27,11 +27,10 @@ hipError_t launch_accept(const void* logits, int f32, const int32_t* draft, cons
                          int32_t* tgt_out, void* ws, hipStream_t st);
 hipError_t launch_topw(const void* logits, int f32, int B, int Nd, int V, int W, int32_t* tok,
                        float* logp, void* ws, hipStream_t st);
-hipError_t launch_sample(const void* logits, int f32t, const void* dlogits, int f32d,
-                         const int32_t* draft, const int32_t* parent, const float* u,
-                         unsigned long long seed, float temperature, int B, int N, int V, int Nd,
-                         int Dmax, int32_t* accept_len, int32_t* path, int32_t* corr, void* ws,
-                         hipStream_t st);
+hipError_t launch_sample(const void* logits, int f32, const int32_t* draft,
+                         const int32_t* parent, const float* u, unsigned long long seed,
+                         float temperature, int B, int N, int V, int Dmax, int32_t* accept_len,
+                         int32_t* path, int32_t* corr, void* ws, hipStream_t st);
 hipError_t launch_build_tree(const int32_t* tok, const float* logp, const int32_t* root_tok, int B,
                              int Nd, int W, int budget, int32_t* parent, int32_t* token,
                              int32_t* depth, float* score, int32_t* n_nodes, hipStream_t st);
@@ -109,7 +108,7 @@ const char* tv_status_string(int status) {
   }
 }
 
-int tv_version(void) { return 1; }
+int tv_version(void) { return 2; }
 
 size_t tv_tree_verify_attention_workspace(int B, int N, int Hq, int Hkv, int D, int Lmax) {
   if (check_attention_sizes(B, N, Hq, Hkv, D, Lmax) != TV_OK) return 0;
@@ -318,41 +317,35 @@ int tv_tree_accept_noalloc(const void* logits, int logits_dtype, const int32_t* 
   return e == hipSuccess ? TV_OK : TV_ERR_LAUNCH;
 }
 
-static int check_sampled_sizes(int B, int N, int V, int Nd, int Dmax) {
+static int check_sampled_sizes(int B, int N, int V, int Dmax) {
   const int rc = check_accept_sizes(B, N, V, Dmax);
   if (rc != TV_OK) return rc;
-  if (Nd < 1) return TV_ERR_SHAPE;
-  if (Nd > TV_MAX_DRAFT_DEPTH) return TV_ERR_UNSUPPORTED;
+  if ((long long)V > tv::kMaxSampledVocab) return TV_ERR_UNSUPPORTED;
   return TV_OK;
 }
 
-size_t tv_tree_accept_sampled_workspace(int B, int N, int V, int Nd) {
-  if (check_sampled_sizes(B, N, V, Nd, 1) != TV_OK) return 0;
-  return tv::sample_plan(B, N, V, Nd).ws_bytes;
+size_t tv_tree_accept_sampled_workspace(int B, int N, int V) {
+  if (check_sampled_sizes(B, N, V, 1) != TV_OK) return 0;
+  return tv::sample_plan(B, N, V).ws_bytes;
 }
 
-int tv_tree_accept_sampled(const void* logits, int logits_dtype, const void* draft_logits,
-                           int draft_dtype, const int32_t* draft_tok, const int32_t* parent,
-                           const float* u_accept, unsigned long long seed, float temperature,
-                           int B, int N, int V, int Nd, int Dmax, int32_t* accept_len,
+int tv_tree_accept_sampled(const void* logits, int logits_dtype, const int32_t* draft_tok,
+                           const int32_t* parent, const float* u_accept, unsigned long long seed,
+                           float temperature, int B, int N, int V, int Dmax, int32_t* accept_len,
                            int32_t* path, int32_t* correction, void* workspace,
                            size_t workspace_bytes, hipStream_t stream) {
-  int rc = check_sampled_sizes(B, N, V, Nd, Dmax);
+  int rc = check_sampled_sizes(B, N, V, Dmax);
   if (rc != TV_OK) return rc;
   if (!(temperature > 0.f) || !(temperature < INFINITY)) return TV_ERR_SHAPE;
-  if ((logits_dtype != TV_BF16 && logits_dtype != TV_F32) ||
-      (draft_dtype != TV_BF16 && draft_dtype != TV_F32))
-    return TV_ERR_DTYPE;
-  if (!logits || !draft_logits || !draft_tok || !parent || !u_accept || !accept_len || !path ||
-      !correction)
+  if (logits_dtype != TV_BF16 && logits_dtype != TV_F32) return TV_ERR_DTYPE;
+  if (!logits || !draft_tok || !parent || !u_accept || !accept_len || !path || !correction)
     return TV_ERR_NULL;
-  const tv::SamplePlan p = tv::sample_plan(B, N, V, Nd);
+  const tv::SamplePlan p = tv::sample_plan(B, N, V);
   if (!workspace || workspace_bytes < p.ws_bytes) return TV_ERR_WORKSPACE;
   if (misaligned(workspace)) return TV_ERR_ALIGN;
-  hipError_t e = tv::launch_sample(logits, logits_dtype == TV_F32, draft_logits,
-                                   draft_dtype == TV_F32, draft_tok, parent, u_accept, seed,
-                                   temperature, B, N, V, Nd, Dmax, accept_len, path, correction,
-                                   workspace, stream);
+  hipError_t e = tv::launch_sample(logits, logits_dtype == TV_F32, draft_tok, parent, u_accept,
+                                   seed, temperature, B, N, V, Dmax, accept_len, path,
+                                   correction, workspace, stream);
   return e == hipSuccess ? TV_OK : TV_ERR_LAUNCH;
 }
 

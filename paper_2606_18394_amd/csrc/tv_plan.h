@@ -250,6 +250,7 @@ inline size_t accept_ws_bytes(int B, int N) {
 // and its W best (value, token) pairs; a second kernel merges the splits of
 // each row.  Splits as in the acceptance scan.
 constexpr int kTopwMax = 16;             // largest branching width W
+constexpr int kMaxDraftDepth = 64;       // == TV_MAX_DRAFT_DEPTH
 constexpr size_t kTopwPartBytes = 8 + 8 * kTopwMax;
 
 struct TopwPlan {
@@ -280,13 +281,15 @@ inline size_t topw_ws_bytes(int B, int Nd) {
   return (size_t)(rows * accept_split_cap(rows)) * kTopwPartBytes;
 }
 
-// Non-greedy acceptance: an lse scan over the B*N target rows and B*Nd
-// draft rows (splits as in the acceptance scan, in vocabulary entries that
-// are multiples of 8), then one workgroup per (sequence, race split) that
-// repeats the acceptance and races its vocabulary slice (about 512
-// workgroups in all, at least 8 entries per thread).
-constexpr int kMaxDraftDepth = 64;       // == TV_MAX_DRAFT_DEPTH
+// Non-greedy acceptance: an lse scan over the B*N target rows (splits as
+// in the acceptance scan, in vocabulary entries that are multiples of 8),
+// then one workgroup per (sequence, race split) that repeats the tests and
+// races its vocabulary slice (about 512 workgroups in all, at least 8
+// entries per thread, at most kRaceSlice entries so that the slice's token
+// mask fits in LDS).
 constexpr int kMaxRaceSplit = 64;
+constexpr long long kRaceSlice = 131072;
+constexpr long long kMaxSampledVocab = kRaceSlice * kMaxRaceSplit;
 
 struct SamplePlan {
   int nsplit, nrace, lse_grid;
@@ -294,9 +297,9 @@ struct SamplePlan {
   size_t race_bytes, ws_bytes;
 };
 
-inline SamplePlan sample_plan(int B, int N, int V, int Nd) {
+inline SamplePlan sample_plan(int B, int N, int V) {
   SamplePlan p{};
-  const long long rows = (long long)B * (N + Nd);
+  const long long rows = (long long)B * N;
   long long ns = accept_split_cap(rows);
   const long long per_round = (long long)kScanThreads * kScanLoadsPerThread * 8;
   const long long by_size = ((long long)V + per_round - 1) / per_round;
@@ -308,6 +311,8 @@ inline SamplePlan sample_plan(int B, int N, int V, int Nd) {
   long long nr = (512 + B - 1) / B;
   const long long by_v = ((long long)V + 8 * 256 - 1) / (8 * 256);
   if (nr > by_v) nr = by_v;
+  const long long by_mask = ((long long)V + kRaceSlice - 1) / kRaceSlice;
+  if (nr < by_mask) nr = by_mask;
   if (nr > kMaxRaceSplit) nr = kMaxRaceSplit;
   if (nr < 1) nr = 1;
   p.rps = ((V + nr - 1) / nr + 7) / 8 * 8;

@@ -1,29 +1,38 @@
-// Non-greedy tree acceptance (temperature T > 0) for CDNA4 (gfx950): the
-// speculative sampling test of every draft node, the deepest accepted path,
-// and the correction token drawn at its last node (Sec. 2.4).
+// Non-greedy tree acceptance (temperature T > 0) for CDNA4 (gfx950).
 //
-// With p_u = softmax(logits[u] / T) and q_d = softmax(draft_logits[d-1] / T),
-// draft node i (token y, parent u, depth d) passes when
-// u_i * q_d(y) < p_u(y), i.e. u_i < min(1, p/q); it is accepted when it
-// passes and its parent is accepted.  The correction token at the deepest
-// accepted node v comes from max(0, p_v - q_{d(v)+1}) when v has children
-// (all of them rejected), else from p_v (an all-zero residual falls back to
-// p_v too), by an exponential race: the winner is argmax w(x) / E_x with
-// E_x = -ln U(b, x), U from Philox4x32-10 (Salmon et al., SC 2011) on the
-// counter (x / 4, b, 0, 0) and the 64-bit seed as key, word x % 4, mapped
-// to (0, 1) by its top 23 bits.
+// The speculative sampling rule (Sec. 2.4) applied to a tree whose
+// children are deterministic drafts (top-W, Alg. 1): each child's proposal
+// is the point mass at its token, so the children of the current node v are
+// tested in index order against the target residual left by the rejected
+// ones -- child c (token y) passes when u_c * (1 - S) < e_c, with
+// e_c = p_v(y) for a valid token not already rejected at v and 0 otherwise,
+// and S the mass of v's earlier children's distinct tokens -- and the first
+// child that passes is followed.  This keeps verification lossless
+// (Sec. 2.2).  The walk ends at a node none of whose children passes; the
+// correction token is drawn there from p_v without its children's tokens
+// (from p_v when that leaves no mass), by an exponential race: the winner
+// is argmax w(x) / E_x with E_x = -ln U(b, x), U from Philox4x32-10 (Salmon
+// et al., SC 2011) on the counter (x / 4, b, 0, 0) and the 64-bit seed as
+// key, word x % 4, mapped to (0, 1) by its top 23 bits.
+//
+// The walk needs no sequential descent: whether child c passes depends only
+// on its earlier siblings, so every node's test is taken at once, a node is
+// selected when it passes and no earlier sibling does (an LDS atomicMin per
+// parent), and the walk is the chain of nodes whose whole root path is
+// selected (an AND over root paths by pointer jumping).
 //
 // Three kernels:
-//   lse_scan: one workgroup per (row, vocabulary split) over the B*N target
-//     rows and the B*Nd draft rows: running (max, sum of exponentials) of
-//     x / T per thread, merged across the workgroup.
+//   lse_scan: one workgroup per (node row, vocabulary split): running
+//     (max, sum of exponentials) of x / T per thread, merged across the
+//     workgroup.
 //   sample_accept: one workgroup per (sequence, vocabulary split).  Each
-//     merges the log-sum-exps of its sequence, runs the acceptance (depths,
-//     then the root-path AND of the tests, both by pointer jumping) and
-//     races its vocabulary slice for the correction token, keeping two
-//     keys: the residual race and the plain p_v race.  Split 0 writes the
-//     path.  Every workgroup of a sequence repeats the acceptance, which
-//     costs less than a kernel boundary between acceptance and race.
+//     merges the log-sum-exps of its sequence, takes every node's test,
+//     finds the walk's last node and races its vocabulary slice for the
+//     correction token with that node's child tokens masked by an LDS
+//     bitmap, keeping two keys: the residual race and the plain p_v race.
+//     Split 0 writes the path.  Every workgroup of a sequence repeats the
+//     tests, which costs less than a kernel boundary between them and the
+//     race.
 //   sample_finish: one wave per sequence merges the race keys.
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -35,7 +44,6 @@ namespace tv {
 
 struct SampleArgs {
   const void* logits;   // [B, N, V] target
-  const void* dlogits;  // [B, Nd, V] draft head, row d - 1 = depth d
   const int32_t* draft;
   const int32_t* parent;
   const float* u;       // [B, N] acceptance uniforms
@@ -43,12 +51,12 @@ struct SampleArgs {
   int32_t* path;
   int32_t* corr;
   unsigned long long* race;  // [B, nrace, 2] race keys
-  float2* lse_part;          // [B*N + B*Nd, nsplit] (max, sum exp) of x / T
+  float2* lse_part;          // [B*N, nsplit] (max, sum exp) of x / T
   unsigned int seed_lo, seed_hi;
   float invT;
-  int B, N, V, Nd, Dmax, nsplit, nrace;
+  int B, N, V, Dmax, nsplit, nrace;
   long long eps;  // vocabulary entries per lse split, a multiple of 8
-  long long rps;  // vocabulary entries per race split, a multiple of 8
+  long long rps;  // vocabulary entries per race split, a multiple of 8, <= kRaceSlice
 };
 
 // ------------------------------------------------------------ generator
@@ -192,21 +200,15 @@ __device__ __forceinline__ void lse_slice(const void* rowp, long long x0, long l
   }
 }
 
-template <bool F32T, bool F32D>
+template <bool F32>
 __global__ __launch_bounds__(kScanThreads) void lse_scan(SampleArgs a, int vec) {
   const int row = blockIdx.x / a.nsplit, split = blockIdx.x % a.nsplit;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int trows = a.B * a.N;
   const long long x0 = (long long)split * a.eps;
   const long long x1 = x0 + a.eps < a.V ? x0 + a.eps : a.V;
   float m = -INFINITY, s = 0.f;
-  if (row < trows) {
-    const char* rowp = (const char*)a.logits + (size_t)row * a.V * (F32T ? 4 : 2);
-    lse_slice<F32T>(rowp, x0, x1, vec != 0, a.invT, m, s);
-  } else {
-    const char* rowp = (const char*)a.dlogits + (size_t)(row - trows) * a.V * (F32D ? 4 : 2);
-    lse_slice<F32D>(rowp, x0, x1, vec != 0, a.invT, m, s);
-  }
+  const char* rowp = (const char*)a.logits + (size_t)row * a.V * (F32 ? 4 : 2);
+  lse_slice<F32>(rowp, x0, x1, vec != 0, a.invT, m, s);
   __shared__ float rm[kScanThreads / 64], rs[kScanThreads / 64];
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) lse_merge2(m, s, __shfl_xor(m, o), __shfl_xor(s, o));
@@ -227,116 +229,120 @@ __global__ __launch_bounds__(kScanThreads) void lse_scan(SampleArgs a, int vec) 
 
 constexpr int kSampleThreads = 512;
 constexpr int kNodesPerThread = kMaxNodes / kSampleThreads;
+static_assert(kMaxNodes % kSampleThreads == 0, "whole node batches per thread");
 
-template <bool F32T, bool F32D>
+template <bool F32>
 __global__ __launch_bounds__(kSampleThreads) void sample_accept(SampleArgs a, int vec) {
   __shared__ float lse_t[kMaxNodes];
-  __shared__ float lse_d[kMaxDraftDepth];
+  __shared__ float ef[kMaxNodes];        // effective mass of each node's token at its parent
+  __shared__ int tokl[kMaxNodes];
+  __shared__ int first_pass[kMaxNodes];  // per parent: lowest passing child
   __shared__ short par[kMaxNodes], jmp0[kMaxNodes], jmp1[kMaxNodes], dep0[kMaxNodes],
       dep1[kMaxNodes];
   __shared__ unsigned char ok0[kMaxNodes], ok1[kMaxNodes];
+  __shared__ unsigned int mask[kRaceSlice / 32];  // child tokens of the last node, this slice
   __shared__ unsigned int best_key;
   __shared__ unsigned long long red[2][kSampleThreads / 64];
 
   const int b = blockIdx.x / a.nrace, sp = blockIdx.x % a.nrace;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int N = a.N, Nd = a.Nd, V = a.V;
+  const int N = a.N, V = a.V;
 
   // ---- tree, tokens, log-sum-exps
   int bad = 0;
-  int tok[kNodesPerThread];
 #pragma unroll
   for (int k = 0; k < kNodesPerThread; ++k) {
     const int i = tid + kSampleThreads * k;
-    tok[k] = 0;
     if (i < N) {
       const int p = a.parent[(size_t)b * N + i];
       const int badi = (i == 0) ? (p != -1) : (p < 0 || p >= i);
       bad |= badi;
       par[i] = (short)(badi || i == 0 ? 0 : p);
-      tok[k] = a.draft[(size_t)b * N + i];
+      tokl[i] = a.draft[(size_t)b * N + i];
+      first_pass[i] = 0x7FFFFFFF;
+      const size_t row = (size_t)b * N + i;
+      float m = -INFINITY, s = 0.f;
+      for (int q = 0; q < a.nsplit; ++q) {
+        const float2 ps = a.lse_part[row * a.nsplit + q];
+        lse_merge2(m, s, ps.x, ps.y);
+      }
+      lse_t[i] = m + __logf(s);
     }
-  }
-  for (int r = tid; r < N + Nd; r += kSampleThreads) {
-    const size_t row = r < N ? (size_t)b * N + r : (size_t)a.B * N + (size_t)b * Nd + (r - N);
-    float m = -INFINITY, s = 0.f;
-    for (int k = 0; k < a.nsplit; ++k) {
-      const float2 ps = a.lse_part[row * a.nsplit + k];
-      lse_merge2(m, s, ps.x, ps.y);
-    }
-    const float l = m + __logf(s);
-    if (r < N) lse_t[r] = l;
-    else lse_d[r - N] = l;
   }
   if (tid == 0) best_key = 0u;
   bad = __syncthreads_or(bad);
 
   int len = -1, v = 0, dv = 0;
-  if (!bad && N <= 64) {
-    // Trees of at most 64 nodes: wave 0 alone, lane i holding node i, with
-    // lane exchanges in place of LDS rounds and workgroup barriers.  Every
-    // lane of the wave takes part in each exchange.
-    __shared__ int s_res[3];
-    if (wave == 0) {
-      const int i = lane;
-      const bool node = i < N;
-      const int pp = node && i > 0 ? par[i] : 0;  // the root jumps to itself
-      int jmp = pp, dep = node && i > 0 ? 1 : 0;
-      for (int r = 0; r < 6 && __any(jmp != 0); ++r) {
-        dep += __shfl(dep, jmp);
-        jmp = __shfl(jmp, jmp);
-      }
-      const bool deep = __any(node && dep > Nd);
-      int ok = node ? 1 : 0;
-      if (node && i > 0 && dep <= Nd) {
-        const int y = tok[0];
-        ok = 0;
-        if (y >= 0 && y < V) {
-          const float pl = load_logit<F32T>(a.logits, ((size_t)b * N + pp) * V + y);
-          const float ql = load_logit<F32D>(a.dlogits, ((size_t)b * Nd + dep - 1) * V + y);
-          const float p = __expf(pl * a.invT - lse_t[pp]);
-          const float q = __expf(ql * a.invT - lse_d[dep - 1]);
-          ok = a.u[(size_t)b * N + i] * q < p;
-        }
-      }
-      jmp = pp;
-      for (int r = 0; r < 6 && __any(jmp != 0); ++r) {
-        ok &= __shfl(ok, jmp);
-        jmp = __shfl(jmp, jmp);
-      }
-      unsigned int k = ok ? ((unsigned int)dep << 16) | (0xFFFFu - (unsigned int)i) : 0u;
+  if (!bad) {
+    // e: p at the parent of each node's token (0 for a token outside [0, V))
+    float e[kNodesPerThread];
 #pragma unroll
-      for (int o = 32; o >= 1; o >>= 1) {
-        const unsigned int other = __shfl_xor(k, o);
-        k = other > k ? other : k;
+    for (int k = 0; k < kNodesPerThread; ++k) {
+      const int i = tid + kSampleThreads * k;
+      e[k] = 0.f;
+      if (i >= 1 && i < N) {
+        const int y = tokl[i], u = par[i];
+        if (y >= 0 && y < V)
+          e[k] = __expf(load_logit<F32>(a.logits, ((size_t)b * N + u) * V + y) * a.invT -
+                        lse_t[u]);
       }
-      if (lane == 0) {
-        const int d = (int)(k >> 16);
-        s_res[0] = deep || d + 1 > a.Dmax ? -1 : d + 1;
-        s_res[1] = (int)(0xFFFFu - (k & 0xFFFFu));
-        s_res[2] = d;
+    }
+    // a token repeated among a node's children has no mass left after its
+    // first occurrence (children follow their parent: siblings of i lie in
+    // (par[i], i))
+#pragma unroll
+    for (int k = 0; k < kNodesPerThread; ++k) {
+      const int i = tid + kSampleThreads * k;
+      if (i >= 1 && i < N) {
+        const int u = par[i], y = tokl[i];
+        bool dup = false;
+        for (int j = u + 1; j < i && !dup; ++j) dup = par[j] == u && tokl[j] == y;
+        ef[i] = dup ? 0.f : e[k];
       }
     }
     __syncthreads();
-    len = s_res[0];
-    v = s_res[1];
-    dv = s_res[2];
-  } else if (!bad) {
-    // depths by pointer jumping (the root jumps to itself)
-    for (int i = tid; i < N; i += kSampleThreads) {
-      jmp0[i] = par[i];
-      dep0[i] = i == 0 ? 0 : 1;
+    // the test against the residual of the earlier siblings (their masses
+    // summed in index order), then the lowest passing child of each parent
+    unsigned char pass[kNodesPerThread];
+#pragma unroll
+    for (int k = 0; k < kNodesPerThread; ++k) {
+      const int i = tid + kSampleThreads * k;
+      pass[k] = 0;
+      if (i >= 1 && i < N) {
+        const int u = par[i];
+        float S = 0.f;
+        for (int j = u + 1; j < i; ++j)
+          if (par[j] == u) S += ef[j];
+        pass[k] = a.u[(size_t)b * N + i] * (1.f - S) < ef[i];
+        if (pass[k]) atomicMin(&first_pass[u], i);
+      }
     }
     __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kNodesPerThread; ++k) {
+      const int i = tid + kSampleThreads * k;
+      if (i < N) {
+        // the root (par = 0 here) jumps to itself
+        ok0[i] = i == 0 ? 1 : (pass[k] && first_pass[par[i]] == i);
+        jmp0[i] = par[i];
+        dep0[i] = i == 0 ? 0 : 1;
+      }
+    }
+    __syncthreads();
+    // pointer jumping: afterwards dep = depth and ok = every node of the
+    // root path selected; 11 rounds reach the root from any of 2048 nodes
     int cur = 0, more, rounds = 0;
     do {
       const short* jc = cur ? jmp1 : jmp0;
       const short* dc = cur ? dep1 : dep0;
+      const unsigned char* oc = cur ? ok1 : ok0;
       short* jn = cur ? jmp0 : jmp1;
       short* dn = cur ? dep0 : dep1;
+      unsigned char* on = cur ? ok0 : ok1;
       more = 0;
       for (int i = tid; i < N; i += kSampleThreads) {
         const int j = jc[i];
+        on[i] = oc[i] & oc[j];
         dn[i] = dc[i] + dc[j];
         jn[i] = jc[j];
         more |= jc[j] != 0;
@@ -344,61 +350,20 @@ __global__ __launch_bounds__(kSampleThreads) void sample_accept(SampleArgs a, in
       cur ^= 1;
     } while (__syncthreads_or(more) && ++rounds < 16);
     const short* depth = cur ? dep1 : dep0;
-    // the test of every node, then the AND over its root path
-    int deep = 0;
-#pragma unroll
-    for (int k = 0; k < kNodesPerThread; ++k) {
-      const int i = tid + kSampleThreads * k;
-      if (i >= N) break;
-      const int d = depth[i];
-      deep |= d > Nd;
-      unsigned char t = 1;
-      if (i > 0 && d <= Nd) {
-        const int y = tok[k], u = par[i];
-        t = 0;
-        if (y >= 0 && y < V) {
-          const float pl = load_logit<F32T>(a.logits, ((size_t)b * N + u) * V + y);
-          const float ql = load_logit<F32D>(a.dlogits, ((size_t)b * Nd + d - 1) * V + y);
-          const float p = __expf(pl * a.invT - lse_t[u]);
-          const float q = __expf(ql * a.invT - lse_d[d - 1]);
-          t = a.u[(size_t)b * N + i] * q < p;
-        }
+    const unsigned char* acc = cur ? ok1 : ok0;
+    // the selected nodes form one chain from the root: its deepest node
+    unsigned int mk = 0u;
+    for (int i = tid; i < N; i += kSampleThreads)
+      if (acc[i]) {
+        const unsigned int k = ((unsigned int)depth[i] << 16) | (0xFFFFu - (unsigned int)i);
+        mk = mk > k ? mk : k;
       }
-      ok0[i] = t;
-      jmp0[i] = par[i];
-    }
-    bad = __syncthreads_or(deep);  // deeper than the draft logits reach
-    if (!bad) {
-      cur = 0;
-      rounds = 0;
-      do {
-        const short* jc = cur ? jmp1 : jmp0;
-        const unsigned char* oc = cur ? ok1 : ok0;
-        short* jn = cur ? jmp0 : jmp1;
-        unsigned char* on = cur ? ok0 : ok1;
-        more = 0;
-        for (int i = tid; i < N; i += kSampleThreads) {
-          const int j = jc[i];
-          on[i] = oc[i] & oc[j];
-          jn[i] = jc[j];
-          more |= jc[j] != 0;
-        }
-        cur ^= 1;
-      } while (__syncthreads_or(more) && ++rounds < 16);
-      const unsigned char* acc = cur ? ok1 : ok0;
-      unsigned int mk = 0u;
-      for (int i = tid; i < N; i += kSampleThreads)
-        if (acc[i]) {
-          const unsigned int k = ((unsigned int)depth[i] << 16) | (0xFFFFu - (unsigned int)i);
-          mk = mk > k ? mk : k;
-        }
-      atomicMax(&best_key, mk);
-      __syncthreads();
-      const unsigned int bk = best_key;
-      dv = (int)(bk >> 16);
-      v = (int)(0xFFFFu - (bk & 0xFFFFu));
-      len = dv + 1 > a.Dmax ? -1 : dv + 1;
-    }
+    atomicMax(&best_key, mk);
+    __syncthreads();
+    const unsigned int bk = best_key;
+    dv = (int)(bk >> 16);
+    v = (int)(0xFFFFu - (bk & 0xFFFFu));
+    len = dv + 1 > a.Dmax ? -1 : dv + 1;
   }
   if (sp == 0) {
     int32_t* pth = a.path + (size_t)b * a.Dmax;
@@ -421,50 +386,48 @@ __global__ __launch_bounds__(kSampleThreads) void sample_accept(SampleArgs a, in
     return;
   }
 
-  // ---- the race over this split's slice of the vocabulary
-  int child = 0;
-  for (int i = 1 + tid; i < N; i += kSampleThreads) child |= par[i] == v;
-  const bool has_child = __syncthreads_or(child) != 0;
-  const float lv = lse_t[v];
-  const float lq = has_child ? lse_d[dv] : 0.f;
-  const size_t prow = ((size_t)b * N + v) * V;
-  const size_t qrow = ((size_t)b * Nd + dv) * V;
+  // ---- the race over this split's slice of the vocabulary, v's child
+  // tokens (all rejected) masked
   const long long x0 = (long long)sp * a.rps;
   const long long x1 = x0 + a.rps < V ? x0 + a.rps : V;
+  const int words = (int)((x1 - x0 + 31) / 32);
+  for (int k = tid; k < words; k += kSampleThreads) mask[k] = 0u;
+  __syncthreads();
+  for (int i = 1 + tid; i < N; i += kSampleThreads)
+    if (par[i] == v) {
+      const long long y = tokl[i];
+      if (y >= x0 && y < x1)
+        atomicOr(&mask[(y - x0) >> 5], 1u << ((unsigned int)(y - x0) & 31u));
+    }
+  __syncthreads();
+  const float lv = lse_t[v];
+  const size_t prow = ((size_t)b * N + v) * V;
   unsigned long long kres = 0ull, kp = 0ull;
   for (long long xg = x0 + 8ll * tid; xg < x1; xg += 8ll * kSampleThreads) {
-    float pl[8], ql[8];
+    float pl[8];
     if (vec && xg + 8 <= x1) {
-      load8<F32T>(a.logits, prow + xg, pl);
-      if (has_child) load8<F32D>(a.dlogits, qrow + xg, ql);
+      load8<F32>(a.logits, prow + xg, pl);
     } else {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        pl[e] = xg + e < x1 ? load_logit<F32T>(a.logits, prow + xg + e) : -INFINITY;
-        ql[e] = has_child && xg + e < x1 ? load_logit<F32D>(a.dlogits, qrow + xg + e) : 0.f;
-      }
+      for (int e = 0; e < 8; ++e)
+        pl[e] = xg + e < x1 ? load_logit<F32>(a.logits, prow + xg + e) : -INFINITY;
     }
+    // 8 entries from an offset that is a multiple of 8 lie in one mask word
+    const unsigned int mbits = mask[(xg - x0) >> 5] >> ((unsigned int)(xg - x0) & 31u);
     const uint4 r0 = philox4x32_10(make_uint4((unsigned int)(xg >> 2), (unsigned int)b, 0u, 0u),
                                    a.seed_lo, a.seed_hi);
     const uint4 r1 = philox4x32_10(
         make_uint4((unsigned int)(xg >> 2) + 1u, (unsigned int)b, 0u, 0u), a.seed_lo, a.seed_hi);
-    const unsigned int words[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
+    const unsigned int wd[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       if (xg + e >= x1) break;
-      const float inv_e = 1.f / -__logf(open_uniform(words[e]));
       const float p = __expf(pl[e] * a.invT - lv);
-      const unsigned int x = (unsigned int)(xg + e);
       if (p > 0.f) {
-        const unsigned long long k = race_key(p * inv_e, x);
+        const unsigned long long k = race_key(p / -__logf(open_uniform(wd[e])),
+                                              (unsigned int)(xg + e));
         kp = k > kp ? k : kp;
-      }
-      if (has_child) {
-        const float w = p - __expf(ql[e] * a.invT - lq);
-        if (w > 0.f) {
-          const unsigned long long k = race_key(w * inv_e, x);
-          kres = k > kres ? k : kres;
-        }
+        if (!((mbits >> e) & 1u)) kres = k > kres ? k : kres;
       }
     }
   }
@@ -500,37 +463,35 @@ __global__ __launch_bounds__(64) void sample_finish(SampleArgs a) {
   kres = wave_max_key(kres);
   kp = wave_max_key(kp);
   if (lane == 0) {
-    const unsigned long long k = kres ? kres : kp;  // all-zero residual: race on p
+    const unsigned long long k = kres ? kres : kp;  // no residual mass: race on p
     a.corr[b] = a.accept_len[b] < 0 || k == 0ull ? -1 : (int)(0xFFFFFFFFu - (unsigned int)k);
   }
 }
 
 // ------------------------------------------------------------ launch
 
-template <bool F32T, bool F32D>
+template <bool F32>
 static hipError_t launch_sample_t(const SampleArgs& a, const SamplePlan& p, int vec,
                                   hipStream_t st) {
-  hipLaunchKernelGGL((lse_scan<F32T, F32D>), dim3(p.lse_grid), dim3(kScanThreads), 0, st, a, vec);
+  hipLaunchKernelGGL((lse_scan<F32>), dim3(p.lse_grid), dim3(kScanThreads), 0, st, a, vec);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((sample_accept<F32T, F32D>), dim3(a.B * p.nrace), dim3(kSampleThreads), 0,
-                     st, a, vec);
+  hipLaunchKernelGGL((sample_accept<F32>), dim3(a.B * p.nrace), dim3(kSampleThreads), 0, st, a,
+                     vec);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(sample_finish, dim3(a.B), dim3(64), 0, st, a);
   return hipGetLastError();
 }
 
-hipError_t launch_sample(const void* logits, int f32t, const void* dlogits, int f32d,
-                         const int32_t* draft, const int32_t* parent, const float* u,
-                         unsigned long long seed, float temperature, int B, int N, int V, int Nd,
-                         int Dmax, int32_t* accept_len, int32_t* path, int32_t* corr, void* ws,
-                         hipStream_t st) {
-  const SamplePlan p = sample_plan(B, N, V, Nd);
-  const int vec = (uintptr_t)logits % 16 == 0 && (uintptr_t)dlogits % 16 == 0 && V % 8 == 0;
+hipError_t launch_sample(const void* logits, int f32, const int32_t* draft,
+                         const int32_t* parent, const float* u, unsigned long long seed,
+                         float temperature, int B, int N, int V, int Dmax, int32_t* accept_len,
+                         int32_t* path, int32_t* corr, void* ws, hipStream_t st) {
+  const SamplePlan p = sample_plan(B, N, V);
+  const int vec = (uintptr_t)logits % 16 == 0 && V % 8 == 0;
   SampleArgs a;
   a.logits = logits;
-  a.dlogits = dlogits;
   a.draft = draft;
   a.parent = parent;
   a.u = u;
@@ -545,18 +506,12 @@ hipError_t launch_sample(const void* logits, int f32t, const void* dlogits, int 
   a.B = B;
   a.N = N;
   a.V = V;
-  a.Nd = Nd;
   a.Dmax = Dmax;
   a.nsplit = p.nsplit;
   a.nrace = p.nrace;
   a.eps = p.eps;
   a.rps = p.rps;
-  if (f32t) {
-    return f32d ? launch_sample_t<true, true>(a, p, vec, st)
-                : launch_sample_t<true, false>(a, p, vec, st);
-  }
-  return f32d ? launch_sample_t<false, true>(a, p, vec, st)
-              : launch_sample_t<false, false>(a, p, vec, st);
+  return f32 ? launch_sample_t<true>(a, p, vec, st) : launch_sample_t<false>(a, p, vec, st);
 }
 
 }  // namespace tv

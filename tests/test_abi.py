@@ -41,7 +41,7 @@ def test_every_declared_symbol_is_exported():
 
 def test_status_strings_and_version():
     lib = _lib()
-    assert lib.tv_version() == 1
+    assert lib.tv_version() == 2
     for code in [0, -1, -2, -3, -4, -5, -6, -7, -8]:
         assert lib.tv_status_string(code)
     assert b"unknown" in lib.tv_status_string(123)
@@ -294,32 +294,30 @@ def test_block_causal_host_errors():
 
 
 def _samp(lib, **kw):
-    a = dict(lg=FAKE, dt=0, dl=FAKE, ddt=0, tok=FAKE, par=FAKE, u=FAKE, seed=1, T=1.0, B=1, N=64,
-             V=151936, Nd=8, Dmax=9, ln=FAKE, path=FAKE, corr=FAKE, ws=FAKE, wsb=1 << 40)
+    a = dict(lg=FAKE, dt=0, tok=FAKE, par=FAKE, u=FAKE, seed=1, T=1.0, B=1, N=64,
+             V=151936, Dmax=9, ln=FAKE, path=FAKE, corr=FAKE, ws=FAKE, wsb=1 << 40)
     a.update(kw)
     return lib.tv_tree_accept_sampled(
-        a["lg"], a["dt"], a["dl"], a["ddt"], a["tok"], a["par"], a["u"], a["seed"],
-        ctypes.c_float(a["T"]), a["B"], a["N"], a["V"], a["Nd"], a["Dmax"], a["ln"], a["path"],
-        a["corr"], a["ws"], a["wsb"], None)
+        a["lg"], a["dt"], a["tok"], a["par"], a["u"], a["seed"], ctypes.c_float(a["T"]),
+        a["B"], a["N"], a["V"], a["Dmax"], a["ln"], a["path"], a["corr"], a["ws"], a["wsb"],
+        None)
 
 
 def test_sampled_accept_host_errors():
     lib = _lib()
-    assert lib.tv_tree_accept_sampled_workspace(1, 64, 151936, 8) > 0
-    assert lib.tv_tree_accept_sampled_workspace(1, 64, 151936, 65) == 0
-    assert lib.tv_tree_accept_sampled_workspace(1, 64, 151936, 0) == 0
+    assert lib.tv_tree_accept_sampled_workspace(1, 64, 151936) > 0
+    assert lib.tv_tree_accept_sampled_workspace(1, 64, 1 << 23) > 0
+    assert lib.tv_tree_accept_sampled_workspace(1, 64, (1 << 23) + 1) == 0
+    assert lib.tv_tree_accept_sampled_workspace(1, 0, 100) == 0
     assert _samp(lib, lg=None) == -1
-    assert _samp(lib, dl=None) == -1
     assert _samp(lib, u=None) == -1
     assert _samp(lib, corr=None) == -1
     assert _samp(lib, dt=2) == -3
-    assert _samp(lib, ddt=-1) == -3
     assert _samp(lib, T=0.0) == -2
     assert _samp(lib, T=-1.0) == -2
     assert _samp(lib, T=float("inf")) == -2
     assert _samp(lib, T=float("nan")) == -2
-    assert _samp(lib, Nd=0) == -2
-    assert _samp(lib, Nd=65) == -4
+    assert _samp(lib, V=(1 << 23) + 8) == -4
     assert _samp(lib, N=2049) == -4
     assert _samp(lib, Dmax=0) == -2
     assert _samp(lib, ws=None) == -5

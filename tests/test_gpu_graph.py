@@ -86,7 +86,7 @@ def test_acceptance_and_drafting_graph_replays():
     def call():
         tree_accept(lg, draft, par, w.Dmax, accept_len=outs["ln"], path=outs["path"],
                     tgt_argmax=outs["tgt"])
-        tree_accept_sampled(lg, dl, draft, par, u, 77, 1.0, w.Dmax, accept_len=outs["sln"],
+        tree_accept_sampled(lg, draft, par, u, 77, 1.0, w.Dmax, accept_len=outs["sln"],
                             path=outs["spath"], correction=outs["corr"])
         draft_topw(dl, W, tok=outs["tok"], logp=outs["lp"])
         built["t"] = build_tree(outs["tok"], outs["lp"], w.N)

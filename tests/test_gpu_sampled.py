@@ -1,5 +1,6 @@
 """GPU parity of non-greedy tree acceptance (Sec. 2.4 speculative sampling
-along tree branches) against the oracle, through the C ABI.
+over each node's deterministic children against the target residual, which
+keeps verification lossless) against the oracle, through the C ABI.
 
 The acceptance tests and the race are decided in fp32 on the GPU and in
 fp64 in the oracle.  Inputs are drawn so that no node's test lies within
@@ -18,59 +19,76 @@ from helpers import dev_bf16, dev_i32
 pytestmark = pytest.mark.gpu
 
 CASES = [
-    # (B, N, V, Nd, depth cap, T, dtype target, dtype draft, p_match)
-    (3, 20, 1000, 5, 5, 1.0, "bf16", "bf16", 0.5),
-    (2, 33, 999, 6, 6, 1.0, "f32", "bf16", 0.5),
-    (4, 17, 4096, 4, 4, 0.6, "bf16", "f32", 0.3),
-    (1, 64, 151936, 8, 8, 1.0, "bf16", "bf16", 0.6),
-    (16, 64, 151936, 8, 8, 1.0, "bf16", "bf16", 0.5),
-    (2, 300, 2048, 12, 12, 1.3, "f32", "f32", 0.7),
-    (1, 1, 64, 1, 1, 1.0, "bf16", "bf16", 0.5),
+    # (B, N, V, depth cap, branching, T, dtype, p_match, duplicates among siblings)
+    (3, 20, 1000, 5, 4, 1.0, "bf16", 0.5, True),
+    (2, 33, 999, 6, 4, 1.0, "f32", 0.5, True),
+    (4, 17, 4096, 4, 4, 0.6, "bf16", 0.3, False),
+    (1, 64, 151936, 8, 4, 1.0, "bf16", 0.6, False),
+    (16, 64, 151936, 8, 4, 1.0, "bf16", 0.5, False),
+    (2, 300, 2048, 12, 4, 1.3, "f32", 0.7, True),
+    (1, 1, 64, 1, 1, 1.0, "bf16", 0.5, False),
+    # node slots past the first 512 of every thread batch, wide fan-out
+    (2, 1100, 512, 16, 40, 1.0, "bf16", 0.6, True),
+    (1, 2048, 300, 24, 200, 0.8, "f32", 0.5, True),
+    # a vocabulary that needs several race slices even for one sequence
+    (1, 40, 300007, 6, 8, 1.0, "bf16", 0.6, False),
 ]
 
 
 def _logits(rng, shape, dtype, std=2.0):
     x = rng.standard_normal(size=shape, dtype=np.float32) * np.float32(std)
     if dtype == "f32":
-        return x, torch.from_numpy(x).cuda(), x.astype(np.float64)
+        return torch.from_numpy(x).cuda(), x.astype(np.float64)
     bits = synth.bf16_bits(x)
-    return bits, dev_bf16(bits), oracle.decode_bf16(bits)
+    return dev_bf16(bits), oracle.decode_bf16(bits)
+
+
+def _tokens(rng, par, lg64, pm, dup):
+    """Draft tokens: the target's most likely token at the parent with
+    probability pm, else uniform; without dup every node's children carry
+    distinct tokens (as top-W drafting makes them)."""
+    B, N = par.shape
+    V = lg64.shape[-1]
+    best = lg64.argmax(-1)
+    tok = rng.integers(0, V, size=(B, N)).astype(np.int32)
+    for b in range(B):
+        used = {}
+        for i in range(1, N):
+            p = int(par[b, i])
+            y = int(best[b, p]) if rng.random() < pm else int(tok[b, i])
+            if not dup:
+                while y in used.get(p, ()):
+                    y = int(rng.integers(0, V))
+            used.setdefault(p, set()).add(y)
+            tok[b, i] = y
+    return tok
 
 
 def _inputs(case):
-    B, N, V, Nd, depth, T, dt, ddt, pm = CASES[case]
+    B, N, V, depth, br, T, dt, pm, dup = CASES[case]
     rng = np.random.default_rng(2000 + case)
-    par = np.stack([synth.random_tree(rng, N, depth=min(depth, max(N - 1, 1)), branching=4)
+    par = np.stack([synth.random_tree(rng, N, depth=min(depth, max(N - 1, 1)), branching=br)
                     if N > 1 else np.array([-1], np.int32) for _ in range(B)])
-    _, lg_d, lg64 = _logits(rng, (B, N, V), dt)
-    _, dl_d, dl64 = _logits(rng, (B, Nd, V), ddt)
-    # draft tokens: the target's most likely token at the parent with
-    # probability p_match, else uniform
-    tok = rng.integers(0, V, size=(B, N)).astype(np.int32)
-    best = lg64.argmax(-1)
-    for b in range(B):
-        for i in range(1, N):
-            if rng.random() < pm:
-                tok[b, i] = best[b, par[b, i]]
+    lg_d, lg64 = _logits(rng, (B, N, V), dt)
+    tok = _tokens(rng, par, lg64, pm, dup)
     seed = int(rng.integers(0, 2**63))
     u = rng.random((B, N), dtype=np.float32)
     for _ in range(20):   # keep every test clear of its threshold
-        res = oracle_sampled(lg64, dl64, tok, par, u.astype(np.float64), seed, T, depth + 1,
+        res = oracle_sampled(lg64, tok, par, u.astype(np.float64), seed, T, depth + 1,
                              detail=True)
         close = res[3]["margin"] < 1e-4
         if not close.any():
             break
         u[close] = rng.random(int(close.sum()), dtype=np.float32)
     assert not close.any()
-    return dict(par=par, tok=tok, u=u, seed=seed, T=T, Dmax=depth + 1, lg_d=lg_d, dl_d=dl_d,
-                ref=res)
+    return dict(par=par, tok=tok, u=u, seed=seed, T=T, Dmax=depth + 1, lg_d=lg_d, ref=res)
 
 
 def _gpu(x):
     from paper_2606_18394_amd import tree_accept_sampled
-    ln, path, corr = tree_accept_sampled(x["lg_d"], x["dl_d"], dev_i32(x["tok"]),
-                                         dev_i32(x["par"]), torch.from_numpy(x["u"]).cuda(),
-                                         x["seed"], x["T"], x["Dmax"])
+    ln, path, corr = tree_accept_sampled(x["lg_d"], dev_i32(x["tok"]), dev_i32(x["par"]),
+                                         torch.from_numpy(x["u"]).cuda(), x["seed"], x["T"],
+                                         x["Dmax"])
     torch.cuda.synchronize()
     return ln.cpu().numpy(), path.cpu().numpy(), corr.cpu().numpy()
 
@@ -103,35 +121,40 @@ def test_sampled_invalid_and_too_deep():
     x["par"] = par
     got = _gpu(x)
     assert got[0][0] == -1 and got[2][0] == -1 and (got[1][0] == -1).all()
-    # trees deeper than the draft logits reach
-    y = _inputs(2)
-    y["dl_d"] = y["dl_d"][:, :2].contiguous()
-    got = _gpu(y)
-    ref = oracle_sampled(
-        *(t.float().cpu().numpy().astype(np.float64) for t in (y["lg_d"], y["dl_d"])),
-        y["tok"], y["par"], y["u"].astype(np.float64), y["seed"], y["T"], y["Dmax"])
-    np.testing.assert_array_equal(got[0], ref[0])
-    np.testing.assert_array_equal(got[2], ref[2])
-
-
-def test_sampled_equal_distributions_accept_the_chain():
-    """Draft logits equal to the target's at the parent: every ratio is 1,
-    the whole chain is accepted and the correction is drawn from p at the
-    leaf."""
-    from paper_2606_18394_amd import tree_accept_sampled
-    rng = np.random.default_rng(7)
+    # a chain whose every draft is the target's near-certain choice is
+    # accepted end to end, which needs N path entries: Dmax = 4 is too short
     N, V = 9, 512
-    lg = rng.standard_normal((1, N, V), dtype=np.float32)
-    dl = lg[:, :N - 1].copy()
-    par = np.arange(-1, N - 1, dtype=np.int32)[None]
-    tok = rng.integers(0, V, size=(1, N)).astype(np.int32)
-    u = np.full((1, N), 0.5, np.float32)
-    ln, path, corr = tree_accept_sampled(torch.from_numpy(lg).cuda(), torch.from_numpy(dl).cuda(),
-                                         dev_i32(tok), dev_i32(par), torch.from_numpy(u).cuda(),
-                                         123, 1.0, N)
+    lg = np.zeros((1, N, V), np.float32)
+    lg[0, :, 5] = 40.0
+    y = dict(par=np.arange(-1, N - 1, dtype=np.int32)[None], tok=np.full((1, N), 5, np.int32),
+             u=np.full((1, N), 0.5, np.float32), seed=3, T=1.0, Dmax=4,
+             lg_d=torch.from_numpy(lg).cuda())
+    got = _gpu(y)
+    assert got[0][0] == -1 and got[2][0] == -1 and (got[1][0] == -1).all()
+    y["Dmax"] = N
+    got = _gpu(y)
+    assert got[0][0] == N and got[1][0].tolist() == list(range(N)) and got[2][0] == 5
+
+
+def test_sampled_low_temperature_matches_greedy_acceptance():
+    """At T = 1e-3 the target distributions are point masses: the walk is
+    the greedy path and the correction the greedy prediction at its end
+    (siblings carry distinct tokens)."""
+    from paper_2606_18394_amd import tree_accept
+    rng = np.random.default_rng(77)
+    B, N, V = 4, 64, 4096
+    par = np.stack([synth.random_tree(rng, N, depth=8, branching=4) for _ in range(B)])
+    lg = np.round(rng.standard_normal((B, N, V)).astype(np.float32) * 4)
+    # a unique maximum per row, 1.5 above the rest (p is one-hot in fp32)
+    lg[np.arange(B)[:, None], np.arange(N), rng.integers(0, V, size=(B, N))] = \
+        lg.max(-1) + 1.5
+    tok = _tokens(rng, par, lg.astype(np.float64), 0.7, False)
+    x = dict(par=par, tok=tok, u=rng.random((B, N), dtype=np.float32), seed=5, T=1e-3,
+             Dmax=N, lg_d=torch.from_numpy(lg).cuda())
+    ln, path, corr = _gpu(x)
+    gl, gp, gt = tree_accept(x["lg_d"], dev_i32(tok), dev_i32(par), N)
     torch.cuda.synchronize()
-    eln, epath, ecorr = oracle_sampled(lg.astype(np.float64), dl.astype(np.float64), tok, par,
-                                       u.astype(np.float64), 123, 1.0, N)
-    assert ln.item() == N == eln[0]
-    assert path.cpu().numpy()[0].tolist() == list(range(N))
-    assert corr.item() == ecorr[0]
+    gl, gp, gt = gl.cpu().numpy(), gp.cpu().numpy(), gt.cpu().numpy()
+    np.testing.assert_array_equal(ln, gl)
+    np.testing.assert_array_equal(path, gp)
+    np.testing.assert_array_equal(corr, gt[np.arange(B), gp[np.arange(B), gl - 1]])

@@ -134,8 +134,8 @@ def test_low_temperature_is_the_greedy_rule(seed):
     rng = np.random.default_rng(40 + seed)
     B, N, V = 4, 24, 9
     lg, tok, par, u = _case(rng, B=B, N=N, V=V, depth=6, dup=False)
-    lg = np.round(lg * 4)                           # a clear gap to the runner-up ...
-    lg[np.arange(B)[:, None], np.arange(N), rng.integers(0, V, size=(B, N))] += 20.5
+    lg = np.round(lg * 4)                           # a unique maximum per row ...
+    lg[np.arange(B)[:, None], np.arange(N), rng.integers(0, V, size=(B, N))] = lg.max(-1) + 1.5
     tgt = lg.argmax(-1)
     for b in range(B):                              # ... and many matching drafts
         for i in range(1, N):

@@ -237,6 +237,10 @@ __global__ __launch_bounds__(kSampleThreads) void sample_accept(SampleArgs a, in
   __shared__ float ef[kMaxNodes];        // effective mass of each node's token at its parent
   __shared__ int tokl[kMaxNodes];
   __shared__ int first_pass[kMaxNodes];  // per parent: lowest passing child
+  __shared__ int cnt[kMaxNodes];         // per parent: children, then slots taken
+  __shared__ int start[kMaxNodes + 1];   // per parent: first slot of its children
+  __shared__ short grp[kMaxNodes], srt[kMaxNodes];  // children by parent: any order, index order
+  __shared__ int wsum[kSampleThreads / 64];
   __shared__ short par[kMaxNodes], jmp0[kMaxNodes], jmp1[kMaxNodes], dep0[kMaxNodes],
       dep1[kMaxNodes];
   __shared__ unsigned char ok0[kMaxNodes], ok1[kMaxNodes];
@@ -287,16 +291,74 @@ __global__ __launch_bounds__(kSampleThreads) void sample_accept(SampleArgs a, in
                         lse_t[u]);
       }
     }
+    // The children of every node in index order: a counting sort of the
+    // non-root nodes by parent (children counted per parent, a scan for
+    // the first slot of each parent's group, slots taken in any order, then
+    // each node placed by its rank among its siblings, the number of them
+    // with a lower index).  Siblings are then contiguous, so a node's
+    // earlier siblings are the slots before it in its group.
+    for (int i = tid; i < N; i += kSampleThreads) cnt[i] = 0;
+    __syncthreads();
+    for (int i = 1 + tid; i < N; i += kSampleThreads) atomicAdd(&cnt[par[i]], 1);
+    __syncthreads();
+    {
+      // exclusive scan of cnt[0 .. N): thread t sums entries 4t .. 4t + 3
+      constexpr int kPer = kMaxNodes / kSampleThreads;
+      int c[kPer], tot = 0;
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) {
+        const int p = kPer * tid + k;
+        c[k] = p < N ? cnt[p] : 0;
+        tot += c[k];
+      }
+      int incl = tot;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o);
+        if (lane >= o) incl += y;
+      }
+      if (lane == 63) wsum[wave] = incl;
+      __syncthreads();
+      int off = incl - tot;
+      for (int w = 0; w < wave; ++w) off += wsum[w];
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) {
+        const int p = kPer * tid + k;
+        if (p < N) start[p] = off;
+        off += c[k];
+      }
+      if (tid == 0) start[N] = N - 1;  // every non-root node has one parent
+    }
+    for (int i = tid; i < N; i += kSampleThreads) cnt[i] = 0;
+    __syncthreads();
+    for (int i = 1 + tid; i < N; i += kSampleThreads) {
+      const int p = par[i];
+      grp[start[p] + atomicAdd(&cnt[p], 1)] = (short)i;
+    }
+    __syncthreads();
+    int rank[kNodesPerThread];
+#pragma unroll
+    for (int k = 0; k < kNodesPerThread; ++k) {
+      const int i = tid + kSampleThreads * k;
+      rank[k] = 0;
+      if (i >= 1 && i < N) {
+        const int p = par[i], s0 = start[p], s1 = start[p + 1];
+        int r = 0;
+        for (int m = s0; m < s1; ++m) r += grp[m] < i;
+        srt[s0 + r] = (short)i;
+        rank[k] = r;
+      }
+    }
+    __syncthreads();
     // a token repeated among a node's children has no mass left after its
-    // first occurrence (children follow their parent: siblings of i lie in
-    // (par[i], i))
+    // first occurrence
 #pragma unroll
     for (int k = 0; k < kNodesPerThread; ++k) {
       const int i = tid + kSampleThreads * k;
       if (i >= 1 && i < N) {
-        const int u = par[i], y = tokl[i];
+        const int s0 = start[par[i]], y = tokl[i];
         bool dup = false;
-        for (int j = u + 1; j < i && !dup; ++j) dup = par[j] == u && tokl[j] == y;
+        for (int m = s0; m < s0 + rank[k]; ++m) dup |= tokl[srt[m]] == y;
         ef[i] = dup ? 0.f : e[k];
       }
     }
@@ -309,10 +371,9 @@ __global__ __launch_bounds__(kSampleThreads) void sample_accept(SampleArgs a, in
       const int i = tid + kSampleThreads * k;
       pass[k] = 0;
       if (i >= 1 && i < N) {
-        const int u = par[i];
+        const int u = par[i], s0 = start[u];
         float S = 0.f;
-        for (int j = u + 1; j < i; ++j)
-          if (par[j] == u) S += ef[j];
+        for (int m = s0; m < s0 + rank[k]; ++m) S += ef[srt[m]];
         pass[k] = a.u[(size_t)b * N + i] * (1.f - S) < ef[i];
         if (pass[k]) atomicMin(&first_pass[u], i);
       }

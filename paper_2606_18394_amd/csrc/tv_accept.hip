@@ -19,10 +19,10 @@
 // index on ties) and write the path.
 //
 // Two kernels: the scan stores one key per (row, split); one workgroup per
-// sequence merges its rows' keys in LDS and runs the acceptance.  (A single
-// kernel whose last split and last row carry on through arrival counters
-// was measured slower: its chain of dependent device-scope round trips
-// outlasts the kernel boundary it saves.)
+// sequence merges its rows' keys in registers (one thread per row) and runs
+// the acceptance.  (A single kernel whose last split and last row carry on
+// through arrival counters was measured slower: its chain of dependent
+// device-scope round trips outlasts the kernel boundary it saves.)
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -277,46 +277,36 @@ __global__ __launch_bounds__(kAcceptScanThreads) void accept_scan(AcceptArgs a) 
   if (threadIdx.x == 0) a.part[(size_t)row * a.nsplit + split] = key;
 }
 
-// Second kernel: one workgroup per sequence merges the split keys of its
-// rows (LDS max) and runs the acceptance.
+// Second kernel: one workgroup per sequence; thread t takes rows t,
+// t + kFinishThreads, ...: it requests every split key of its row at once
+// (indices past the last split repeat it, which leaves the max unchanged),
+// keeps the max in registers, and the acceptance runs on the merged
+// predictions.  The parents and tokens are requested first, so all of the
+// kernel's global loads are in flight together.
 __global__ __launch_bounds__(kFinishThreads) void accept_finish(AcceptArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   const int tid = threadIdx.x;
   const int b = blockIdx.x;
   const int N = a.N;
-  // The split keys go out in batches of kFinishLoads per thread (one batch
-  // for every plan but the largest trees).  The first batch is requested
-  // before the nodes' parents and tokens, and at clamped indices (a repeat
-  // leaves the max unchanged), so all of them are in flight together.
-  constexpr int kFinishLoads = 8;
-  const size_t kbase = (size_t)b * N * a.nsplit;
-  const int nkeys = N * a.nsplit;
-  unsigned long long kv[kFinishLoads];
-#pragma unroll
-  for (int u = 0; u < kFinishLoads; ++u) kv[u] = a.part[kbase + min(kFinishThreads * u + tid, nkeys - 1)];
-  int pv[kMaxNodes / kFinishThreads], dv[kMaxNodes / kFinishThreads];
+  constexpr int kRows = kMaxNodes / kFinishThreads;
+  int pv[kRows], dv[kRows];
   load_nodes(a, b, pv, dv);
-  unsigned long long* rowkey = reinterpret_cast<unsigned long long*>(lds + accept_lds_bytes(N));
-  for (int i = tid; i < N; i += kFinishThreads) rowkey[i] = 0ull;
-  __syncthreads();
-  for (int idx0 = 0; idx0 < nkeys; idx0 += kFinishThreads * kFinishLoads) {
-    if (idx0 > 0) {
-#pragma unroll
-      for (int u = 0; u < kFinishLoads; ++u)
-        kv[u] = a.part[kbase + min(idx0 + kFinishThreads * u + tid, nkeys - 1)];
-    }
-#pragma unroll
-    for (int u = 0; u < kFinishLoads; ++u) {
-      const int idx = idx0 + kFinishThreads * u + tid;
-      if (idx < nkeys) atomicMax(&rowkey[idx / a.nsplit], kv[u]);
-    }
-  }
-  __syncthreads();
   const SeqLds l = seq_lds(lds, N);
-  for (int i = tid; i < N; i += kFinishThreads) {
-    const int t = key_index(rowkey[i]);
-    l.tgt[i] = t;
-    if (a.tgt_out) a.tgt_out[(size_t)b * N + i] = t;
+#pragma unroll
+  for (int k = 0; k < kRows; ++k) {
+    const int i = tid + kFinishThreads * k;
+    if (i < N) {
+      const unsigned long long* kp = a.part + ((size_t)b * N + i) * a.nsplit;
+      unsigned long long kv[kAcceptMaxSplit];
+#pragma unroll
+      for (int s = 0; s < kAcceptMaxSplit; ++s) kv[s] = kp[min(s, a.nsplit - 1)];
+      unsigned long long key = 0ull;
+#pragma unroll
+      for (int s = 0; s < kAcceptMaxSplit; ++s) key = umax64(key, kv[s]);
+      const int t = key_index(key);
+      l.tgt[i] = t;
+      if (a.tgt_out) a.tgt_out[(size_t)b * N + i] = t;
+    }
   }
   __syncthreads();
   accept_sequence(a, b, l, pv, dv);
@@ -422,8 +412,7 @@ hipError_t launch_accept(const void* logits, int f32, const int32_t* draft, cons
   if (N <= 64)
     hipLaunchKernelGGL(accept_finish_wave, dim3(B), dim3(64), 0, st, a);
   else
-    hipLaunchKernelGGL(accept_finish, dim3(B), dim3(kFinishThreads), accept_lds_bytes(N) + (size_t)N * 8,
-                       st, a);
+    hipLaunchKernelGGL(accept_finish, dim3(B), dim3(kFinishThreads), accept_lds_bytes(N), st, a);
   return hipGetLastError();
 }
 

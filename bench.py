@@ -159,8 +159,8 @@ def summarize_traffic(dirs, workload, kernel_family):
 
 Commands (repository root, rocprofv3 run from /tmp with TMPDIR=/tmp; one counter per run):
 
-    rocprofv3 --pmc FETCH_SIZE --output-format csv -d <f> -o b -- python3 bench.py --workload {workload} --core-only --steps 40 --warmup 5
-    rocprofv3 --pmc WRITE_SIZE --output-format csv -d <w> -o b -- python3 bench.py --workload {workload} --core-only --steps 40 --warmup 5
+    rocprofv3 --pmc FETCH_SIZE --output-format csv -d <f> -o b -- python3 bench.py --workload {workload} --core-only --steps 20 --warmup 3
+    rocprofv3 --pmc WRITE_SIZE --output-format csv -d <w> -o b -- python3 bench.py --workload {workload} --core-only --steps 20 --warmup 3
     rocprofv3 --pmc FETCH_SIZE --output-format csv -d <cf> -o c -- python3 bench.py --copy-only
     rocprofv3 --pmc WRITE_SIZE --output-format csv -d <cw> -o c -- python3 bench.py --copy-only
     python3 bench.py --workload {workload} --kernel {kernel_family} --summarize-traffic <f> <w> <cf> <cw>

@@ -312,49 +312,107 @@ __global__ __launch_bounds__(kFinishThreads) void accept_finish(AcceptArgs a) {
   accept_sequence(a, b, l, pv, dv);
 }
 
-// Second kernel for trees of at most 64 nodes: one wave per sequence, lane
-// i holding node i, so the merge, the pointer jumping and the path need no
-// LDS and no workgroup barrier (lane exchanges only).  Same results as
-// accept_finish.
+// Second kernel for trees of at most 64 * NPL nodes (NPL = 1 or 2): one
+// wave per sequence, lane l holding nodes l, l + 64, ..., l + 64 (NPL - 1),
+// so the merge, the pointer jumping and the path need no LDS and no
+// workgroup barrier (lane exchanges only).  Same results as accept_finish.
+
+// Split keys a node's merge requests: the plans give trees of more than
+// 32 * NPL nodes at most min(16, 64 / NPL) splits (the acceptance plan
+// aims at about 2048 (row, split) pairs and caps splits at 16).
+template <int NPL>
+constexpr int wave_finish_loads() {
+  return 64 / NPL < kAcceptMaxSplit ? 64 / NPL : kAcceptMaxSplit;
+}
+
+// The value of node j (held by lane j % 64 in slot j / 64).  Every lane
+// takes part in every exchange (an inactive source lane would read as
+// zero), so the slot is selected after the shuffles.
+template <int NPL>
+__device__ __forceinline__ int lane_fetch(const int (&v)[NPL], int j) {
+  const int src = j & 63, slot = j >> 6;
+  int r = __shfl(v[0], src);
+#pragma unroll
+  for (int q = 1; q < NPL; ++q) {
+    const int t = __shfl(v[q], src);
+    r = slot == q ? t : r;
+  }
+  return r;
+}
+
+template <int NPL>
 __global__ __launch_bounds__(64) void accept_finish_wave(AcceptArgs a) {
-  const int b = blockIdx.x, i = threadIdx.x;
+  const int b = blockIdx.x, lane = threadIdx.x;
   const int N = a.N;
-  const bool node = i < N;
-  const int p = node ? a.parent[(size_t)b * N + i] : 0;
-  const int y = node ? a.draft[(size_t)b * N + i] : 0;
-  // this node's prediction: the max of its split keys, all requested at
+  int p[NPL], y[NPL], tgt[NPL], jmp[NPL], ok[NPL], dep[NPL];
+  bool node[NPL];
+  int badi = 0;
+#pragma unroll
+  for (int q = 0; q < NPL; ++q) {
+    const int i = lane + 64 * q;
+    node[q] = i < N;
+    p[q] = node[q] ? a.parent[(size_t)b * N + i] : 0;
+    y[q] = node[q] ? a.draft[(size_t)b * N + i] : 0;
+  }
+  // each node's prediction: the max of its split keys, all requested at
   // once (indices past the last split repeat it, which leaves the max
   // unchanged and keeps the loads free of branches)
-  unsigned long long key = 0ull;
-  {
-    const unsigned long long* kp = a.part + ((size_t)b * N + (node ? i : 0)) * a.nsplit;
-    constexpr int kLoads = kAcceptMaxSplit;
+  constexpr int kLoads = wave_finish_loads<NPL>();
+#pragma unroll
+  for (int q = 0; q < NPL; ++q) {
+    const int i = lane + 64 * q;
+    const unsigned long long* kp = a.part + ((size_t)b * N + (node[q] ? i : 0)) * a.nsplit;
     unsigned long long kv[kLoads];
 #pragma unroll
     for (int k = 0; k < kLoads; ++k) kv[k] = kp[min(k, a.nsplit - 1)];
+    unsigned long long key = 0ull;
 #pragma unroll
     for (int k = 0; k < kLoads; ++k) key = umax64(key, kv[k]);
-    if (!node) key = 0ull;
+    tgt[q] = key_index(node[q] ? key : 0ull);
+    if (node[q] && a.tgt_out) a.tgt_out[(size_t)b * N + i] = tgt[q];
+    const int bq = node[q] && ((i == 0) ? (p[q] != -1) : (p[q] < 0 || p[q] >= i));
+    badi |= bq;
+    jmp[q] = node[q] && i > 0 && !bq ? p[q] : 0;  // the root (and padding) jump to node 0
   }
-  const int tgt = key_index(key);
-  if (node && a.tgt_out) a.tgt_out[(size_t)b * N + i] = tgt;
-  const int badi = node && ((i == 0) ? (p != -1) : (p < 0 || p >= i));
   const bool bad = __any(badi);
   int len = -1, v = 0, depth = 0;
-  int jmp = node && i > 0 && !badi ? p : 0;  // the root (and padding) jump to node 0
   if (!bad) {
-    // every lane takes part in a lane exchange (an inactive source lane
-    // would read as zero), so the shuffle comes before the selection
-    const int tgt_parent = __shfl(tgt, jmp);
-    int ok = !node ? 0 : (i == 0 ? 1 : (y == tgt_parent));
-    int dep = node && i > 0 ? 1 : 0;
-    // pointer jumping: ceil(log2 64) = 6 rounds reach the root
-    for (int r = 0; r < 6 && __any(jmp != 0); ++r) {
-      ok &= __shfl(ok, jmp);
-      dep += __shfl(dep, jmp);
-      jmp = __shfl(jmp, jmp);
+#pragma unroll
+    for (int q = 0; q < NPL; ++q) {
+      const int i = lane + 64 * q;
+      const int tgt_parent = lane_fetch<NPL>(tgt, jmp[q]);
+      ok[q] = !node[q] ? 0 : (i == 0 ? 1 : (y[q] == tgt_parent));
+      dep[q] = node[q] && i > 0 ? 1 : 0;
     }
-    unsigned int k = ok ? ((unsigned int)dep << 16) | (0xFFFFu - (unsigned int)i) : 0u;
+    // pointer jumping: ceil(log2(64 NPL)) rounds reach the root; every
+    // exchange of a round reads the values of the round before
+    int more = 0;
+#pragma unroll
+    for (int q = 0; q < NPL; ++q) more |= jmp[q] != 0;
+    for (int r = 0; r < 12 && __any(more); ++r) {
+      int okj[NPL], depj[NPL], jj[NPL];
+#pragma unroll
+      for (int q = 0; q < NPL; ++q) {
+        okj[q] = lane_fetch<NPL>(ok, jmp[q]);
+        depj[q] = lane_fetch<NPL>(dep, jmp[q]);
+        jj[q] = lane_fetch<NPL>(jmp, jmp[q]);
+      }
+      more = 0;
+#pragma unroll
+      for (int q = 0; q < NPL; ++q) {
+        ok[q] &= okj[q];
+        dep[q] += depj[q];
+        jmp[q] = jj[q];
+        more |= jmp[q] != 0;
+      }
+    }
+    unsigned int k = 0u;
+#pragma unroll
+    for (int q = 0; q < NPL; ++q) {
+      const unsigned int i = (unsigned int)(lane + 64 * q);
+      const unsigned int kq = ok[q] ? ((unsigned int)dep[q] << 16) | (0xFFFFu - i) : 0u;
+      k = kq > k ? kq : k;
+    }
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) {
       const unsigned int other = __shfl_xor(k, o);
@@ -365,17 +423,17 @@ __global__ __launch_bounds__(64) void accept_finish_wave(AcceptArgs a) {
     len = depth + 1 > a.Dmax ? -1 : depth + 1;
   }
   int32_t* pth = a.path + (size_t)b * a.Dmax;
-  for (int k = i; k < a.Dmax; k += 64)
+  for (int k = lane; k < a.Dmax; k += 64)
     if (k >= len) pth[k] = -1;
   if (len > 0) {
     // walk up from v: the node at depth k of the path goes to entry k
     int u = v;
     for (int k = depth; k >= 0; --k) {
-      if (i == 0) pth[k] = u;
-      u = __shfl(p, u);
+      if (lane == 0) pth[k] = u;
+      u = lane_fetch<NPL>(p, u);
     }
   }
-  if (i == 0) a.accept_len[b] = len;
+  if (lane == 0) a.accept_len[b] = len;
 }
 
 hipError_t launch_accept(const void* logits, int f32, const int32_t* draft, const int32_t* parent,
@@ -409,8 +467,15 @@ hipError_t launch_accept(const void* logits, int f32, const int32_t* draft, cons
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (N <= 64)
-    hipLaunchKernelGGL(accept_finish_wave, dim3(B), dim3(64), 0, st, a);
+  // One wave per sequence up to 128 nodes (the plans' split counts fit its
+  // loads, checked here), else a workgroup of kFinishThreads.  At two nodes
+  // per lane the wave takes 13.3 us against 17.1 us for the workgroup
+  // (long_ctx, 128 nodes); at eight per lane its lane exchanges (eight per
+  // value and round) made it 55.8 us against 37.8 us (big_tree_32b).
+  if (N <= 64 && p.nsplit <= wave_finish_loads<1>())
+    hipLaunchKernelGGL(accept_finish_wave<1>, dim3(B), dim3(64), 0, st, a);
+  else if (N <= 128 && p.nsplit <= wave_finish_loads<2>())
+    hipLaunchKernelGGL(accept_finish_wave<2>, dim3(B), dim3(64), 0, st, a);
   else
     hipLaunchKernelGGL(accept_finish, dim3(B), dim3(kFinishThreads), accept_lds_bytes(N), st, a);
   return hipGetLastError();

@@ -135,3 +135,23 @@ def test_row_count_plans(B):
     rng = np.random.default_rng(20 + B)
     inp = _small(rng, B, 2048, 48, "bf16", depth=14, width=4)
     _compare(inp, oracle_draft_tokens(inp), 16)
+
+
+@pytest.mark.parametrize("N", [65, 100, 128, 129, 200, 256, 257, 300, 511, 512, 513])
+def test_node_counts_around_the_one_wave_limits(N):
+    """Trees whose nodes share a wave's lanes (one to eight per lane) and
+    the first size past them; bushy random trees, a full chain, and an
+    invalid parent in a later lane slot."""
+    rng = np.random.default_rng(300 + N)
+    B = 3
+    inp = _small(rng, B, N, 700, "bf16", depth=min(20, N - 1), width=6)
+    inp["parent"][1] = synth.chain_tree(N)
+    draft = oracle_draft_tokens(inp)
+    tgt = oracle.target_argmax(host_logits_f64(inp))
+    draft[1, 1:] = tgt[1, :-1]              # the chain is accepted end to end
+    ln = _compare(inp, draft, N)
+    assert ln[1] == N
+    _compare(inp, draft, 12)                 # the chain's path is too long: sentinel
+    inp["parent"][2, N - 1] = N - 1          # invalid: a node its own parent
+    ln = _compare(inp, draft, N)
+    assert ln[2] == -1

@@ -18,11 +18,15 @@
 // parent links (O(log depth) rounds), pick the deepest accepted node (lowest
 // index on ties) and write the path.
 //
-// Two kernels: the scan stores one key per (row, split); one workgroup per
-// sequence merges its rows' keys in registers (one thread per row) and runs
-// the acceptance.  (A single kernel whose last split and last row carry on
-// through arrival counters was measured slower: its chain of dependent
-// device-scope round trips outlasts the kernel boundary it saves.)
+// Two kernels: the scan stores one key per (row, split); one wave (trees of
+// up to 128 nodes) or one workgroup per sequence merges its rows' keys in
+// registers and runs the acceptance.  A single kernel in which the split
+// that completes a row merges it and the row that completes a sequence runs
+// its acceptance (device-scope key and prediction stores, per-row and
+// per-sequence arrival counters) was parity-green and slower on every
+// workload: 16.2 / 20.8 / 62.1 / 39.9 us against 9.4 / 13.4 / 56.1 / 38.1 us
+// for 64 / 128 / 16 x 64 / 512 nodes over 151936 bf16 logits.  Its chain of
+// dependent device-scope round trips outlasts the kernel boundary it saves.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 

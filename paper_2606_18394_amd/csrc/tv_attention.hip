@@ -186,11 +186,17 @@ __device__ __forceinline__ void wait_vm_dyn(int n) {
 }
 
 // Layout of one 32-key tile in LDS: row-major, D bf16 per row, 16-byte
-// chunks XOR-swizzled by the row.  The swizzle is chosen so that
-//   * 16 rows read at the same logical chunk (the K operand reads, 16 lanes
-//     per pass) land in 16 different bank groups, and
-//   * the transposing V reads (rows 8k..8k+7, two adjacent chunks each, 32
-//     lanes per pass) cover every bank exactly once.
+// chunks XOR-swizzled by the row.  With reads served 256 bytes at a time
+// (64 banks; 16 lanes of a ds_read_b128, 32 of a ds_read_b64_tr_b16) the
+// swizzle is free of bank conflicts: 16 rows at one logical chunk (the K
+// operand reads) land in 16 bank groups, and the transposing V reads (rows
+// 8k..8k+7, two adjacent chunks) cover every bank once.  The hardware
+// serves the K reads 128 bytes at a time (8 lanes), where rows r and r + 4
+// collide: the K reads are 2-way, a third of the LDS-active cycles, as the
+// bank-conflict counter shows.  A swizzle free of conflicts at both widths
+// (((r & 3) << 1) | ((r >> 2) & 1) | (((r >> 2) ^ (r >> 3)) & 1) << 3 for
+// D = 128) removed them and a third of the LDS-active cycles but not a
+// cycle of the kernel (about 1% slower), so this one stays.
 template <int D>
 struct TileLayout {
   static constexpr int kRowBytes = 2 * D;

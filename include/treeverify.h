@@ -22,8 +22,9 @@
  *   - Every tensor pointer is caller-owned DEVICE memory, row-major and
  *     contiguous, 16-byte aligned.  The library never allocates or frees.
  *   - Calls are asynchronous on `stream` (0 = the null stream) and never
- *     synchronise the host.  They keep no global mutable state; concurrent
- *     calls are safe when they use distinct workspaces.
+ *     synchronise the host.  They keep no global mutable state (apart from
+ *     tv_tree_accept_noalloc, which shares a static scratch array per GPU);
+ *     concurrent calls are safe when they use distinct workspaces.
  *   - The workspace is caller-owned device memory of at least the size the
  *     matching *_workspace() query returns.  It must be zero-filled once
  *     before its first use; the kernels leave it ready for the next call.

@@ -1,5 +1,7 @@
 // C entry points: argument checks, workspace sizing and launches.  No
-// allocation, no host synchronisation, no global mutable state.
+// allocation and no host synchronisation.  The only global state is that of
+// the allocation-free acceptance: its static device scratch array and the
+// per-device cache of that array's address.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 

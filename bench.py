@@ -5,8 +5,10 @@ A step is one pass of the whole hot path over one batch: tree-masked GQA
 attention of all draft-tree nodes (one attention layer at the workload's
 shape) followed by greedy tree acceptance over the nodes' target logits.
 Inputs are seeded synthetic tensors of the workload's shape, resident in HBM
-before timing starts; R input replicas (> 512 MB in total, twice the MI355X
-last-level cache) are rotated so every step reads from HBM.
+before timing starts.  Each timed graph rotates over enough input replicas
+that at least 512 MB (twice the MI355X last-level cache) is touched between
+two uses of one replica, so every timed call reads its inputs from HBM; the
+JSON labels each group of timings with its reuse distance.
 
 The headline workload is the largest configuration (big_tree_32b: Qwen3-32B
 attention geometry, one sequence, 8192 cached rows, a 512-node tree).  Every
@@ -46,6 +48,7 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 MALL_BYTES = 256 << 20
+MAX_REPLICAS = 4096            # bounds graph size and capture time at the smallest shapes
 PAGE_BLOCK = 64                # rows per paged-cache block in the paged timing
 TRAIN_ANCHORS, TRAIN_BLOCK, TRAIN_CONTEXT = 512, 16, 4096   # training-mask attention timing
 HEADLINE = "big_tree_32b"
@@ -63,7 +66,7 @@ def parse():
     ap.add_argument("--core-only", action="store_true",
                     help="time only the headline workload's step, attention and acceptance "
                          "(no other workloads, no extra paths, no CPU leg): the profiler runs")
-    ap.add_argument("--replicas", type=int, default=0, help="0 = enough to exceed 2x the LLC")
+    ap.add_argument("--replicas", type=int, default=0, help="0 = enough that every timed graph touches 2x the LLC between reuses")
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the CPU leg (oracle timing and the oracle checks)")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
@@ -463,40 +466,63 @@ def _i32(torch, dev, a):
 
 
 class Timer:
-    """HIP graphs of a step's launches, replayed between HIP events on the
-    stream the graphs are launched on.  One graph runs the R replicas in
-    turn, R more graphs run one replica each, so exactly k calls are timed
-    and the timed region measures the GPU, not Python's launch overhead."""
+    """HIP graphs of a path's launches, replayed between HIP events on the
+    stream the graphs are launched on.  A graph's R calls take R different
+    input replicas in turn; k timed calls are k // R replays of that graph
+    and one replay of a graph of its first k % R calls, so exactly k calls
+    are timed and the timed region measures the GPU, not Python's launch
+    overhead.  Two untimed replays come first, so the first timed call finds
+    its replica least recently used."""
 
     def __init__(self, torch, R):
         self.torch, self.R, self.graphs = torch, R, {}
 
-    def capture(self, name, fn):
-        torch = self.torch
+    def _cap(self, fn, rs):
+        g = self.torch.cuda.CUDAGraph()
+        with self.torch.cuda.graph(g):
+            for r in rs:
+                fn(r)
+        return g
 
-        def cap(rs):
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g):
-                for r in rs:
-                    fn(r)
-            return g
-        self.graphs[name] = (cap(range(self.R)), [cap([r]) for r in range(self.R)])
+    def capture(self, name, fn, R=None):
+        R = R or self.R
+        self.graphs[name] = (fn, R, self._cap(fn, range(R)), {})
 
     def time_ms(self, name, k):
         torch = self.torch
-        full, singles = self.graphs[name]
+        fn, R, full, heads = self.graphs[name]
+        rem = k % R
+        if rem and rem not in heads:
+            heads[rem] = self._cap(fn, range(rem))
         for _ in range(2):             # untimed graph warmup
             full.replay()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        for _ in range(k // self.R):
+        for _ in range(k // R):
             full.replay()
-        for r in range(k % self.R):
-            singles[r].replay()
+        if rem:
+            heads[rem].replay()
         e1.record()
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / k     # ms
+
+
+def replicas_for(nbytes):
+    """Input replicas one timed graph rotates over so that at least twice
+    the last-level cache is touched between two uses of one replica: every
+    timed call then reads its inputs from HBM."""
+    return max(1, min(MAX_REPLICAS, -(-2 * MALL_BYTES // max(1, nbytes))))
+
+
+def cache_state(reuse):
+    """Label of the timed graphs' cache state from the bytes each touches
+    between two uses of one input replica."""
+    warm = [nm for nm, b in reuse.items() if b < 2 * MALL_BYTES]
+    mb = ", ".join(f"{nm} {b / 2**20:.0f} MiB" for nm, b in reuse.items())
+    if not warm:
+        return f"cold: every replica reused after >= 2x the 256 MiB LLC ({mb})"
+    return f"warm in the 256 MiB LLC: {', '.join(warm)} (reuse distance {mb})"
 
 
 def run_workload(name, args, extras, cpu_leg):
@@ -524,7 +550,12 @@ def run_workload(name, args, extras, cpu_leg):
     base = dict(q=bf(inp["q"]), kc=bf(inp["k_cache"]), vc=bf(inp["v_cache"]),
                 kt=bf(inp["k_tree"]), vt=bf(inp["v_tree"]), logits=logits0)
     per_rep = sum(t.numel() * t.element_size() for t in base.values())
-    R = args.replicas or max(1, -(-2 * MALL_BYTES // per_rep))
+    # enough replicas that the attention-only and acceptance-only graphs, not
+    # just the step, read every input from HBM
+    attn_bytes, attn_flops, acc_bytes = algorithmic_work(inp, w)
+    R = args.replicas or max(replicas_for(attn_bytes), replicas_for(acc_bytes))
+    reuse = {"step": R * (attn_bytes + acc_bytes), "attention": R * attn_bytes,
+             "accept": R * acc_bytes}
     reps = [base] + [{k: v.clone() for k, v in base.items()} for _ in range(R - 1)]
     parent, kv_len, draft_d = i32(inp["parent"]), i32(inp["kv_len"]), i32(draft)
     outs = [torch.empty(w.B, w.N, w.Hq, w.D, dtype=torch.bfloat16, device=dev) for _ in range(R)]
@@ -576,7 +607,6 @@ def run_workload(name, args, extras, cpu_leg):
     del got_all
     acc = (acc_len.cpu().numpy(), path.cpu().numpy(), targ.cpu().numpy())
 
-    attn_bytes, attn_flops, acc_bytes = algorithmic_work(inp, w)
     rec = {
         "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "D": w.D, "Lmax": w.L, "N": w.N, "V": w.V,
         "logits": w.logits_dtype, "kv_len_sum": int(inp["kv_len"].sum()), "replicas": R,
@@ -587,7 +617,7 @@ def run_workload(name, args, extras, cpu_leg):
                                        attn_flops, "attn_main", w.name),
         "accept_roofline": roofline("tree_accept", ms_acc * 1e-3, acc_bytes, 0,
                                     "accept_scan", w.name),
-        "cache": "cold (replicas rotated)",
+        "cache": cache_state(reuse),
     }
 
     extra = None
@@ -619,7 +649,8 @@ def run_extras(torch, w, inp, args, dev, R, reps, parent, kv_len, draft_d, outs,
     Wd = synth.draft_width(w)
     dl = synth.draft_logits(w)
     dlog0 = torch.from_numpy(dl).to(dev) if w.logits_dtype == "f32" else bf(dl)
-    dlogs = [dlog0] + [dlog0.clone() for _ in range(R - 1)]
+    R_topw = replicas_for(dlog0.numel() * dlog0.element_size())   # a small input: more replicas
+    dlogs = [dlog0] + [dlog0.clone() for _ in range(R_topw - 1)]
     dtok = torch.empty(w.B, w.depth, Wd, dtype=torch.int32, device=dev)
     dlp = torch.empty(w.B, w.depth, Wd, dtype=torch.float32, device=dev)
     ws_topw = torch.zeros(max(256, lib.tv_draft_topw_workspace(w.B, w.depth, w.V)),
@@ -729,12 +760,13 @@ def run_extras(torch, w, inp, args, dev, R, reps, parent, kv_len, draft_d, outs,
         cdst[r].copy_(csrc[r])
 
     for s in range(2):
-        topw(s % R)
+        topw(s % R_topw)
         build(s % R)
         sampled(s % R)
     torch.cuda.synchronize()
     timer = Timer(torch, R)
-    for nm, fn in [("topw", topw), ("build", build), ("attn_paged", attn_paged),
+    timer.capture("topw", topw, R_topw)
+    for nm, fn in [("build", build), ("attn_paged", attn_paged),
                    ("attn_tail", attn_tail), ("train_attn", train_attn), ("sampled", sampled),
                    ("reset", reset), ("copy_floor", copy_floor), ("commit", commit)]:
         timer.capture(nm, fn)
@@ -765,8 +797,11 @@ def run_extras(torch, w, inp, args, dev, R, reps, parent, kv_len, draft_d, outs,
             "anchors": TA, "block": TS, "context": TL, "us": ms["train_attn"] * 1e3,
             "flops": train_flops, "TFLOPs": train_flops / (ms["train_attn"] * 1e-3) / 1e12,
             "mfma_frac": train_flops / (ms["train_attn"] * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
-            "cache": f"warm: its {train_bytes / 1e6:.0f} MB of inputs and output stay in the "
-                     f"256 MB last-level cache between calls"},
+            "cache": cache_state({"training_mask_attention": train_bytes})},
+        "cache": cache_state({"draft_topw": R_topw * dlog0.numel() * dlog0.element_size(),
+                              "paged_attention": R * attn_bytes,
+                              "tree_tail_attention": R * attn_bytes,
+                              "sampled_accept": R * samp_bytes, "copy_floor": R * 4 * half}),
         "commit_us": ms_commit * 1e3, "commit_rows": int(acc_len.sum().item()),
         "copy_floor": {"bytes_moved": 4 * half, "us": ms["copy_floor"] * 1e3,
                        "GBps": 4 * half / (ms["copy_floor"] * 1e-3) / 1e9},

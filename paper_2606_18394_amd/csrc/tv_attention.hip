@@ -127,6 +127,21 @@ __device__ __forceinline__ float2 load_dev(const float2* p) {
   asm volatile("global_load_dwordx2 %0, %1, off sc1" : "=v"(v) : "v"(p) : "memory");
   return v;
 }
+// Plain 16- and 4-byte loads issued as inline assembly, for the prologue:
+// the compiler does not track them, so it inserts no wait of its own that
+// would also drain the tile DMAs issued after them.  Loads return in issue
+// order, so an explicit vmcnt that leaves exactly the younger DMAs
+// outstanding covers them; `loaded` then ties each value to that wait.
+__device__ __forceinline__ bf16x8 load_b128(const __bf16* p) {
+  bf16x8 v;
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+__device__ __forceinline__ int load_i32(const int32_t* p) {
+  int v;
+  asm volatile("global_load_dword %0, %1, off" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
 // Waits for every outstanding vector memory access; `loaded` values of
 // load_dev are tied to the wait so no use is scheduled before it.
 __device__ __forceinline__ void wait_all_vm() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
@@ -169,10 +184,31 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// s_waitcnt vmcnt(n) for a wave-uniform n in 0..63 (the prologue's waits:
+// queries and DMAs still in flight); anything else waits for everything.
+__device__ __forceinline__ void wait_vm_any(int n) {
+  switch (n) {
+#define TV_WAIT_CASE(k) \
+  case k:               \
+    wait_vm<k>();       \
+    break;
+#define TV_WAIT_CASES8(k)                                                                    \
+  TV_WAIT_CASE(k) TV_WAIT_CASE(k + 1) TV_WAIT_CASE(k + 2) TV_WAIT_CASE(k + 3) TV_WAIT_CASE(k + 4) \
+      TV_WAIT_CASE(k + 5) TV_WAIT_CASE(k + 6) TV_WAIT_CASE(k + 7)
+    TV_WAIT_CASES8(0) TV_WAIT_CASES8(8) TV_WAIT_CASES8(16) TV_WAIT_CASES8(24)
+    TV_WAIT_CASES8(32) TV_WAIT_CASES8(40) TV_WAIT_CASES8(48) TV_WAIT_CASES8(56)
+#undef TV_WAIT_CASES8
+#undef TV_WAIT_CASE
+    default: wait_vm<0>(); break;
+  }
+}
+
 // n is (tiles still in flight) x (DMAs per tile); only these values occur
 __device__ __forceinline__ void wait_vm_dyn(int n) {
   switch (n) {
+    case 1: wait_vm<1>(); break;
     case 2: wait_vm<2>(); break;
+    case 3: wait_vm<3>(); break;
     case 4: wait_vm<4>(); break;
     case 6: wait_vm<6>(); break;
     case 8: wait_vm<8>(); break;
@@ -624,11 +660,17 @@ void attn_main(AttnArgs a) {
   const int n_iter = t1 > t0 ? (t1 - t0 + WK - 1) / WK : 0;
   const int n_mine = t0 + wk < t1 ? (t1 - t0 - wk + WK - 1) / WK : 0;  // valid tiles
 
-  // Issue order: parents, queries, then the first tiles' DMAs.  Loads
-  // complete in order and the compiler counts only its own loads, so its
-  // wait for the parents (at most the query loads still outstanding) leaves
-  // the younger DMAs in flight while the tree metadata is built.
+  // Issue order: parents, queries, then the first tiles' DMAs, all before
+  // any of them is used.  When the WR waves of a key group share its ring
+  // (WR > 1) the prologue fills every stage: the ring's own refills come
+  // after a workgroup barrier, and the first of them would otherwise wait
+  // for the first tile's round trip (measured: 0.85 us of the Qwen3-8B-
+  // shaped 64-node, 4096-row call).  A single-wave key group refills before
+  // its waits and keeps one stage for that.
   constexpr int kParPerThread = (kMaxNodes + kThreads - 1) / kThreads;
+  constexpr int NQ = NT * NC;  // query loads per lane
+  constexpr int kPro = WR > 1 ? NS : NS - 1;
+  const int npro = min(kPro, n_mine);  // tiles the prologue issues
   int pv[kParPerThread];
   if (has_tree) {
     // indices clamped rather than branched on, so the loads stay in flight
@@ -636,34 +678,36 @@ void attn_main(AttnArgs a) {
 #pragma unroll
     for (int k = 0; k < kParPerThread; ++k) {
       const int i = tid + kThreads * k;
-      pv[k] = a.parent ? pr[i < a.N ? i : a.N - 1] : i - 1;  // NULL: a chain
+      pv[k] = a.parent ? load_i32(pr + (i < a.N ? i : a.N - 1)) : i - 1;  // NULL: a chain
     }
   }
 
   // ---- queries: B operand of S^T = K Q^T, lane holds Q[row l16][8*g4 .. +8]
   const int wrow0 = r0 + kRowsPerWave * wr;
   bf16x8 qf[NT][NC];
+  bool qok[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const int r = wrow0 + nt * 16 + l16;
     const bool ok = r < a.M;
+    qok[nt] = ok;
     const int node = ok ? r / a.G : 0;
     const int h = g * a.G + (ok ? r % a.G : 0);
     const __bf16* qp = a.q + ((size_t)(b * a.N + node) * a.Hq + h) * D + 8 * g4;
 #pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      bf16x8 v = *reinterpret_cast<const bf16x8*>(qp + 32 * c);
-      if (!ok) v = bf16x8{};
-      qf[nt][c] = v;
-    }
+    for (int c = 0; c < NC; ++c) qf[nt][c] = load_b128(qp + 32 * c);
   }
 
 #pragma unroll
-  for (int i = 0; i < NS - 1; ++i)
+  for (int i = 0; i < kPro; ++i)
     if (i < n_mine) issue_tile<D, PW, kPaged>(src, dma_off, wr, lane, t0 + wk + WK * i, ring + i * STAGE);
 
   // ---- tree structure: ancestor-or-self bitmask of this block's nodes
   if (has_tree) {
+    // the parents are done once at most the queries and the DMAs are in flight
+    wait_vm_any(NQ + npro * PW);
+#pragma unroll
+    for (int k = 0; k < kParPerThread; ++k) loaded(pv[k]);
     int bad = 0;
 #pragma unroll
     for (int k = 0; k < kParPerThread; ++k) {
@@ -690,6 +734,17 @@ void attn_main(AttnArgs a) {
     if (tid == 0) *flag = bad;
     __syncthreads();
   }
+
+  // the queries are done once at most the DMAs are in flight; rows past the
+  // block's last row get zero queries
+  wait_vm_any(npro * PW);
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      loaded(qf[nt][c]);
+      if (!qok[nt]) qf[nt][c] = bf16x8{};
+    }
 
   // O^T accumulators, and l: row sums of the bf16 weights, accumulated on
   // the matrix cores as ones^T P^T so numerator and denominator see the same
@@ -720,16 +775,17 @@ void attn_main(AttnArgs a) {
   bf16x8 ones_v = ones;
   asm volatile("" : "+v"(ones_v));  // keep it in registers, not rebuilt every tile
   // Ring step of iteration i: wait for this key group's tile i and refill
-  // the ring.  With WR > 1 my DMAs of tile i are done once at most
-  // min(later tiles, NS-2) tiles' DMAs are outstanding; the barrier makes
-  // the whole group's visible and guarantees the slot of tile i-1 is no
-  // longer read.
+  // the ring.  With WR > 1 the prologue issued tiles 0..NS-1 and step j >= 1
+  // issues tile j+NS-1, so my DMAs of tile i are done once at most
+  // min(later tiles, NS-1 at step 0, NS-2 after) tiles' DMAs are
+  // outstanding; the barrier makes the whole group's visible and guarantees
+  // the slot of tile i-1 is no longer read.
   auto ring_step = [&](int i) {
     const bool mine = i < n_mine;
     if (WR > 1) {
-      if (mine) wait_vm_dyn(min(n_mine - 1 - i, NS - 2) * PW);
+      if (mine) wait_vm_dyn(min(n_mine - 1 - i, i == 0 ? NS - 1 : NS - 2) * PW);
       __syncthreads();
-      if (i + NS - 1 < n_mine)
+      if (i >= 1 && i + NS - 1 < n_mine)
         issue_tile<D, PW, kPaged>(src, dma_off, wr, lane, t0 + wk + WK * (i + NS - 1),
                           ring + ((i + NS - 1) % NS) * STAGE);
     } else {

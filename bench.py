@@ -108,7 +108,9 @@ def _counter_rows(d, counter):
 KERNEL_PATTERNS = {
     # the verification launch is the contiguous-cache instantiation with the
     # most dispatches (the other timed paths launch fewer)
-    "attn_main": (r"attn_main<(\d+), (\d+), (\d+), (\d+)(?:, false)?>", "attn_main<%s,%s,%s,%s>"),
+    # (template arguments D, WR, WK, NS, paged, shared queries)
+    "attn_main": (r"attn_main<(\d+), (\d+), (\d+), (\d+), false(?:, (?:false|true))?>",
+                  "attn_main<%s,%s,%s,%s>"),
     "accept_scan": (r"accept_scan<(\w+), (\w+)>", "accept_scan<%s,%s>"),
 }
 

@@ -579,7 +579,7 @@ __device__ __forceinline__ void merge_chunks(const AttnArgs& a, size_t part0, in
 // waves of a key group share one LDS ring and walk that group's tiles (every
 // WK-th tile of the chunk) in lock step; WK > 1 groups merge their partial
 // softmax states in LDS at the end.
-template <int D, int WR, int WK, int NS, bool kPaged>
+template <int D, int WR, int WK, int NS, bool kPaged, bool kShareQ>
 __global__ __launch_bounds__(64 * WR * WK) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_main(AttnArgs a) {
   using TL = TileLayout<D>;
@@ -618,7 +618,12 @@ void attn_main(AttnArgs a) {
   constexpr int RING = WK * NS * STAGE;
   const uint32_t ring = (uint32_t)(uintptr_t)smem + wk * NS * STAGE;
   const unsigned char* ring_ptr = smem + wk * NS * STAGE;
-  uint32_t* anc = reinterpret_cast<uint32_t*>(smem + RING);
+  // the block's queries (kShareQ) follow the rings, then the tree tables
+  static_assert(!kShareQ || (WK > 1 && WR > 1), "queries are shared between key groups");
+  constexpr bool qshare = kShareQ;
+  const bool qload = !qshare || wk == 0;  // this wave loads its queries from memory
+  unsigned char* qlds = smem + RING;
+  uint32_t* anc = reinterpret_cast<uint32_t*>(smem + RING + (qshare ? RB * D * 2 : 0));
   const int anc_nodes = RB / a.G + 2;
   int32_t* par = reinterpret_cast<int32_t*>(anc + anc_nodes * ntt);
   int* flag = par + a.N;
@@ -694,8 +699,10 @@ void attn_main(AttnArgs a) {
     const int node = ok ? r / a.G : 0;
     const int h = g * a.G + (ok ? r % a.G : 0);
     const __bf16* qp = a.q + ((size_t)(b * a.N + node) * a.Hq + h) * D + 8 * g4;
+    if (qload) {
 #pragma unroll
-    for (int c = 0; c < NC; ++c) qf[nt][c] = load_b128(qp + 32 * c);
+      for (int c = 0; c < NC; ++c) qf[nt][c] = load_b128(qp + 32 * c);
+    }
   }
 
 #pragma unroll
@@ -705,7 +712,7 @@ void attn_main(AttnArgs a) {
   // ---- tree structure: ancestor-or-self bitmask of this block's nodes
   if (has_tree) {
     // the parents are done once at most the queries and the DMAs are in flight
-    wait_vm_any(NQ + npro * PW);
+    wait_vm_any((qload ? NQ : 0) + npro * PW);
 #pragma unroll
     for (int k = 0; k < kParPerThread; ++k) loaded(pv[k]);
     int bad = 0;
@@ -736,15 +743,27 @@ void attn_main(AttnArgs a) {
   }
 
   // the queries are done once at most the DMAs are in flight; rows past the
-  // block's last row get zero queries
-  wait_vm_any(npro * PW);
+  // block's last row get zero queries.  Shared queries sit in LDS in the
+  // tile layout, one 32-row tile per row group, read like the K operand.
+  if (qload) {
+    wait_vm_any(npro * PW);
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt)
+    for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      loaded(qf[nt][c]);
-      if (!qok[nt]) qf[nt][c] = bf16x8{};
-    }
+      for (int c = 0; c < NC; ++c) {
+        loaded(qf[nt][c]);
+        if (!qok[nt]) qf[nt][c] = bf16x8{};
+      }
+  }
+  // (the other key groups read them after the first ring step's barrier)
+  unsigned char* qt = qlds + wr * TL::kBytes;
+  if (qshare && wk == 0) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+        *reinterpret_cast<bf16x8*>(qt + TL::off(16 * nt + l16, 4 * c + g4)) = qf[nt][c];
+  }
 
   // O^T accumulators, and l: row sums of the bf16 weights, accumulated on
   // the matrix cores as ones^T P^T so numerator and denominator see the same
@@ -796,10 +815,20 @@ void attn_main(AttnArgs a) {
     }
   };
   // Full cache tiles first, without masking; the tiles that need a mask
-  // (the cache tail, then the tree tiles) all come after them.
+  // (the cache tail, then the tree tiles) all come after them.  Shared
+  // queries are read behind the first step's workgroup barrier: every
+  // workgroup here has n_iter >= 1, so this loop always runs step 0.
+  auto shared_queries = [&]() {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+        qf[nt][c] = *reinterpret_cast<const bf16x8*>(qt + TL::off(16 * nt + l16, 4 * c + g4));
+  };
   int i = 0;
   for (; i < n_iter; ++i) {
     ring_step(i);
+    if (i == 0 && qshare && wk != 0) shared_queries();
     const int t = t0 + wk + WK * i;
     if (i >= n_mine || t >= nct || (t + 1) * kKeyTile > kvl) break;
     const MaskInfo mk{t, nct, kvl, ntt, g4, a.tail, anc};
@@ -987,6 +1016,16 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
              bad != 0);
 }
 
+template <int D, int WR, int WK, int NS, bool kPaged, bool kShareQ>
+static hipError_t launch_main(const AttnArgs& a, const AttnPlan& p, hipStream_t st) {
+  hipError_t e = hipFuncSetAttribute((const void*)attn_main<D, WR, WK, NS, kPaged, kShareQ>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)p.lds_bytes);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((attn_main<D, WR, WK, NS, kPaged, kShareQ>), dim3(p.grid), dim3(64 * WR * WK),
+                     p.lds_bytes, st, a);
+  return hipGetLastError();
+}
+
 template <int D, int ARR, bool kPaged>
 static hipError_t launch_attn_t(const AttnArgs& a, const AttnPlan& p, hipStream_t st) {
   constexpr Arrangement ar = kArrangements[ARR];
@@ -994,13 +1033,14 @@ static hipError_t launch_attn_t(const AttnArgs& a, const AttnPlan& p, hipStream_
   if constexpr (NS == 0) {
     return hipErrorInvalidValue;  // never planned: the ring does not fit
   } else {
-    hipError_t e = hipFuncSetAttribute((const void*)attn_main<D, ar.WR, ar.WK, NS, kPaged>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       (int)p.lds_bytes);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((attn_main<D, ar.WR, ar.WK, NS, kPaged>), dim3(p.grid), dim3(64 * ar.WR * ar.WK),
-                       p.lds_bytes, st, a);
-    e = hipGetLastError();
+    // query sharing is a separate instantiation, so the kernels without it
+    // carry none of its code or scalar registers
+    hipError_t e;
+    if constexpr (ar.WK > 1 && ar.WR > 1)
+      e = p.qshare ? launch_main<D, ar.WR, ar.WK, NS, kPaged, true>(a, p, st)
+                   : launch_main<D, ar.WR, ar.WK, NS, kPaged, false>(a, p, st);
+    else
+      e = launch_main<D, ar.WR, ar.WK, NS, kPaged, false>(a, p, st);
     if (e != hipSuccess || p.S == 1 || p.fused) return e;
     constexpr int RB = kRowsPerWave * ar.WR;
     const int frags = a.B * a.Hkv * p.nRB * (D / 16) * (RB / 16);

@@ -53,12 +53,15 @@ struct AttnPlan {
   int spread;                  // work order of several sequences (below)
   size_t ws_o_bytes, ws_ml_bytes, ws_sync_bytes, ws_bytes;
   size_t lds_bytes;            // dynamic LDS of the main kernel
+  int qshare;                  // key group 0 loads the queries, the others read them from LDS
 };
 
-inline size_t attn_lds_bytes(int D, int WR, int WK, int NS, int G, int N) {
+// Dynamic LDS of the main kernel: the rings, then (qshare) the block's
+// queries, then the tree tables; the key-group merge reuses it afterwards.
+inline size_t attn_lds_bytes(int D, int WR, int WK, int NS, int G, int N, bool qshare) {
   const int RB = kRowsPerWave * WR;
   const size_t stage = 2 * (size_t)kKeyTile * 2 * D;
-  const size_t ring = (size_t)WK * NS * stage;
+  const size_t ring = (size_t)WK * NS * stage + (qshare ? (size_t)RB * D * 2 : 0);
   const int words = cdiv(N, 32);
   const int nodes = RB / G + 2;
   const size_t tree = (size_t)nodes * words * 4 + (size_t)N * 4 + 16;
@@ -114,7 +117,22 @@ inline AttnPlan attn_plan_arr(int B, int N, int Hq, int Hkv, int D, int Lmax, in
   // 16 x 64 nodes (Hq 32, Hkv 4) in the kernel: 1.2% faster than its merge
   // kernel, which had to wait for the slowest sequence.
   p.fused = p.S > 1 && (size_t)p.S * p.RB * D * 4 <= (size_t)kFusedMergeBytes * p.threads;
-  p.lds_bytes = p.NS > 0 ? attn_lds_bytes(D, ar.WR, ar.WK, p.NS, p.G, N) : kMaxLds + 1;
+  // With several key groups every one of them needs the block's queries.
+  // When the grid fills every CU, key group 0 loads them and shares them
+  // through LDS where that fits: the other groups' copies were 64 KB of
+  // requests per workgroup ahead of the first tiles at the Qwen3-8B-shaped
+  // 64-node call (2 x 4 waves; 2% faster shared).  On a GPU left mostly
+  // idle the copies cost nothing and the LDS hop only adds latency (3%
+  // slower for a grid of two workgroups).
+  p.qshare = 0;
+  p.lds_bytes = p.NS > 0 ? attn_lds_bytes(D, ar.WR, ar.WK, p.NS, p.G, N, false) : kMaxLds + 1;
+  if (p.NS > 0 && ar.WK > 1 && ar.WR > 1 && p.nwork >= 256LL * p.wg_per_cu) {
+    const size_t with_q = attn_lds_bytes(D, ar.WR, ar.WK, p.NS, p.G, N, true);
+    if (with_q * p.wg_per_cu <= kMaxLds) {
+      p.qshare = 1;
+      p.lds_bytes = with_q;
+    }
+  }
   // Workgroups go to the XCDs round-robin, and the row blocks of one
   // (sequence, KV head, chunk) read the same keys, so they stay on one XCD
   // (its L2).  With one sequence, XCD x takes a contiguous run of work

@@ -158,23 +158,31 @@ __device__ __forceinline__ unsigned long long scan_slice(const AcceptArgs& a, in
 constexpr int kFinishThreads = 512;
 static_assert(kMaxNodes % kFinishThreads == 0, "whole node batches per thread");
 
-// Per-node LDS arrays of one sequence's acceptance (accept_lds_bytes).
+// Per-node LDS arrays of one sequence's acceptance (accept_lds_bytes): the
+// prediction, the parent, and the pointer-jumping state packed into one
+// word per node (double-buffered), so a round reads a node's whole state
+// and its jump target's with one access each.
 struct SeqLds {
   int* tgt;
-  short *jmp0, *jmp1, *dep0, *dep1, *par;
-  unsigned char *ok0, *ok1;
+  short* par;
+  unsigned int *st0, *st1;
 };
+
+// state word: jump target (bits 0-10), path length to it (bits 11-22),
+// every node on that stretch matches the prediction at its parent (bit 23)
+constexpr unsigned int kJmpMask = 0x7FFu, kDepShift = 11, kDepMask = 0xFFFu, kOkBit = 1u << 23;
+static_assert(kMaxNodes - 1 <= (int)kJmpMask && kMaxNodes - 1 <= (int)kDepMask, "state word fields");
+
+__device__ __forceinline__ unsigned int pack_state(unsigned int jmp, unsigned int dep, bool ok) {
+  return jmp | (dep << kDepShift) | (ok ? kOkBit : 0u);
+}
 
 __device__ __forceinline__ SeqLds seq_lds(unsigned char* base, int N) {
   SeqLds l;
-  l.tgt = reinterpret_cast<int*>(base);
-  l.jmp0 = reinterpret_cast<short*>(base + 4 * (size_t)N);
-  l.jmp1 = l.jmp0 + N;
-  l.dep0 = l.jmp1 + N;
-  l.dep1 = l.dep0 + N;
-  l.par = l.dep1 + N;
-  l.ok0 = reinterpret_cast<unsigned char*>(l.par + N);
-  l.ok1 = l.ok0 + N;
+  l.st0 = reinterpret_cast<unsigned int*>(base);
+  l.st1 = l.st0 + N;
+  l.tgt = reinterpret_cast<int*>(l.st1 + N);
+  l.par = reinterpret_cast<short*>(l.tgt + N);
   return l;
 }
 
@@ -216,42 +224,45 @@ __device__ __forceinline__ void accept_sequence(const AcceptArgs& a, int b, cons
       if (i >= N) break;
       // the root (par = -1) jumps to itself
       const int p = i == 0 ? 0 : l.par[i];
-      l.ok0[i] = i == 0 ? 1 : dv[k] == l.tgt[p];
-      l.jmp0[i] = (short)p;
-      l.dep0[i] = i == 0 ? 0 : 1;
+      l.st0[i] = pack_state((unsigned int)p, i == 0 ? 0u : 1u, i == 0 || dv[k] == l.tgt[p]);
     }
     __syncthreads();
-    // pointer jumping: afterwards jmp = root, dep = depth and ok = every
-    // node on the root path matches the prediction at its parent.  Jumps
-    // double each round, so ceil(log2(kMaxNodes)) = 11 rounds reach the
-    // root from any node; the round cap only bounds the loop.
+    // pointer jumping: afterwards every node jumps to the root with its
+    // depth, and ok = every node on its root path matches the prediction at
+    // its parent.  Jumps double each round, so ceil(log2(kMaxNodes)) = 11
+    // rounds reach the root from any node; the round cap only bounds the loop.
     int cur = 0, more, rounds = 0;
     do {
-      const short* jc = cur ? l.jmp1 : l.jmp0;
-      const short* dc = cur ? l.dep1 : l.dep0;
-      const unsigned char* oc = cur ? l.ok1 : l.ok0;
-      short* jn = cur ? l.jmp0 : l.jmp1;
-      short* dn = cur ? l.dep0 : l.dep1;
-      unsigned char* on = cur ? l.ok0 : l.ok1;
+      const unsigned int* sc = cur ? l.st1 : l.st0;
+      unsigned int* sn = cur ? l.st0 : l.st1;
       more = 0;
       for (int i = tid; i < N; i += kFinishThreads) {
-        const int j = jc[i];
-        on[i] = oc[i] & oc[j];
-        dn[i] = dc[i] + dc[j];
-        jn[i] = jc[j];
-        more |= jc[j] != 0;
+        const unsigned int wi = sc[i];
+        const unsigned int wj = sc[wi & kJmpMask];
+        const unsigned int jn = wj & kJmpMask;
+        const unsigned int dep = ((wi >> kDepShift) & kDepMask) + ((wj >> kDepShift) & kDepMask);
+        sn[i] = pack_state(jn, dep, (wi & wj & kOkBit) != 0);
+        more |= jn != 0;
       }
       cur ^= 1;
     } while (__syncthreads_or(more) && ++rounds < 16);
-    const short* dc = cur ? l.dep1 : l.dep0;
-    const unsigned char* oc = cur ? l.ok1 : l.ok0;
+    const unsigned int* sc = cur ? l.st1 : l.st0;
     unsigned int mk = 0u;
-    for (int i = tid; i < N; i += kFinishThreads)
-      if (oc[i]) {
-        const unsigned int k = ((unsigned int)dc[i] << 16) | (0xFFFFu - (unsigned int)i);
+    for (int i = tid; i < N; i += kFinishThreads) {
+      const unsigned int w = sc[i];
+      if (w & kOkBit) {
+        const unsigned int k = (((w >> kDepShift) & kDepMask) << 16) | (0xFFFFu - (unsigned int)i);
         mk = mk > k ? mk : k;
       }
-    atomicMax(&best_key, mk);  // LDS atomic, one per thread
+    }
+    // the wave's maximum first: same-address LDS atomics serialise, and one
+    // per thread took 2 us of the 512-node acceptance
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      const unsigned int other = __shfl_xor(mk, o);
+      mk = other > mk ? other : mk;
+    }
+    if ((tid & 63) == 0) atomicMax(&best_key, mk);
     __syncthreads();
   }
   const unsigned int bk = best_key;

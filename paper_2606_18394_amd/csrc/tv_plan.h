@@ -343,10 +343,9 @@ inline SamplePlan sample_plan(int B, int N, int V) {
   return p;
 }
 
-// LDS of the acceptance of one sequence of N nodes: per node the target
-// argmax (int), jump pointers and depths (2 x 2 short, double-buffered),
-// parent (short) and acceptance flags (2 bytes); the finish kernel adds the
-// merged 64-bit key per node.
-constexpr size_t accept_lds_bytes(int N) { return (size_t)N * 16 + 16; }
+// LDS of the acceptance of one sequence of N nodes: per node the
+// pointer-jumping state (two packed 32-bit words, double-buffered), the
+// target argmax (int) and the parent (short).
+constexpr size_t accept_lds_bytes(int N) { return (size_t)N * 14 + 16; }
 
 }  // namespace tv

@@ -31,6 +31,7 @@
 #include <stdint.h>
 
 #include "tv_plan.h"
+#include "tv_walk.h"
 
 namespace tv {
 
@@ -168,15 +169,6 @@ struct SeqLds {
   unsigned int *st0, *st1;
 };
 
-// state word: jump target (bits 0-10), path length to it (bits 11-22),
-// every node on that stretch matches the prediction at its parent (bit 23)
-constexpr unsigned int kJmpMask = 0x7FFu, kDepShift = 11, kDepMask = 0xFFFu, kOkBit = 1u << 23;
-static_assert(kMaxNodes - 1 <= (int)kJmpMask && kMaxNodes - 1 <= (int)kDepMask, "state word fields");
-
-__device__ __forceinline__ unsigned int pack_state(unsigned int jmp, unsigned int dep, bool ok) {
-  return jmp | (dep << kDepShift) | (ok ? kOkBit : 0u);
-}
-
 __device__ __forceinline__ SeqLds seq_lds(unsigned char* base, int N) {
   SeqLds l;
   l.st0 = reinterpret_cast<unsigned int*>(base);
@@ -237,31 +229,21 @@ __device__ __forceinline__ void accept_sequence(const AcceptArgs& a, int b, cons
       unsigned int* sn = cur ? l.st0 : l.st1;
       more = 0;
       for (int i = tid; i < N; i += kFinishThreads) {
-        const unsigned int wi = sc[i];
-        const unsigned int wj = sc[wi & kJmpMask];
-        const unsigned int jn = wj & kJmpMask;
-        const unsigned int dep = ((wi >> kDepShift) & kDepMask) + ((wj >> kDepShift) & kDepMask);
-        sn[i] = pack_state(jn, dep, (wi & wj & kOkBit) != 0);
-        more |= jn != 0;
+        const unsigned int w = jump_state(sc, i);
+        sn[i] = w;
+        more |= (w & kJmpMask) != 0;
       }
       cur ^= 1;
     } while (__syncthreads_or(more) && ++rounds < 16);
     const unsigned int* sc = cur ? l.st1 : l.st0;
     unsigned int mk = 0u;
     for (int i = tid; i < N; i += kFinishThreads) {
-      const unsigned int w = sc[i];
-      if (w & kOkBit) {
-        const unsigned int k = (((w >> kDepShift) & kDepMask) << 16) | (0xFFFFu - (unsigned int)i);
-        mk = mk > k ? mk : k;
-      }
+      const unsigned int k = deepest_key(sc[i], i);
+      mk = mk > k ? mk : k;
     }
     // the wave's maximum first: same-address LDS atomics serialise, and one
     // per thread took 2 us of the 512-node acceptance
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-      const unsigned int other = __shfl_xor(mk, o);
-      mk = other > mk ? other : mk;
-    }
+    mk = wave_max_u32(mk);
     if ((tid & 63) == 0) atomicMax(&best_key, mk);
     __syncthreads();
   }

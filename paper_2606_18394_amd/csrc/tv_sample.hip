@@ -39,6 +39,7 @@
 #include <stdint.h>
 
 #include "tv_plan.h"
+#include "tv_walk.h"
 
 namespace tv {
 
@@ -241,9 +242,8 @@ __global__ __launch_bounds__(kSampleThreads) void sample_accept(SampleArgs a, in
   __shared__ int start[kMaxNodes + 1];   // per parent: first slot of its children
   __shared__ short grp[kMaxNodes], srt[kMaxNodes];  // children by parent: any order, index order
   __shared__ int wsum[kSampleThreads / 64];
-  __shared__ short par[kMaxNodes], jmp0[kMaxNodes], jmp1[kMaxNodes], dep0[kMaxNodes],
-      dep1[kMaxNodes];
-  __shared__ unsigned char ok0[kMaxNodes], ok1[kMaxNodes];
+  __shared__ short par[kMaxNodes];
+  __shared__ unsigned int st0[kMaxNodes], st1[kMaxNodes];  // pointer-jumping state words
   __shared__ unsigned int mask[kRaceSlice / 32];  // child tokens of the last node, this slice
   __shared__ unsigned int best_key;
   __shared__ unsigned long long red[2][kSampleThreads / 64];
@@ -384,9 +384,8 @@ __global__ __launch_bounds__(kSampleThreads) void sample_accept(SampleArgs a, in
       const int i = tid + kSampleThreads * k;
       if (i < N) {
         // the root (par = 0 here) jumps to itself
-        ok0[i] = i == 0 ? 1 : (pass[k] && first_pass[par[i]] == i);
-        jmp0[i] = par[i];
-        dep0[i] = i == 0 ? 0 : 1;
+        st0[i] = pack_state((unsigned int)par[i], i == 0 ? 0u : 1u,
+                            i == 0 || (pass[k] && first_pass[par[i]] == i));
       }
     }
     __syncthreads();
@@ -394,32 +393,26 @@ __global__ __launch_bounds__(kSampleThreads) void sample_accept(SampleArgs a, in
     // root path selected; 11 rounds reach the root from any of 2048 nodes
     int cur = 0, more, rounds = 0;
     do {
-      const short* jc = cur ? jmp1 : jmp0;
-      const short* dc = cur ? dep1 : dep0;
-      const unsigned char* oc = cur ? ok1 : ok0;
-      short* jn = cur ? jmp0 : jmp1;
-      short* dn = cur ? dep0 : dep1;
-      unsigned char* on = cur ? ok0 : ok1;
+      const unsigned int* sc = cur ? st1 : st0;
+      unsigned int* sn = cur ? st0 : st1;
       more = 0;
       for (int i = tid; i < N; i += kSampleThreads) {
-        const int j = jc[i];
-        on[i] = oc[i] & oc[j];
-        dn[i] = dc[i] + dc[j];
-        jn[i] = jc[j];
-        more |= jc[j] != 0;
+        const unsigned int w = jump_state(sc, i);
+        sn[i] = w;
+        more |= (w & kJmpMask) != 0;
       }
       cur ^= 1;
     } while (__syncthreads_or(more) && ++rounds < 16);
-    const short* depth = cur ? dep1 : dep0;
-    const unsigned char* acc = cur ? ok1 : ok0;
+    const unsigned int* sc = cur ? st1 : st0;
     // the selected nodes form one chain from the root: its deepest node
+    // (the wave's maximum first; one LDS atomic per wave)
     unsigned int mk = 0u;
-    for (int i = tid; i < N; i += kSampleThreads)
-      if (acc[i]) {
-        const unsigned int k = ((unsigned int)depth[i] << 16) | (0xFFFFu - (unsigned int)i);
-        mk = mk > k ? mk : k;
-      }
-    atomicMax(&best_key, mk);
+    for (int i = tid; i < N; i += kSampleThreads) {
+      const unsigned int k = deepest_key(sc[i], i);
+      mk = mk > k ? mk : k;
+    }
+    mk = wave_max_u32(mk);
+    if (lane == 0) atomicMax(&best_key, mk);
     __syncthreads();
     const unsigned int bk = best_key;
     dv = (int)(bk >> 16);

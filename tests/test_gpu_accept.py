@@ -155,3 +155,13 @@ def test_node_counts_around_the_one_wave_limits(N):
     inp["parent"][2, N - 1] = N - 1          # invalid: a node its own parent
     ln = _compare(inp, draft, N)
     assert ln[2] == -1
+
+
+@pytest.mark.parametrize("N", [129, 300])
+def test_finish_with_most_split_keys(N):
+    """One sequence over a large f32 vocabulary: the most vocabulary splits
+    the plan gives (16 at 129 nodes), so the finish of trees over 128 nodes
+    merges its largest number of split keys per node."""
+    rng = np.random.default_rng(700 + N)
+    inp = _small(rng, 1, N, 151936, "f32", depth=12, width=5)
+    _compare(inp, oracle_draft_tokens(inp), 16)

@@ -73,6 +73,14 @@ int main() {
       }
     }
     if (p.lds_bytes > 160 * 1024) ok = false;
+    // shared queries: several key groups of several waves, a grid that
+    // fills every CU, and the queries' LDS counted in the kernel's
+    if (p.qshare) {
+      if (p.WK < 2 || p.WR < 2 || p.nwork < 256LL * p.wg_per_cu) ok = false;
+      if (p.lds_bytes != tv::attn_lds_bytes(D, p.WR, p.WK, p.NS, p.G, N, true)) ok = false;
+    } else if (p.NS > 0 && p.lds_bytes != tv::attn_lds_bytes(D, p.WR, p.WK, p.NS, p.G, N, false)) {
+      ok = false;
+    }
     for (int esize : {2, 4})
       for (int vec : {1, 16 / esize}) {
         const tv::AcceptPlan ap = tv::accept_plan(B, N, V, esize, vec);

@@ -17,11 +17,15 @@
 // groups that share out the chunk's tiles, each streaming its tiles through
 // an LDS ring of NS stages; key groups merge their softmax states in LDS at
 // the end.  The host plan (tv_plan.h) picks WR, WK, NS and S per shape so
-// that every CU holds 8 waves (two per SIMD).
+// that every CU holds 8 waves (two per SIMD).  The prologue requests the
+// parents, the queries and every ring stage before it uses any of them;
+// with several key groups on a full grid, key group 0 alone loads the
+// queries and hands them to the others through LDS.
 //
 // Per tile.  K and V move HBM -> LDS with global_load_lds_dwordx4 (no
-// register staging), rows XOR-swizzled in 16-byte chunks so the reads below
-// are free of bank conflicts.  A wave computes S^T = K Q^T with
+// register staging), rows XOR-swizzled in 16-byte chunks so the transposing
+// V reads are free of bank conflicts and the K reads at most two-way (see
+// TileLayout).  A wave computes S^T = K Q^T with
 // v_mfma_f32_16x16x32_bf16 (keys on the M side, its 32 rows on the N side),
 // runs an fp32 base-2 online softmax on the accumulators with a lazily moved
 // reference maximum, and accumulates O^T += V^T P^T: P^T comes straight from
@@ -29,9 +33,10 @@
 // data movement) and V^T from ds_read_b64_tr_b16 transposing reads.
 //
 // Split-KV merge (S > 1).  Every chunk stores its (max, sum, O) partial.
-// When one workgroup can merge a row block in one batch of loads, the
-// chunk that finishes last does it inside this kernel (arrival counters in
-// the workspace); otherwise a second kernel merges all row blocks.
+// When one workgroup can merge a row block with at most two batches of
+// loads, the chunk that finishes last does it inside this kernel (arrival
+// counters in the workspace); otherwise a second kernel merges all row
+// blocks.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>

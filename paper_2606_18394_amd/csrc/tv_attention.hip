@@ -98,6 +98,37 @@ __device__ __forceinline__ Segment segment(const AttnArgs& a, int b, int i_hi) {
   return sg;
 }
 
+// Longest-first order of a ragged batch (spread = 2).  XCD x serves one KV
+// head and lane x / Hkv of L = 8 / Hkv lanes of chunks; pair p of the lane
+// is sequence p / (S / L) and its (p % (S / L))-th chunk in that lane, as in
+// work_item.  Every wave of the workgroup ranks the lane's pairs (at most
+// 64, one per lane) by their tile count, longest first and lower pair index
+// on ties, and the workgroup takes the pair whose rank is its own pair
+// index.  The ranking is the same in every workgroup, so this permutes the
+// pairs: every work item is still covered once.
+__device__ __forceinline__ void longest_first(const AttnArgs& a, int bid, WorkItem& it) {
+  const int lane = threadIdx.x & 63;
+  const int L = kXcds / a.Hkv, per_b = a.S / L, npairs = a.B * per_b;
+  const int x = bid % kXcds, target = (bid / kXcds) / a.nRB, ln = x / a.Hkv;
+  int key = -1;
+  if (lane < npairs) {
+    const int pb = lane / per_b;
+    const int ps = ((ln - pb) % L + L) % L + L * (lane % per_b);
+    const int cap = a.tail ? a.Lmax - a.N : a.Lmax;
+    int kvl = a.kv_len ? a.kv_len[pb] : cap;
+    kvl = kvl < 0 ? 0 : (kvl > cap ? cap : kvl);
+    const int tiles = (kvl + kKeyTile - 1) / kKeyTile + (a.N - 1) / kKeyTile + 1;
+    const int work = max(0, min(a.chunk, tiles - ps * a.chunk));
+    key = work * 64 + (63 - lane);  // distinct keys
+  }
+  int rank = 0;
+  for (int q = 0; q < 64; ++q) rank += __shfl(key, q) > key;
+  const unsigned long long hit = __ballot(lane < npairs && rank == target);
+  const int p = __builtin_amdgcn_readfirstlane(hit ? (int)__builtin_ctzll(hit) : 0);
+  it.b = p / per_b;
+  it.s = ((ln - it.b) % L + L) % L + L * (p % per_b);
+}
+
 // Four output values, or four NaN when the sequence's tree is invalid (the
 // NaN is written as a bit pattern: the kernels assume no NaN arithmetic).
 __device__ __forceinline__ void store_out4(__bf16* p, const f32x4& acc, float inv, bool nan) {
@@ -603,6 +634,7 @@ void attn_main(AttnArgs a) {
 
   WorkItem it{};
   if (!work_item(gridDim.x, a.nwork, a.S, a.nRB, a.spread, a.B, a.Hkv, blockIdx.x, it)) return;
+  if (a.spread == 2) longest_first(a, blockIdx.x, it);
   const int s = it.s, rb = it.rb, g = it.g, b = it.b;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);

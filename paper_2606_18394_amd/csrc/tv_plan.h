@@ -142,12 +142,21 @@ inline AttnPlan attn_plan_arr(int B, int N, int Hq, int Hkv, int D, int Lmax, in
   // sequence b goes to lane (b + s) % L.  Every XCD then sees every
   // sequence.  This needs Hkv to divide 8 and L to divide S.
   p.spread = B > 1 && kXcds % Hkv == 0 && p.S % (kXcds / Hkv) == 0;
+  // Within an XCD workgroups start in index order as slots free up, so a
+  // long chunk that starts in a late round sets the kernel's end.  When an
+  // XCD's (sequence, chunk) pairs fit one wave, each workgroup ranks them by
+  // their tile counts (from kv_len, on the device) and takes the pair whose
+  // rank is its position: the longest chunks start first (spread = 2).
+  if (p.spread && (long long)B * (p.S / (kXcds / Hkv)) <= 64) p.spread = 2;
   return p;
 }
 
 // The work item (sequence b, KV head g, row block rb, chunk s) of launched
 // workgroup `bid`; false for padding workgroups past the work.  constexpr,
-// so the kernels and the host checks decode with this same function.
+// so the kernels and the host checks decode with this same function.  With
+// spread = 2 the kernel then replaces the (b, s) pair by the pair of the
+// same XCD lane whose length rank is this one's index: a permutation of the
+// lane's pairs, so every work item is still covered once.
 struct WorkItem {
   int b, g, rb, s;
 };

@@ -101,30 +101,57 @@ __device__ __forceinline__ Segment segment(const AttnArgs& a, int b, int i_hi) {
 // Longest-first order of a ragged batch (spread = 2).  XCD x serves one KV
 // head and lane x / Hkv of L = 8 / Hkv lanes of chunks; pair p of the lane
 // is sequence p / (S / L) and its (p % (S / L))-th chunk in that lane, as in
-// work_item.  Every wave of the workgroup ranks the lane's pairs (at most
-// 64, one per lane) by their tile count, longest first and lower pair index
-// on ties, and the workgroup takes the pair whose rank is its own pair
-// index.  The ranking is the same in every workgroup, so this permutes the
-// pairs: every work item is still covered once.
+// work_item.  Each pair gets the distinct key (tile count << 16 | 0xFFFF - p)
+// (longest first, lower pair index on ties), and the workgroup takes the
+// pair whose key is the (i+1)-th largest, i its own pair index: with one
+// pair per lane by counting larger keys over lane exchanges, else by
+// bisection on the key value with wave-wide counts (each lane holds up to
+// kRankPerLane pairs).  Every workgroup finds the same order, so this
+// permutes the pairs: every work item is still covered once.
+constexpr int kRankPerLane = 16;  // == kMaxRankPairs / 64 in tv_plan.h
+
 __device__ __forceinline__ void longest_first(const AttnArgs& a, int bid, WorkItem& it) {
   const int lane = threadIdx.x & 63;
   const int L = kXcds / a.Hkv, per_b = a.S / L, npairs = a.B * per_b;
   const int x = bid % kXcds, target = (bid / kXcds) / a.nRB, ln = x / a.Hkv;
-  int key = -1;
-  if (lane < npairs) {
-    const int pb = lane / per_b;
-    const int ps = ((ln - pb) % L + L) % L + L * (lane % per_b);
-    const int cap = a.tail ? a.Lmax - a.N : a.Lmax;
-    int kvl = a.kv_len ? a.kv_len[pb] : cap;
-    kvl = kvl < 0 ? 0 : (kvl > cap ? cap : kvl);
-    const int tiles = (kvl + kKeyTile - 1) / kKeyTile + (a.N - 1) / kKeyTile + 1;
-    const int work = max(0, min(a.chunk, tiles - ps * a.chunk));
-    key = work * 64 + (63 - lane);  // distinct keys
+  const int cap = a.tail ? a.Lmax - a.N : a.Lmax;
+  int key[kRankPerLane];
+#pragma unroll
+  for (int k = 0; k < kRankPerLane; ++k) {
+    const int p = lane + 64 * k;
+    key[k] = -1;
+    if (p < npairs) {
+      const int pb = p / per_b;
+      const int ps = ((ln - pb) % L + L) % L + L * (p % per_b);
+      int kvl = a.kv_len ? a.kv_len[pb] : cap;
+      kvl = kvl < 0 ? 0 : (kvl > cap ? cap : kvl);
+      const int tiles = (kvl + kKeyTile - 1) / kKeyTile + (a.N - 1) / kKeyTile + 1;
+      const int work = max(0, min(a.chunk, tiles - ps * a.chunk));  // < 2^14 (plan)
+      key[k] = (work << 16) | (0xFFFF - p);
+    }
   }
-  int rank = 0;
-  for (int q = 0; q < 64; ++q) rank += __shfl(key, q) > key;
-  const unsigned long long hit = __ballot(lane < npairs && rank == target);
-  const int p = __builtin_amdgcn_readfirstlane(hit ? (int)__builtin_ctzll(hit) : 0);
+  int p;
+  const int nk = (npairs + 63) / 64;  // pair slots in use per lane
+  if (nk == 1) {
+    // one pair per lane: every lane counts the larger keys by lane exchanges
+    int rank = 0;
+    for (int q = 0; q < 64; ++q) rank += __shfl(key[0], q) > key[0];
+    const unsigned long long hit = __ballot(lane < npairs && rank == target);
+    p = __builtin_amdgcn_readfirstlane(hit ? (int)__builtin_ctzll(hit) : 0);
+  } else {
+    // the largest v with at least target + 1 keys >= v is the wanted key
+    int lo = 0, hi = 1 << 30;
+    while (hi - lo > 1) {
+      const int mid = lo + ((hi - lo) >> 1);
+      int c = 0;
+#pragma unroll
+      for (int k = 0; k < kRankPerLane; ++k)
+        if (k < nk) c += __popcll(__ballot(key[k] >= mid));
+      if (c >= target + 1) lo = mid;
+      else hi = mid;
+    }
+    p = 0xFFFF - (lo & 0xFFFF);
+  }
   it.b = p / per_b;
   it.s = ((ln - it.b) % L + L) % L + L * (p % per_b);
 }

@@ -8,6 +8,7 @@ namespace tv {
 
 constexpr int kKeyTile = 32;       // keys one wave consumes per step
 constexpr int kXcds = 8;           // MI355X accelerator complex dies
+constexpr int kMaxRankPairs = 1024;  // longest-first ranking: pairs per XCD lane (16 per lane)
 constexpr int kMaxNodes = 2048;    // == TV_MAX_NODES
 
 inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
@@ -144,10 +145,12 @@ inline AttnPlan attn_plan_arr(int B, int N, int Hq, int Hkv, int D, int Lmax, in
   p.spread = B > 1 && kXcds % Hkv == 0 && p.S % (kXcds / Hkv) == 0;
   // Within an XCD workgroups start in index order as slots free up, so a
   // long chunk that starts in a late round sets the kernel's end.  When an
-  // XCD's (sequence, chunk) pairs fit one wave, each workgroup ranks them by
-  // their tile counts (from kv_len, on the device) and takes the pair whose
-  // rank is its position: the longest chunks start first (spread = 2).
-  if (p.spread && (long long)B * (p.S / (kXcds / Hkv)) <= 64) p.spread = 2;
+  // XCD's (sequence, chunk) pairs fit the ranking (kMaxRankPairs, tile
+  // counts below 2^14), each workgroup ranks them by their tile counts (from
+  // kv_len, on the device) and takes the pair whose rank is its position:
+  // the longest chunks start first (spread = 2).
+  if (p.spread && (long long)B * (p.S / (kXcds / Hkv)) <= kMaxRankPairs && p.chunk < (1 << 14))
+    p.spread = 2;
   return p;
 }
 

@@ -347,7 +347,7 @@ def algorithmic_work(inp, w):
 
 def kernel_source_sha():
     h = hashlib.sha256()
-    for f in ["tv_attention.hip", "tv_accept.hip", "tv_plan.h", "tv_walk.h"]:
+    for f in ["tv_attention.hip", "tv_accept.hip", "tv_plan.h", "tv_walk.h", "tv_stream.h"]:
         with open(os.path.join(ROOT, "paper_2606_18394_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

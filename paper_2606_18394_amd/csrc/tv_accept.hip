@@ -31,6 +31,7 @@
 #include <stdint.h>
 
 #include "tv_plan.h"
+#include "tv_stream.h"
 #include "tv_walk.h"
 
 namespace tv {
@@ -121,7 +122,7 @@ __device__ __forceinline__ unsigned long long scan_slice(const AcceptArgs& a, in
 #pragma unroll
       for (int u = 0; u < L; ++u) {
         const long long cu = c + (long long)u * kAcceptScanThreads;
-        if (cu < c1) w[u] = base[cu];
+        if (cu < c1) w[u] = load_stream(base + cu);
       }
 #pragma unroll
       for (int u = 0; u < L; ++u) {
@@ -133,10 +134,10 @@ __device__ __forceinline__ unsigned long long scan_slice(const AcceptArgs& a, in
     for (long long c = c0 + tid; c < c1; c += kAcceptScanThreads) {
       float x;
       if (F32) {
-        x = reinterpret_cast<const float*>(a.logits)[(size_t)row * a.V + c];
+        x = load_stream(reinterpret_cast<const float*>(a.logits) + (size_t)row * a.V + c);
       } else {
         const unsigned short h =
-            reinterpret_cast<const unsigned short*>(a.logits)[(size_t)row * a.V + c];
+            load_stream(reinterpret_cast<const unsigned short*>(a.logits) + (size_t)row * a.V + c);
         x = __uint_as_float((unsigned int)h << 16);
       }
       best.see(x, (unsigned int)c);

@@ -26,6 +26,7 @@
 #include <stdint.h>
 
 #include "tv_plan.h"
+#include "tv_stream.h"
 
 namespace tv {
 
@@ -179,11 +180,11 @@ __global__ __launch_bounds__(kScanThreads) void topw_scan(TopwArgs a) {
       const long long cu = c + (long long)u * kScanThreads;
       const long long cl = cu < c1 ? cu : c1 - 1;
       if (VEC) {
-        raw[u] = reinterpret_cast<const uint4*>(rowp)[cl];
+        raw[u] = load_stream(reinterpret_cast<const uint4*>(rowp) + cl);
       } else if (F32) {
-        raw[u].x = reinterpret_cast<const unsigned int*>(rowp)[cl];
+        raw[u].x = load_stream(reinterpret_cast<const unsigned int*>(rowp) + cl);
       } else {
-        raw[u].x = (unsigned int)reinterpret_cast<const unsigned short*>(rowp)[cl] << 16;
+        raw[u].x = (unsigned int)load_stream(reinterpret_cast<const unsigned short*>(rowp) + cl) << 16;
       }
     }
     float x[L][E];

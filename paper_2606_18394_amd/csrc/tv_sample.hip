@@ -39,6 +39,7 @@
 #include <stdint.h>
 
 #include "tv_plan.h"
+#include "tv_stream.h"
 #include "tv_walk.h"
 
 namespace tv {
@@ -160,7 +161,7 @@ __device__ __forceinline__ void lse_slice(const void* rowp, long long x0, long l
 #pragma unroll
       for (int u = 0; u < L; ++u) {
         const long long cu = c + (long long)u * kScanThreads;
-        raw[u] = base[cu < c1 ? cu : c1 - 1];
+        raw[u] = load_stream(base + (cu < c1 ? cu : c1 - 1));
       }
       float x[L][E];
 #pragma unroll

@@ -61,6 +61,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--settle-ms", type=float, default=200.0,
+                    help="untimed replays of each timed graph for at least this long before its "
+                         "timed region, so the GPU clock has left its idle ramp")
     ap.add_argument("--workload", default=HEADLINE,
                     help="headline workload (default: the largest, big_tree_32b)")
     ap.add_argument("--core-only", action="store_true",
@@ -473,11 +476,15 @@ class Timer:
     input replicas in turn; k timed calls are k // R replays of that graph
     and one replay of a graph of its first k % R calls, so exactly k calls
     are timed and the timed region measures the GPU, not Python's launch
-    overhead.  Two untimed replays come first, so the first timed call finds
-    its replica least recently used."""
+    overhead.  Untimed replays come first, for at least `settle_s` seconds:
+    the shader clock ramps up over the first tens of milliseconds of work
+    after the GPU has idled (graph capture idles it), and the timed region
+    should see the clock a continuously running step sees.  They end with a
+    whole replay, so the first timed call finds its replica least recently
+    used."""
 
-    def __init__(self, torch, R):
-        self.torch, self.R, self.graphs = torch, R, {}
+    def __init__(self, torch, R, settle_s=0.2):
+        self.torch, self.R, self.graphs, self.settle_s = torch, R, {}, settle_s
 
     def _cap(self, fn, rs):
         g = self.torch.cuda.CUDAGraph()
@@ -496,8 +503,13 @@ class Timer:
         rem = k % R
         if rem and rem not in heads:
             heads[rem] = self._cap(fn, range(rem))
-        for _ in range(2):             # untimed graph warmup
+        t0 = time.perf_counter()
+        n = 0
+        while n < 2 or time.perf_counter() - t0 < self.settle_s:   # untimed replays
             full.replay()
+            n += 1
+            if n % 8 == 0:
+                torch.cuda.synchronize()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
@@ -590,7 +602,7 @@ def run_workload(name, args, extras, cpu_leg):
     torch.cuda.current_stream(dev).wait_stream(side)
     torch.cuda.synchronize()
 
-    timer = Timer(torch, R)
+    timer = Timer(torch, R, args.settle_ms * 1e-3)
     for nm, fn in [("step", step), ("attn", attn), ("accept", accept)]:
         timer.capture(nm, fn)
     torch.cuda.synchronize()
@@ -766,7 +778,7 @@ def run_extras(torch, w, inp, args, dev, R, reps, parent, kv_len, draft_d, outs,
         build(s % R)
         sampled(s % R)
     torch.cuda.synchronize()
-    timer = Timer(torch, R)
+    timer = Timer(torch, R, args.settle_ms * 1e-3)
     timer.capture("topw", topw, R_topw)
     for nm, fn in [("build", build), ("attn_paged", attn_paged),
                    ("attn_tail", attn_tail), ("train_attn", train_attn), ("sampled", sampled),
@@ -878,6 +890,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle_ms": args.settle_ms,
         "ms_per_step": ms_step,
         "higher_is_better": True,
         "scaling": "weak",

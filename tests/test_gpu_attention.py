@@ -53,6 +53,10 @@ FUZZ = [
     (3, 128, 32, 4, 128, 6000, [5999, 1234, 100], "random"),
     (1, 256, 64, 8, 64, 6000, [6000], "random"),
     (2, 128, 32, 4, 64, 6000, [6000, 37], "chain"),
+    # many short ragged sequences: the longest-first ranking holds two (40
+    # sequences) and eight (512 sequences) pairs per lane
+    (40, 8, 8, 4, 64, 2048, [(97 * i * i + 13 * i) % 2049 for i in range(40)], "random"),
+    (512, 2, 8, 8, 64, 200, [(31 * i) % 201 for i in range(512)], "random"),
 ]
 
 

@@ -1011,9 +1011,12 @@ void attn_main(AttnArgs a) {
 // workgroup: out = sum_s e_s O_s / sum_s e_s l_s with e_s = 2^(m_s - m*),
 // folded in online over batches of U chunks.  Only chunks that hold tiles
 // of this row block were written.  One wave per 16x16 fragment.  The
-// parents (for the tree check) and the first batch of partials are all
-// requested before any is used, so a merge of up to U chunks waits for one
-// round of memory latency.
+// parents (for the tree check), kv_len and the first batch of partials are
+// all requested before any is used, so a merge of up to U chunks waits for
+// one round of memory latency: the first batch reads the slots of the
+// first min(S, U) chunks whether or not they were written by this call
+// (they lie inside the workspace), and only the nval chunks that hold
+// tiles, known once kv_len arrives, are folded in.
 template <int D, int RB>
 __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
   constexpr int NTG = RB / 16, DT = D / 16, U = 16;
@@ -1036,9 +1039,17 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
   // chunks of this row block that hold tiles (the same count the main
   // kernel derives from kv_len and the block's last node)
   const int i_hi = (min(rb * RB + RB, a.M) - 1) / a.G;
+  const size_t base = (size_t)(bg * a.nRB + rb) * a.S;  // first chunk partial
+  float2 ml0[U];
+  f32x4 ov0[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+    if (u < a.S) {
+      ml0[u] = a.ws_ml[(base + u) * RB + row];
+      ov0[u] = a.ws_o[((base + u) * DT * NTG + dt * NTG + ntg) * 64 + lane];
+    }
   const int T = segment(a, b, i_hi).T;
   const int nval = min(a.S, (T + a.chunk - 1) / a.chunk);
-  const size_t base = (size_t)(bg * a.nRB + rb) * a.S;  // first chunk partial
   float m = -INFINITY, l = 0.f;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   for (int s0 = 0; s0 < nval; s0 += U) {
@@ -1047,8 +1058,13 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
       if (s0 + u < nval) {
-        ml[u] = a.ws_ml[(base + s0 + u) * RB + row];
-        ov[u] = a.ws_o[((base + s0 + u) * DT * NTG + dt * NTG + ntg) * 64 + lane];
+        if (s0 == 0) {
+          ml[u] = ml0[u];
+          ov[u] = ov0[u];
+        } else {
+          ml[u] = a.ws_ml[(base + s0 + u) * RB + row];
+          ov[u] = a.ws_o[((base + s0 + u) * DT * NTG + dt * NTG + ntg) * 64 + lane];
+        }
       }
     float mb = m;
 #pragma unroll

@@ -310,11 +310,6 @@ __global__ __launch_bounds__(kFinishThreads) void accept_finish(AcceptArgs a) {
   accept_sequence(a, b, l, pv, dv);
 }
 
-// Second kernel for trees of at most 64 * NPL nodes (NPL = 1 or 2): one
-// wave per sequence, lane l holding nodes l, l + 64, ..., l + 64 (NPL - 1),
-// so the merge, the pointer jumping and the path need no LDS and no
-// workgroup barrier (lane exchanges only).  Same results as accept_finish.
-
 // Split keys a node's merge requests: the plans give trees of more than
 // 32 * NPL nodes at most min(16, 64 / NPL) splits (the acceptance plan
 // aims at about 2048 (row, split) pairs and caps splits at 16).
@@ -338,77 +333,164 @@ __device__ __forceinline__ int lane_fetch(const int (&v)[NPL], int j) {
   return r;
 }
 
+// Loads issued as inline assembly, so that the compiler neither waits for
+// them where it would (before work that does not use them) nor moves their
+// uses; completion is awaited with explicit vmcnt waits (loads return in
+// issue order), after which `loaded` ties each value to the wait.
+__device__ __forceinline__ int ld_i32(const int32_t* p) {
+  int v;
+  asm volatile("global_load_dword %0, %1, off" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+__device__ __forceinline__ unsigned long long ld_u64(const unsigned long long* p) {
+  unsigned long long v;
+  asm volatile("global_load_dwordx2 %0, %1, off" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+template <class T>
+__device__ __forceinline__ void loaded(T& v) {
+  asm volatile("" : "+v"(v));
+}
+// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding)
+template <int n>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Second kernel for trees of at most 64 * NPL nodes (NPL = 1 or 2): one
+// wave per sequence, lane l holding nodes l, l + 64, ..., l + 64 (NPL - 1),
+// so everything runs on lane exchanges: no LDS and no workgroup barrier.
+// The tree's shape needs only the parents, so while the split keys are in
+// flight, pointer jumping over the parent links gives every node its
+// ancestor-or-self set as a bitmask of 64 * NPL bits (its depth is the
+// set's size minus one).  Once the keys are in, one ballot per slot gives
+// the nodes whose token equals the prediction at their parent (the root
+// always passes); a node is accepted iff its set holds no node outside
+// that ballot, the deepest accepted node (lowest index on ties) ends the
+// path, and every node of its set writes its own path entry.  Same results
+// as accept_finish.
 template <int NPL>
 __global__ __launch_bounds__(64) void accept_finish_wave(AcceptArgs a) {
+  constexpr int NW = 2 * NPL;  // 32-bit words of a node set
   const int b = blockIdx.x, lane = threadIdx.x;
   const int N = a.N;
-  int p[NPL], y[NPL], tgt[NPL], jmp[NPL], ok[NPL], dep[NPL];
+  int p[NPL], y[NPL], tgt[NPL], jmp[NPL];
+  int anc[NW][NPL];  // word w of the ancestor-or-self set of node lane + 64 q
   bool node[NPL];
   int badi = 0;
+  // Requests, oldest first: the parents, each node's split keys (indices
+  // past the last split repeat it, which leaves the max unchanged), the
+  // draft tokens.  Padding lanes read node N - 1's; nothing of theirs is
+  // used.  The parents are awaited before the shape is built, the rest only
+  // after it, so the keys arrive while the lanes exchange parent links.
+  constexpr int kLoads = wave_finish_loads<NPL>();
+  unsigned long long kv[NPL][kLoads];
 #pragma unroll
   for (int q = 0; q < NPL; ++q) {
     const int i = lane + 64 * q;
     node[q] = i < N;
-    p[q] = node[q] ? a.parent[(size_t)b * N + i] : 0;
-    y[q] = node[q] ? a.draft[(size_t)b * N + i] : 0;
+    p[q] = ld_i32(a.parent + (size_t)b * N + (node[q] ? i : N - 1));
   }
-  // each node's prediction: the max of its split keys, all requested at
-  // once (indices past the last split repeat it, which leaves the max
-  // unchanged and keeps the loads free of branches)
-  constexpr int kLoads = wave_finish_loads<NPL>();
 #pragma unroll
   for (int q = 0; q < NPL; ++q) {
     const int i = lane + 64 * q;
-    const unsigned long long* kp = a.part + ((size_t)b * N + (node[q] ? i : 0)) * a.nsplit;
-    unsigned long long kv[kLoads];
+    const unsigned long long* kp = a.part + ((size_t)b * N + (node[q] ? i : N - 1)) * a.nsplit;
 #pragma unroll
-    for (int k = 0; k < kLoads; ++k) kv[k] = kp[min(k, a.nsplit - 1)];
-    unsigned long long key = 0ull;
+    for (int k = 0; k < kLoads; ++k) kv[q][k] = ld_u64(kp + min(k, a.nsplit - 1));
+  }
 #pragma unroll
-    for (int k = 0; k < kLoads; ++k) key = umax64(key, kv[k]);
-    tgt[q] = key_index(node[q] ? key : 0ull);
-    if (node[q] && a.tgt_out) a.tgt_out[(size_t)b * N + i] = tgt[q];
+  for (int q = 0; q < NPL; ++q) {
+    const int i = lane + 64 * q;
+    y[q] = ld_i32(a.draft + (size_t)b * N + (node[q] ? i : N - 1));
+  }
+  wait_vm<NPL * kLoads + NPL>();
+#pragma unroll
+  for (int q = 0; q < NPL; ++q) {
+    loaded(p[q]);
+    if (!node[q]) p[q] = 0;
+  }
+  // the shape: valid parents, then pointer jumping on (jump target,
+  // ancestor set); the root and padding jump to node 0, whose set is {0}
+  int more = 0;
+#pragma unroll
+  for (int q = 0; q < NPL; ++q) {
+    const int i = lane + 64 * q;
     const int bq = node[q] && ((i == 0) ? (p[q] != -1) : (p[q] < 0 || p[q] >= i));
     badi |= bq;
-    jmp[q] = node[q] && i > 0 && !bq ? p[q] : 0;  // the root (and padding) jump to node 0
+    jmp[q] = node[q] && i > 0 && !bq ? p[q] : 0;
+    more |= jmp[q] != 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w)
+      anc[w][q] = !node[q] ? 0 : (int)((w == (i >> 5) ? 1u << (i & 31) : 0u) | (w == 0 ? 1u : 0u));
   }
   const bool bad = __any(badi);
-  int len = -1, v = 0, depth = 0;
   if (!bad) {
-#pragma unroll
-    for (int q = 0; q < NPL; ++q) {
-      const int i = lane + 64 * q;
-      const int tgt_parent = lane_fetch<NPL>(tgt, jmp[q]);
-      ok[q] = !node[q] ? 0 : (i == 0 ? 1 : (y[q] == tgt_parent));
-      dep[q] = node[q] && i > 0 ? 1 : 0;
-    }
-    // pointer jumping: ceil(log2(64 NPL)) rounds reach the root; every
-    // exchange of a round reads the values of the round before
-    int more = 0;
-#pragma unroll
-    for (int q = 0; q < NPL; ++q) more |= jmp[q] != 0;
+    // every exchange of a round reads the values of the round before;
+    // ceil(log2(64 NPL)) rounds reach the root from any node
     for (int r = 0; r < 12 && __any(more); ++r) {
-      int okj[NPL], depj[NPL], jj[NPL];
+      int aj[NW][NPL], jj[NPL];
 #pragma unroll
       for (int q = 0; q < NPL; ++q) {
-        okj[q] = lane_fetch<NPL>(ok, jmp[q]);
-        depj[q] = lane_fetch<NPL>(dep, jmp[q]);
         jj[q] = lane_fetch<NPL>(jmp, jmp[q]);
+#pragma unroll
+        for (int w = 0; w < NW; ++w) aj[w][q] = lane_fetch<NPL>(anc[w], jmp[q]);
       }
       more = 0;
 #pragma unroll
       for (int q = 0; q < NPL; ++q) {
-        ok[q] &= okj[q];
-        dep[q] += depj[q];
         jmp[q] = jj[q];
         more |= jmp[q] != 0;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) anc[w][q] |= aj[w][q];
       }
+    }
+  }
+  // the predictions: the max of each node's split keys
+  wait_vm<0>();
+#pragma unroll
+  for (int q = 0; q < NPL; ++q) {
+    loaded(y[q]);
+#pragma unroll
+    for (int k = 0; k < kLoads; ++k) loaded(kv[q][k]);
+  }
+#pragma unroll
+  for (int q = 0; q < NPL; ++q) {
+    const int i = lane + 64 * q;
+    unsigned long long key = 0ull;
+#pragma unroll
+    for (int k = 0; k < kLoads; ++k) key = umax64(key, kv[q][k]);
+    tgt[q] = key_index(node[q] ? key : 0ull);
+    if (node[q] && a.tgt_out) a.tgt_out[(size_t)b * N + i] = tgt[q];
+  }
+  int len = -1, depth = 0, dep[NPL];
+  unsigned int avw[NW];  // the winner's ancestor set
+  if (!bad) {
+    // nodes that pass: word w of the mask holds nodes 32 w .. 32 w + 31
+    unsigned int okw[NW];
+#pragma unroll
+    for (int q = 0; q < NPL; ++q) {
+      const int i = lane + 64 * q;
+      const int tp = lane_fetch<NPL>(tgt, node[q] && i > 0 ? p[q] : 0);
+      const bool pass = node[q] && (i == 0 || y[q] == tp);
+      const unsigned long long m = __ballot(pass);
+      okw[2 * q] = (unsigned int)m;
+      okw[2 * q + 1] = (unsigned int)(m >> 32);
     }
     unsigned int k = 0u;
 #pragma unroll
     for (int q = 0; q < NPL; ++q) {
-      const unsigned int i = (unsigned int)(lane + 64 * q);
-      const unsigned int kq = ok[q] ? ((unsigned int)dep[q] << 16) | (0xFFFFu - i) : 0u;
+      const int i = lane + 64 * q;
+      unsigned int fail = 0u;
+      int cnt = 0;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        fail |= (unsigned int)anc[w][q] & ~okw[w];
+        cnt += __popc((unsigned int)anc[w][q]);
+      }
+      dep[q] = cnt - 1;
+      const unsigned int kq =
+          node[q] && fail == 0u ? ((unsigned int)dep[q] << 16) | (0xFFFFu - (unsigned int)i) : 0u;
       k = kq > k ? kq : k;
     }
 #pragma unroll
@@ -417,18 +499,24 @@ __global__ __launch_bounds__(64) void accept_finish_wave(AcceptArgs a) {
       k = other > k ? other : k;
     }
     depth = (int)(k >> 16);
-    v = (int)(0xFFFFu - (k & 0xFFFFu));
+    const int v = (int)(0xFFFFu - (k & 0xFFFFu));
     len = depth + 1 > a.Dmax ? -1 : depth + 1;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) avw[w] = (unsigned int)lane_fetch<NPL>(anc[w], v);
   }
   int32_t* pth = a.path + (size_t)b * a.Dmax;
   for (int k = lane; k < a.Dmax; k += 64)
     if (k >= len) pth[k] = -1;
   if (len > 0) {
-    // walk up from v: the node at depth k of the path goes to entry k
-    int u = v;
-    for (int k = depth; k >= 0; --k) {
-      if (lane == 0) pth[k] = u;
-      u = lane_fetch<NPL>(p, u);
+    // the winner's root path: each of its nodes writes the entry at its depth
+#pragma unroll
+    for (int q = 0; q < NPL; ++q) {
+      const int i = lane + 64 * q;
+      unsigned int on = 0u;
+#pragma unroll
+      for (int w = 0; w < NW; ++w)
+        if (w == (i >> 5)) on = (avw[w] >> (i & 31)) & 1u;
+      if (node[q] && on) pth[dep[q]] = i;
     }
   }
   if (lane == 0) a.accept_len[b] = len;

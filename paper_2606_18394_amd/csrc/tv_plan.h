@@ -254,9 +254,9 @@ struct AcceptPlan {
   size_t ws_bytes;
 };
 
-// Fraction of its last round of loads that a thread fills when a row of
-// `chunks` vector chunks is cut into ns splits (rounds of per_round chunks
-// per workgroup).
+// Share of a workgroup's load slots that carry data when a row of `chunks`
+// vector chunks is cut into ns splits (whole rounds of per_round chunks per
+// workgroup; the last round is partly empty).
 inline double accept_round_fill(long long chunks, long long ns, long long per_round) {
   const long long c = (chunks + ns - 1) / ns;
   const long long rounds = (c + per_round - 1) / per_round;
@@ -273,12 +273,13 @@ inline AcceptPlan accept_plan(int B, int N, int V, int esize, int vec_elems) {
   const long long by_size = (chunks + per_round - 1) / per_round;
   if (ns > by_size) ns = by_size;
   if (ns < 1) ns = 1;
-  // Down to half as many splits, the count whose last round of loads is
-  // fullest (ties: more splits).  A partly filled last round costs a whole
-  // round of latency: 512 rows of 151936 bf16 logits in 4 splits take 2.3
-  // rounds per thread, in 2 splits 4.6, and the acceptance ran 32.6 us in 4
-  // against 31.7 us in 2; 128 rows stay at 10 splits (0.93 of one round),
-  // where 8 splits (1.16 rounds) were 5% slower.
+  // Down to half as many splits, the count whose load slots are best used
+  // (ties: more splits): a partly filled last round costs a whole round of
+  // latency.  512 rows of 151936 bf16 logits in 4 splits take 2.3 rounds per
+  // thread (77% of the slots used), in 2 splits 4.6 (93%), and the
+  // acceptance ran 32.6 us in 4 against 31.7 us in 2; 128 rows stay at 10
+  // splits (0.93 of one round), where 8 splits (1.16 rounds, 58%) were 5%
+  // slower.
   {
     long long best = ns;
     double best_fill = accept_round_fill(chunks, ns, per_round);

@@ -56,3 +56,43 @@ def test_plans_under_host_sanitizers(tmp_path):
     res = subprocess.run([str(exe)], input=data, capture_output=True, text=True)
     fails = [l for l in res.stdout.splitlines() if l.startswith("FAIL")]
     assert res.returncode == 0 and not fails, "\n".join(fails[:20]) + res.stderr[-1000:]
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="needs g++")
+def test_accept_split_rule(tmp_path):
+    """The acceptance scan's split count: the ~2048-workgroup target (at most
+    16 splits, at least one full round of loads each), then down to half of
+    it the count whose load slots are best used.  Checked against a plain
+    re-derivation of that rule, and at the measured shapes: 512 rows of
+    151936 bf16 logits take 2 splits (4 leave 23% of the slots empty), 128
+    and 64 rows keep 10."""
+    exe = tmp_path / "accept_split_check"
+    subprocess.run(["g++", "-O1", "-std=c++17", "-I", CSRC,
+                    os.path.join(ROOT, "tests", "native", "accept_split_check.cpp"), "-o", str(exe)],
+                   check=True)
+    cases = [(1, 512, 151936, 2), (1, 128, 151936, 2), (1, 64, 151936, 2), (16, 64, 151936, 2),
+             (1, 16, 1024, 4), (3, 100, 50000, 2), (1, 2048, 151936, 4), (7, 33, 32000, 4)]
+    res = subprocess.run([str(exe)], input="".join(f"{b} {n} {v} {e}\n" for b, n, v, e in cases),
+                         capture_output=True, text=True, check=True)
+    got = {tuple(map(int, l.split()[:4])): int(l.split()[4]) for l in res.stdout.splitlines()}
+
+    def rule(b, n, v, esize):
+        rows, per_round = b * n, 512 * 4
+        chunks = -(-v // (16 // esize))
+        ns = min(16, max(1, -(-2048 // rows)), -(-chunks // per_round))
+        ns = max(ns, 1)
+
+        def fill(k):
+            c = -(-chunks // k)
+            return c / (-(-c // per_round) * per_round)
+        best = ns
+        for k in range(ns - 1, 0, -1):
+            if 2 * k < ns:
+                break
+            if fill(k) > fill(best) + 1e-9:
+                best = k
+        return best
+    for c in cases:
+        assert got[c] == rule(*c), (c, got[c], rule(*c))
+    assert got[(1, 512, 151936, 2)] == 2
+    assert got[(1, 128, 151936, 2)] == 10 and got[(1, 64, 151936, 2)] == 10

@@ -257,6 +257,16 @@ def summarize_counters(dirs, workload):
     path = os.path.join(ROOT, "profiles", f"counters_attn_main_{workload}.md")
     with open(path, "w") as fh:
         fh.write("\n".join(lines) + "\n")
+    # the matrix-core busy fraction for the bench line, with the sources'
+    # hash so that it is reported only while it describes the running code
+    if "SQ_VALU_MFMA_BUSY_CYCLES" in c:
+        rec = {"kernel": kernel, "workload": workload, "dispatches": len(durs[kernel]),
+               "median_us": round(t * 1e6, 2),
+               "mfma_busy_frac": round(c["SQ_VALU_MFMA_BUSY_CYCLES"] / (SIMDS * CLOCK_HZ * t), 4),
+               "kernel_src_sha": kernel_source_sha()}
+        with open(path[:-3] + ".json", "w") as fh:
+            json.dump(rec, fh, indent=1)
+            fh.write("\n")
     print(path)
 
 
@@ -369,6 +379,20 @@ def measured_traffic(kernel, workload):
     return rec.get("hbm_bytes_per_launch")
 
 
+def measured_mfma_busy(workload):
+    """Fraction of the attention kernel's SIMD-cycles its matrix cores were
+    busy (SQ_VALU_MFMA_BUSY_CYCLES from committed rocprofv3 counter runs), only
+    if they were taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"counters_attn_main_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    if rec.get("kernel_src_sha") != kernel_source_sha():
+        return None
+    return rec.get("mfma_busy_frac")
+
+
 def roofline(name, t_s, nbytes, flops, kernel, workload):
     """Position of one kernel against the roofline that binds it: HBM bytes
     or bf16 MFMA flops at the MI355X peaks, whichever takes longer."""
@@ -380,6 +404,8 @@ def roofline(name, t_s, nbytes, flops, kernel, workload):
     r["frac"] = r["achieved"] / r["peak"]
     r["kernel"] = name
     r["traffic"] = measured_traffic(kernel, workload)
+    if kernel == "attn_main" and r["bound"] == "mfma":
+        r["mfma_busy"] = measured_mfma_busy(workload)
     return r
 
 

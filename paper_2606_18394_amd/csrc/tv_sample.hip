@@ -140,19 +140,25 @@ __device__ __forceinline__ unsigned long long wave_max_key(unsigned long long k)
 
 // ------------------------------------------------------------ lse_scan
 
-// (max, sum exp) of x / T over elements [x0, x1) of a row; x0 and x1 are
-// multiples of 8 (or x1 = V) so that vectorised rows read whole 16-byte
-// chunks of either dtype
+// (max, sum exp) of x / T over elements [x0, x1) of a row, into m and s,
+// which start at (-inf, 0); x0 and x1 are multiples of 8 (or x1 = V) so that
+// vectorised rows read whole 16-byte chunks of either dtype
 template <bool F32>
 __device__ __forceinline__ void lse_slice(const void* rowp, long long x0, long long x1, bool vec,
                                           float invT, float& m, float& s) {
   constexpr int E = F32 ? 4 : 8;  // elements per 16-byte chunk
-  constexpr int L = kScanLoadsPerThread;
+  constexpr int L = kLseScanLoads;
   const int tid = threadIdx.x;
   if (vec) {
+    // In base-2 units: with c2 = log2(e) / T a weight is exp2(x * c2 - m2)
+    // (one fma and one exp2 per logit), m2 the running maximum of x * c2;
+    // the batch maximum is taken on the raw logits (c2 > 0 keeps the order).
+    // m is returned in the natural units of x / T.
+    const float c2 = invT * 1.4426950408889634f;
+    float m2 = -INFINITY;
     const long long c0 = x0 / E, c1 = (x1 + E - 1) / E;
     const uint4* base = reinterpret_cast<const uint4*>(rowp);
-    for (long long c = c0 + tid; c < c1; c += (long long)L * kScanThreads) {
+    for (long long c = c0 + tid; c < c1; c += (long long)L * kLseScanThreads) {
       // all L loads are issued first (past the end: the last chunk again),
       // then decoded with the padding replaced by -inf bit patterns, so the
       // loads are in flight together
@@ -160,22 +166,22 @@ __device__ __forceinline__ void lse_slice(const void* rowp, long long x0, long l
       uint4 raw[L];
 #pragma unroll
       for (int u = 0; u < L; ++u) {
-        const long long cu = c + (long long)u * kScanThreads;
+        const long long cu = c + (long long)u * kLseScanThreads;
         raw[u] = load_stream(base + (cu < c1 ? cu : c1 - 1));
       }
       float x[L][E];
 #pragma unroll
       for (int u = 0; u < L; ++u) {
-        const bool in = c + (long long)u * kScanThreads < c1;
+        const bool in = c + (long long)u * kLseScanThreads < c1;
         const unsigned int ws[4] = {in ? raw[u].x : kNegInf, in ? raw[u].y : kNegInf,
                                     in ? raw[u].z : kNegInf, in ? raw[u].w : kNegInf};
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
           if (F32) {
-            x[u][k] = __uint_as_float(ws[k]) * invT;
+            x[u][k] = __uint_as_float(ws[k]);
           } else {
-            x[u][2 * k] = __uint_as_float(ws[k] << 16) * invT;
-            x[u][2 * k + 1] = __uint_as_float(ws[k] & 0xFFFF0000u) * invT;
+            x[u][2 * k] = __uint_as_float(ws[k] << 16);
+            x[u][2 * k + 1] = __uint_as_float(ws[k] & 0xFFFF0000u);
           }
         }
       }
@@ -185,17 +191,18 @@ __device__ __forceinline__ void lse_slice(const void* rowp, long long x0, long l
 #pragma unroll
         for (int e = 0; e < E; ++e) bm = fmaxf(bm, x[u][e]);
       if (bm == -INFINITY) continue;
-      const float mn = fmaxf(m, bm);
+      const float mn = fmaxf(m2, bm * c2);
       float bs = 0.f;
 #pragma unroll
       for (int u = 0; u < L; ++u)
 #pragma unroll
-        for (int e = 0; e < E; ++e) bs += __expf(x[u][e] - mn);
-      s = (m == -INFINITY ? 0.f : s * __expf(m - mn)) + bs;
-      m = mn;
+        for (int e = 0; e < E; ++e) bs += __builtin_amdgcn_exp2f(fmaf(x[u][e], c2, -mn));
+      s = (m2 == -INFINITY ? 0.f : s * __builtin_amdgcn_exp2f(m2 - mn)) + bs;
+      m2 = mn;
     }
+    m = m2 == -INFINITY ? -INFINITY : m2 * 0.6931471805599453f;
   } else {
-    for (long long c = x0 + tid; c < x1; c += kScanThreads) {
+    for (long long c = x0 + tid; c < x1; c += kLseScanThreads) {
       const float x = load_logit<F32>(rowp, (size_t)c) * invT;
       lse_merge2(m, s, x, 1.f);
     }
@@ -203,7 +210,7 @@ __device__ __forceinline__ void lse_slice(const void* rowp, long long x0, long l
 }
 
 template <bool F32>
-__global__ __launch_bounds__(kScanThreads) void lse_scan(SampleArgs a, int vec) {
+__global__ __launch_bounds__(kLseScanThreads) void lse_scan(SampleArgs a, int vec) {
   const int row = blockIdx.x / a.nsplit, split = blockIdx.x % a.nsplit;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const long long x0 = (long long)split * a.eps;
@@ -211,7 +218,7 @@ __global__ __launch_bounds__(kScanThreads) void lse_scan(SampleArgs a, int vec) 
   float m = -INFINITY, s = 0.f;
   const char* rowp = (const char*)a.logits + (size_t)row * a.V * (F32 ? 4 : 2);
   lse_slice<F32>(rowp, x0, x1, vec != 0, a.invT, m, s);
-  __shared__ float rm[kScanThreads / 64], rs[kScanThreads / 64];
+  __shared__ float rm[kLseScanThreads / 64], rs[kLseScanThreads / 64];
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) lse_merge2(m, s, __shfl_xor(m, o), __shfl_xor(s, o));
   if (lane == 0) {
@@ -222,7 +229,7 @@ __global__ __launch_bounds__(kScanThreads) void lse_scan(SampleArgs a, int vec) 
   if (tid == 0) {
     float gm = rm[0], gs = rs[0];
 #pragma unroll
-    for (int w = 1; w < kScanThreads / 64; ++w) lse_merge2(gm, gs, rm[w], rs[w]);
+    for (int w = 1; w < kLseScanThreads / 64; ++w) lse_merge2(gm, gs, rm[w], rs[w]);
     a.lse_part[(size_t)row * a.nsplit + split] = make_float2(gm, gs);
   }
 }
@@ -528,7 +535,7 @@ __global__ __launch_bounds__(64) void sample_finish(SampleArgs a) {
 template <bool F32>
 static hipError_t launch_sample_t(const SampleArgs& a, const SamplePlan& p, int vec,
                                   hipStream_t st) {
-  hipLaunchKernelGGL((lse_scan<F32>), dim3(p.lse_grid), dim3(kScanThreads), 0, st, a, vec);
+  hipLaunchKernelGGL((lse_scan<F32>), dim3(p.lse_grid), dim3(kLseScanThreads), 0, st, a, vec);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((sample_accept<F32>), dim3(a.B * p.nrace), dim3(kSampleThreads), 0, st, a,

@@ -277,9 +277,11 @@ __global__ __launch_bounds__(kAcceptScanThreads) void accept_scan(AcceptArgs a) 
 
 // Second kernel: one workgroup per sequence; thread t takes rows t,
 // t + kFinishThreads, ...: it requests every split key of its row at once
-// (indices past the last split repeat it, which leaves the max unchanged),
-// keeps the max in registers, and the acceptance runs on the merged
-// predictions.  The parents and tokens are requested first, so all of the
+// (only the plan's splits: the split count is the same for every thread,
+// so the loads past it are skipped by a uniform branch; at 512 nodes in 2
+// splits that took the acceptance from 31.7 to 31.1 us, against loads of
+// all 16 slots at clamped indices), keeps the max in registers, and the
+// acceptance runs on the merged predictions.  The parents and tokens are requested first, so all of the
 // kernel's global loads are in flight together.
 __global__ __launch_bounds__(kFinishThreads) void accept_finish(AcceptArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
@@ -297,7 +299,7 @@ __global__ __launch_bounds__(kFinishThreads) void accept_finish(AcceptArgs a) {
       const unsigned long long* kp = a.part + ((size_t)b * N + i) * a.nsplit;
       unsigned long long kv[kAcceptMaxSplit];
 #pragma unroll
-      for (int s = 0; s < kAcceptMaxSplit; ++s) kv[s] = kp[min(s, a.nsplit - 1)];
+      for (int s = 0; s < kAcceptMaxSplit; ++s) kv[s] = s < a.nsplit ? kp[s] : 0ull;
       unsigned long long key = 0ull;
 #pragma unroll
       for (int s = 0; s < kAcceptMaxSplit; ++s) key = umax64(key, kv[s]);

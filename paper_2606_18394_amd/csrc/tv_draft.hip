@@ -13,13 +13,14 @@
 //   argmax.  Finish: one wave per row merges the splits.
 //
 // build: best-first expansion under a node budget, one wave per sequence.
-//   Node i is owned by lane i % 64 (slot i / 64), which keeps the score,
-//   depth and open flag of its slots in registers and caches the best open
-//   node it owns; a pop is a wave argmax of (score, lower index) over those
-//   caches, the winning node's owner rescans its slots in registers, and the
-//   up to W children go to W consecutive lanes.  Only tokens and parents go
-//   to LDS, written during the loop and read once at the end.  Scores are
-//   fp32 sums parent + log-probability, the comparisons that decide the
+//   Node i is owned by lane i % 64 (slot i / 64), which keeps the score
+//   keys of its open nodes in registers and caches its best one; a pop is a
+//   wave maximum of those keys (an order-preserving unsigned image of the
+//   fp32 score) with ties settled by the lower node index, the owner
+//   rescans its slots in registers, and the up to W children go to W
+//   consecutive lanes.  The loop only logs the popped nodes; parents,
+//   tokens, depths and scores are rebuilt from that log at the end.  Scores
+//   are fp32 sums parent + log-probability, the comparisons that decide the
 //   tree.
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -94,50 +95,43 @@ __device__ __forceinline__ bool better(float a, int ia, float b, int ib) {
   return a > b || (a == b && ia < ib);
 }
 
-// Wave-wide best (value, index), with a payload that travels with it;
-// every lane receives the result.  Within each row of 16 lanes: DPP
-// exchanges with lane ^ 1 and lane ^ 2 (quad permutes), then mirrored lanes
-// of each half-row and of the row, after which all 16 lanes hold the row's
-// best; the four rows are then read out as scalars.  (Cross-lane shuffles
-// would go through the LDS crossbar, one round trip per step.)
+// Wave-wide best (value, lower index); every lane receives the result.
+// Within each row of 16 lanes: DPP exchanges with lane ^ 1 and lane ^ 2
+// (quad permutes), then mirrored lanes of each half-row and of the row,
+// after which all 16 lanes hold the row's best; the four rows are then read
+// out as scalars.  (Cross-lane shuffles would go through the LDS crossbar,
+// one round trip per step.)
 template <int CTRL>
 __device__ __forceinline__ int dpp(int x) {
   return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xF, 0xF, false);
 }
 template <int CTRL>
-__device__ __forceinline__ void dpp_best_step(float& v, int& i, int& p) {
+__device__ __forceinline__ void dpp_best_step(float& v, int& i) {
   const float ov = __int_as_float(dpp<CTRL>(__float_as_int(v)));
-  const int oi = dpp<CTRL>(i), op = dpp<CTRL>(p);
+  const int oi = dpp<CTRL>(i);
   if (better(ov, oi, v, i)) {
     v = ov;
     i = oi;
-    p = op;
   }
 }
-__device__ __forceinline__ void wave_best(float& v, int& i, int& p) {
-  dpp_best_step<0xB1>(v, i, p);   // quad_perm(1,0,3,2): lane ^ 1
-  dpp_best_step<0x4E>(v, i, p);   // quad_perm(2,3,0,1): lane ^ 2
-  dpp_best_step<0x141>(v, i, p);  // row_half_mirror: quads of each half-row
-  dpp_best_step<0x140>(v, i, p);  // row_mirror: the two halves of the row
+__device__ __forceinline__ void wave_best(float& v, int& i) {
+  dpp_best_step<0xB1>(v, i);   // quad_perm(1,0,3,2): lane ^ 1
+  dpp_best_step<0x4E>(v, i);   // quad_perm(2,3,0,1): lane ^ 2
+  dpp_best_step<0x141>(v, i);  // row_half_mirror: quads of each half-row
+  dpp_best_step<0x140>(v, i);  // row_mirror: the two halves of the row
   float gv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
-  int gi = __builtin_amdgcn_readlane(i, 0), gp = __builtin_amdgcn_readlane(p, 0);
+  int gi = __builtin_amdgcn_readlane(i, 0);
 #pragma unroll
   for (int r = 16; r < 64; r += 16) {
     const float rv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), r));
-    const int ri = __builtin_amdgcn_readlane(i, r), rp = __builtin_amdgcn_readlane(p, r);
+    const int ri = __builtin_amdgcn_readlane(i, r);
     if (better(rv, ri, gv, gi)) {
       gv = rv;
       gi = ri;
-      gp = rp;
     }
   }
   v = gv;
   i = gi;
-  p = gp;
-}
-__device__ __forceinline__ void wave_best(float& v, int& i) {
-  int p = 0;
-  wave_best(v, i, p);
 }
 
 // (m, s) with s = sum exp(x - m): merge of two such states
@@ -390,116 +384,69 @@ struct BuildArgs {
   int Nd, W, budget;
 };
 
-// Budgets of 65 .. 64 S nodes.  Node i belongs to lane i % 64, slot i / 64,
-// and the score, depth and open flag of a lane's S nodes stay in its
-// registers, so after a pop the owner finds its next best open node with an
-// unrolled register scan (no memory access).  Each lane also caches its
-// best open node, and a pop is one wave argmax of those caches.  Tokens and
-// parents are only written during the loop, so they go to LDS and are read
-// once at the end.
-template <int S>
-__global__ __launch_bounds__(64) void build_tree(BuildArgs a) {
-  static_assert(S >= 1 && S <= 32, "open flags are one 32-bit mask");
-  __shared__ float cand_lp[kMaxDraftDepth * kTopwMax];
-  __shared__ int cand_tok[kMaxDraftDepth * kTopwMax];
-  __shared__ int tk[64 * S];
-  __shared__ short par[64 * S];
-  const int b = blockIdx.x, lane = threadIdx.x;
-  const int Nd = a.Nd, W = a.W, budget = a.budget;
-  const size_t cbase = (size_t)b * Nd * W;
-  for (int k = lane; k < Nd * W; k += 64) {
-    cand_lp[k] = a.logp[cbase + k];
-    cand_tok[k] = a.tok[cbase + k];
-  }
-  if (lane == 0) {
-    tk[0] = a.root_tok ? a.root_tok[b] : -1;
-    par[0] = -1;
-  }
-  __syncthreads();
-  float sc[S];
-  int dep[S];
-#pragma unroll
-  for (int j = 0; j < S; ++j) {
-    sc[j] = 0.f;
-    dep[j] = 0;
-  }
-  unsigned int open = lane == 0 ? 1u : 0u;  // bit j: node lane + 64 j is open (root: Nd >= 1)
-  float bs = lane == 0 ? 0.f : -INFINITY;   // this lane's best open node,
-  int bi = lane == 0 ? 0 : 0x7FFFFFFF;      // its index and depth
-  int bd = 0;
-  int n = 1;
-  // The loop runs in one wave: LDS accesses of a wave execute in order, and
-  // tokens and parents are read only after it.  Each pop of an open node
-  // adds at least one node, so budget - 1 pops end it.
-  for (int it = 0; it < budget && n < budget; ++it) {
-    float gs = bs;
-    int gi = bi, gd = bd;
-    wave_best(gs, gi, gd);
-    if (gi == 0x7FFFFFFF) break;  // nothing open
-    const int v = gi;
-    const int d = gd;
-    if (lane == (v & 63)) {  // the owner closes v and finds its next best
-      open &= ~(1u << (v >> 6));
-      bs = -INFINITY;
-      bi = 0x7FFFFFFF;
-#pragma unroll
-      for (int j = 0; j < S; ++j) {
-        const int i = lane + 64 * j;
-        if (((open >> j) & 1u) && better(sc[j], i, bs, bi)) {
-          bs = sc[j];
-          bi = i;
-          bd = dep[j];
-        }
-      }
-    }
-    const int nk = min(W, budget - n);
-    const int k = (lane - (n & 63)) & 63;  // this lane's child, if k < nk
-    if (k < nk) {
-      const int c = n + k;
-      const int jc = c >> 6;
-      const float s = gs + cand_lp[d * W + k];
-      const bool op = d + 1 < Nd;
-#pragma unroll
-      for (int j = 0; j < S; ++j)
-        if (j == jc) {
-          sc[j] = s;
-          dep[j] = d + 1;
-        }
-      if (op) open |= 1u << jc;
-      tk[c] = cand_tok[d * W + k];
-      par[c] = (short)v;
-      if (op && better(s, c, bs, bi)) {
-        bs = s;
-        bi = c;
-        bd = d + 1;
-      }
-    }
-    n += nk;
-    asm volatile("" ::: "memory");
-  }
-  __syncthreads();
-  const size_t obase = (size_t)b * budget;
-#pragma unroll
-  for (int j = 0; j < S; ++j) {
-    const int i = lane + 64 * j;
-    if (i < budget) {
-      const bool used = i < n;
-      a.parent[obase + i] = used ? (int)par[i] : -1;
-      a.token[obase + i] = used ? tk[i] : -1;
-      a.depth[obase + i] = used ? dep[j] : -1;
-      if (a.score) a.score[obase + i] = used ? sc[j] : -INFINITY;
-    }
-  }
-  if (lane == 0) a.n_nodes[b] = n;
+// Order-preserving map of a score to a nonzero key: a larger score gives a
+// larger key, so one unsigned maximum compares scores.  (-0.0 would sort
+// below +0.0; no score takes that value, since the root's is +0.0 and a
+// sum that cancels to zero rounds to +0.0.)  Key 0 marks "no open node".
+__device__ __forceinline__ unsigned score_key(float s) {
+  const unsigned u = __float_as_uint(s);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key_score(unsigned k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
 }
 
-// Budgets of at most 64 nodes: node i lives in the registers of lane i, so
-// a pop is one wave argmax over the open nodes (no per-lane rescan) and the
-// new children are written by their own lanes.  Same selections, same fp32
-// sums, same outputs as build_tree.
-__global__ __launch_bounds__(64) void build_tree_wave(BuildArgs a) {
+// Wave-wide maximum / minimum of an unsigned value, returned to every lane
+// as a wave-uniform value: DPP steps inside each row of 16 lanes (lane ^ 1,
+// lane ^ 2, then the mirrored quads and halves), then the four rows' values
+// are read out as scalars and combined on the scalar unit.
+template <int CTRL>
+__device__ __forceinline__ unsigned dpp_u32(unsigned x) {
+  return (unsigned)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
+}
+__device__ __forceinline__ unsigned wave_max_u32(unsigned x) {
+  x = max(x, dpp_u32<0xB1>(x));
+  x = max(x, dpp_u32<0x4E>(x));
+  x = max(x, dpp_u32<0x141>(x));
+  x = max(x, dpp_u32<0x140>(x));
+  // row 1 takes row 0's maximum and row 3 row 2's, then rows 2 and 3 take
+  // row 1's: lane 63 holds the wave's
+  x = max(x, (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x142, 0xA, 0xF, false));
+  x = max(x, (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x143, 0xC, 0xF, false));
+  return __builtin_amdgcn_readlane(x, 63);
+}
+__device__ __forceinline__ unsigned wave_min_u32(unsigned x) {
+  x = min(x, dpp_u32<0xB1>(x));
+  x = min(x, dpp_u32<0x4E>(x));
+  x = min(x, dpp_u32<0x141>(x));
+  x = min(x, dpp_u32<0x140>(x));
+  const unsigned r0 = __builtin_amdgcn_readlane(x, 0), r1 = __builtin_amdgcn_readlane(x, 16);
+  const unsigned r2 = __builtin_amdgcn_readlane(x, 32), r3 = __builtin_amdgcn_readlane(x, 48);
+  return min(min(r0, r1), min(r2, r3));
+}
+
+// Best-first expansion for budgets of at most 64 S nodes, one wave per
+// sequence.  Node i belongs to lane i % 64, slot i / 64.  A lane keeps, per
+// slot, the score key of its node while that node is open (0 otherwise)
+// and the slot and depth packed as slot << 8 | depth, plus its best open
+// node (largest key, lowest slot on equal keys).  A pop:
+//  * the wave maximum of the lanes' best keys; the lanes holding it are a
+//    ballot, and with several (equal scores) the lowest node index wins;
+//  * the owner closes the node and rescans its slots in registers;
+//  * the up to W children go to consecutive lanes: child k of a depth-d
+//    node gets key(score + logp[d, k]) if depth d + 1 is below Nd, else 0.
+// Every pop but the last adds exactly W children, so node c >= 1 is child
+// (c - 1) % W of the ((c - 1) / W)-th popped node: the loop only logs the
+// popped nodes (index, depth, key) in LDS, and parents, tokens, depths
+// and scores are rebuilt from that log at the end, with the same fp32 sum
+// the loop's key came from.
+template <int S>
+__global__ __launch_bounds__(64) void build_tree(BuildArgs a) {
+  static_assert(S >= 1 && S <= kMaxNodes / 64, "slots per lane");
   __shared__ float cand_lp[kMaxDraftDepth * kTopwMax];
   __shared__ int cand_tok[kMaxDraftDepth * kTopwMax];
+  __shared__ unsigned pop_key[kMaxNodes];
+  __shared__ int pop_node[kMaxNodes];  // node index | depth << 16
   const int b = blockIdx.x, lane = threadIdx.x;
   const int Nd = a.Nd, W = a.W, budget = a.budget;
   const size_t cbase = (size_t)b * Nd * W;
@@ -508,37 +455,98 @@ __global__ __launch_bounds__(64) void build_tree_wave(BuildArgs a) {
     cand_tok[k] = a.tok[cbase + k];
   }
   __syncthreads();
-  // this lane's node (the root on lane 0)
-  float s = 0.f;
-  int tk = lane == 0 && a.root_tok ? a.root_tok[b] : -1;
-  int par = -1, dep = 0;
-  bool open = lane == 0;  // Nd >= 1
-  int n = 1;
-  // each pop of an open node adds at least one node, so budget - 1 pops end it
-  for (int it = 0; it < budget && n < budget; ++it) {
-    float gs = open ? s : -INFINITY;
-    int gi = open ? lane : 0x7FFFFFFF, gd = dep;
-    wave_best(gs, gi, gd);
-    if (gi == 0x7FFFFFFF) break;  // nothing open
-    if (lane == gi) open = false;
-    const int nk = min(W, budget - n);
-    const int k = lane - n;
-    if (k >= 0 && k < nk) {
-      s = gs + cand_lp[gd * W + k];
-      tk = cand_tok[gd * W + k];
-      par = gi;
-      dep = gd + 1;
-      open = gd + 1 < Nd;
+  unsigned key[S];
+  int sd[S];
+#pragma unroll
+  for (int j = 0; j < S; ++j) {
+    key[j] = 0u;
+    sd[j] = 0;
+  }
+  key[0] = lane == 0 ? score_key(0.f) : 0u;  // the root is open (Nd >= 1)
+  unsigned bk = key[0];                       // this lane's best open node:
+  int bsd = 0;                                // its key and slot << 8 | depth
+  int n = 1, np = 0;
+  // each pop adds at least one node, so at most budget - 1 pops
+  while (n < budget) {
+    const unsigned g = wave_max_u32(bk);
+    if (g == 0u) break;  // nothing open
+    const unsigned long long hold = __ballot(bk == g);
+    int owner;
+    if (__popcll(hold) == 1) {
+      owner = __ffsll((unsigned long long)hold) - 1;
+    } else {  // equal scores: the lowest node index
+      const unsigned idx = bk == g ? (unsigned)((bsd >> 8) * 64 + lane) : 0xFFFFFFFFu;
+      owner = __builtin_amdgcn_readfirstlane((int)(wave_min_u32(idx) & 63u));
     }
+    const int osd = __builtin_amdgcn_readlane(bsd, owner);
+    const int jv = osd >> 8, d = osd & 0xFF;
+    const int nk = min(W, budget - n);
+    const int k = (lane - (n & 63)) & 63;  // this lane's child, if k < nk
+    const bool child = k < nk;
+    const float lp = cand_lp[d * W + (child ? k : 0)];
+    // the owner closes the popped node; every lane rescans (the others
+    // find their best unchanged)
+    const bool own = lane == owner;
+#pragma unroll
+    for (int j = 0; j < S; ++j)
+      if (own && j == jv) key[j] = 0u;
+    unsigned m = key[0];
+#pragma unroll
+    for (int j = 1; j < S; ++j) m = max(m, key[j]);
+    bk = m;
+#pragma unroll
+    for (int j = S - 1; j >= 0; --j)
+      if (key[j] == m) bsd = sd[j];
+    const int c = n + k;
+    // computed on every lane, so that the LDS read above overlaps the rescan
+    unsigned ck = score_key(key_score(g) + lp);
+    if (!child || d + 1 >= Nd) ck = 0u;
+    const int csd = (c >> 6) << 8 | (d + 1);
+    const int jc = child ? c >> 6 : -1;
+#pragma unroll
+    for (int j = 0; j < S; ++j)
+      if (j == jc) {
+        key[j] = ck;
+        sd[j] = csd;
+      }
+    if (ck > bk) {  // a child has the lane's highest index: strictly better only
+      bk = ck;
+      bsd = csd;
+    }
+    if (lane == 0) {
+      pop_key[np] = g;
+      pop_node[np] = (jv * 64 + owner) | d << 16;
+    }
+    ++np;
     n += nk;
   }
+  __syncthreads();
   const size_t obase = (size_t)b * budget;
-  if (lane < budget) {
-    const bool used = lane < n;
-    a.parent[obase + lane] = used ? par : -1;
-    a.token[obase + lane] = used ? tk : -1;
-    a.depth[obase + lane] = used ? dep : -1;
-    if (a.score) a.score[obase + lane] = used ? s : -INFINITY;
+#pragma unroll
+  for (int j = 0; j < S; ++j) {
+    const int c = lane + 64 * j;
+    if (c < budget) {
+      int par = -1, tk = -1, dep = -1;
+      float sc = -INFINITY;
+      if (c == 0) {
+        tk = a.root_tok ? a.root_tok[b] : -1;
+        dep = 0;
+        sc = 0.f;
+      } else if (c < n) {
+        const unsigned t = (unsigned)(c - 1);
+        const unsigned p = t / (unsigned)W, kk = t - p * (unsigned)W;
+        const int pn = pop_node[p];
+        const int pd = pn >> 16;
+        par = pn & 0xFFFF;
+        tk = cand_tok[pd * W + kk];
+        dep = pd + 1;
+        sc = key_score(pop_key[p]) + cand_lp[pd * W + kk];
+      }
+      a.parent[obase + c] = par;
+      a.token[obase + c] = tk;
+      a.depth[obase + c] = dep;
+      if (a.score) a.score[obase + c] = sc;
+    }
   }
   if (lane == 0) a.n_nodes[b] = n;
 }
@@ -558,9 +566,10 @@ hipError_t launch_build_tree(const int32_t* tok, const float* logp, const int32_
   a.Nd = Nd;
   a.W = W;
   a.budget = budget;
+  // slots per lane: the fewest that hold the budget
   if (budget <= 64)
-    hipLaunchKernelGGL(build_tree_wave, dim3(B), dim3(64), 0, st, a);
-  else if (budget <= 128)  // slots per lane: the fewest that hold the budget
+    hipLaunchKernelGGL(build_tree<1>, dim3(B), dim3(64), 0, st, a);
+  else if (budget <= 128)
     hipLaunchKernelGGL(build_tree<2>, dim3(B), dim3(64), 0, st, a);
   else if (budget <= 256)
     hipLaunchKernelGGL(build_tree<4>, dim3(B), dim3(64), 0, st, a);

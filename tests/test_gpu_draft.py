@@ -91,6 +91,10 @@ def _compare_trees(got, ref):
 def _candidates(rng, B, Nd, W, kind):
     if kind == "ties":      # few distinct values: many equal scores
         lp = -np.sort(rng.integers(0, 3, size=(B, Nd, W)), axis=-1).astype(np.float32)
+    elif kind == "mixed":   # any finite values, unsorted: a child may beat its parent
+        lp = (rng.standard_normal((B, Nd, W)) * 2).astype(np.float32)
+    elif kind == "huge":    # sums overflow to -inf, which then tie by node index
+        lp = -rng.uniform(1e38, 3e38, size=(B, Nd, W)).astype(np.float32)
     else:
         lp = -np.sort(rng.exponential(1.5, size=(B, Nd, W)), axis=-1).astype(np.float32)
     tok = rng.integers(0, 151936, size=(B, Nd, W))
@@ -112,7 +116,7 @@ BUILD_CASES = [
     (1, 64, 2, 1000, "normal"),    # deepest draft
     (3, 6, 4, 65, "normal"),       # smallest budget past one node per lane
     (2, 8, 8, 513, "ties"),        # budgets just past 128, 256, 512 and 1024 nodes
-    (1, 10, 6, 129, "ties"),       # (the builder keeps 2, 4, 8, 16 or 32 nodes per lane)
+    (1, 10, 6, 129, "ties"),       # (the builder keeps 1, 2, 4, 8, 16 or 32 nodes per lane)
     (2, 9, 5, 257, "normal"),
     (1, 12, 9, 1025, "normal"),
     (2, 7, 3, 128, "ties"),
@@ -121,6 +125,11 @@ BUILD_CASES = [
     (3, 2, 3, 64, "normal"),       # the full tree (13 nodes) ends before the budget
     (2, 64, 2, 64, "normal"),      # deep and narrow
     (2, 4, 16, 63, "normal"),
+    # log-probabilities are only required to be finite
+    (3, 10, 5, 300, "mixed"),
+    (2, 6, 4, 50, "mixed"),
+    (2, 9, 3, 200, "huge"),
+    (1, 5, 4, 40, "huge"),
 ]
 
 

@@ -142,11 +142,23 @@ __device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2
   m = mn;
 }
 
-template <bool F32, bool VEC, int K>
+// Slices of one load round (ONE) rank their candidates directly: every
+// element >= tau is appended to an LDS list, and each listed candidate's
+// rank is the number of listed candidates better than it; ranks below W are
+// the slice's top-W.  More than kTopwCand candidates (values tied at tau)
+// fall back to the per-thread lists and W rounds of workgroup argmax.
+constexpr int kTopwCand = kScanThreads;
+
+template <bool F32, bool VEC, int K, bool ONE>
 __global__ __launch_bounds__(kScanThreads) void topw_scan(TopwArgs a) {
   constexpr int E = VEC ? (F32 ? 4 : 8) : 1;  // elements per chunk
   constexpr int L = kScanLoadsPerThread;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  __shared__ int s_ncand;
+  __shared__ float s_cv[kTopwCand];
+  __shared__ int s_ci[kTopwCand];
+  if (ONE && tid == 0) s_ncand = 0;  // read after the first round's barrier
+  int ncand = 0;
   const int row = blockIdx.x / a.nsplit;
   const int split = blockIdx.x % a.nsplit;
   const long long nchunks = ((long long)a.V + E - 1) / E;
@@ -201,11 +213,15 @@ __global__ __launch_bounds__(kScanThreads) void topw_scan(TopwArgs a) {
         x[u][0] = __uint_as_float(in ? raw[u].x : 0xFF800000u);
       }
     }
+    float bmu[L];  // maximum of each load
     float bm = -INFINITY;
 #pragma unroll
-    for (int u = 0; u < L; ++u)
+    for (int u = 0; u < L; ++u) {
+      bmu[u] = x[u][0];
 #pragma unroll
-      for (int e = 0; e < E; ++e) bm = fmaxf(bm, x[u][e]);
+      for (int e = 1; e < E; ++e) bmu[u] = fmaxf(bmu[u], x[u][e]);
+      bm = fmaxf(bm, bmu[u]);
+    }
     if (bm != -INFINITY) {  // a thread past the slice end has only padding
       const float mn = fmaxf(m, bm);
       float bs = 0.f;
@@ -237,8 +253,30 @@ __global__ __launch_bounds__(kScanThreads) void topw_scan(TopwArgs a) {
 #pragma unroll
       for (int w = 1; w < kWaves; ++w) tau = fminf(tau, s_tau[w]);
     }
+    if (ONE) {
+      // the slice's top-W are all >= tau: list them (not the padding)
+      if (bm >= tau) {
+#pragma unroll
+        for (int u = 0; u < L; ++u) {
+          const long long cu = c + (long long)u * kScanThreads;
+          if (cu < c1 && bmu[u] >= tau) {
+#pragma unroll
+            for (int e = 0; e < E; ++e)
+              if (x[u][e] >= tau) {
+                const int slot = atomicAdd(&s_ncand, 1);
+                if (slot < kTopwCand) {
+                  s_cv[slot] = x[u][e];
+                  s_ci[slot] = (int)(cu * E + e);
+                }
+              }
+          }
+        }
+      }
+      __syncthreads();
+      ncand = s_ncand;
+    }
     // padding (-inf) never passes; equal values keep the earlier index
-    if (bm >= tau && bm > top.thr()) {
+    if ((!ONE || ncand > kTopwCand) && bm >= tau && bm > top.thr()) {
 #pragma unroll
       for (int u = 0; u < L; ++u) {
         const long long cu = c + (long long)u * kScanThreads;
@@ -260,29 +298,46 @@ __global__ __launch_bounds__(kScanThreads) void topw_scan(TopwArgs a) {
     red_s[wave] = s;
   }
   TopwPart* out = reinterpret_cast<TopwPart*>(a.part + ((size_t)row * a.nsplit + split) * kTopwPartBytes);
-  for (int k = 0; k < W; ++k) {
-    float bv = top.v[0];
-    int bi = top.i[0];
-    wave_best(bv, bi);
-    if (lane == 0) {
-      win_v[wave] = bv;
-      win_i[wave] = bi;
-    }
-    __syncthreads();
-    float gv = win_v[0];
-    int gi = win_i[0];
-#pragma unroll
-    for (int w = 1; w < kScanThreads / 64; ++w)
-      if (better(win_v[w], win_i[w], gv, gi)) {
-        gv = win_v[w];
-        gi = win_i[w];
+  if (ONE && ncand <= kTopwCand) {
+    if (tid < ncand) {
+      const float v = s_cv[tid];
+      const int i = s_ci[tid];
+      int rank = 0;
+      for (int j = 0; j < ncand; ++j) rank += better(s_cv[j], s_ci[j], v, i) ? 1 : 0;
+      if (rank < W) {
+        out->v[rank] = v;
+        out->i[rank] = i;
       }
-    if (top.i[0] == gi && gi != 0x7FFFFFFF) top.pop();  // indices are unique: one owner
-    if (tid == 0) {
-      out->v[k] = gv;
-      out->i[k] = gi;
+    } else if (tid < W) {  // a slice with fewer than W elements
+      out->v[tid] = -INFINITY;
+      out->i[tid] = 0x7FFFFFFF;
     }
-    __syncthreads();
+    __syncthreads();  // the waves' (m, s)
+  } else {
+    for (int k = 0; k < W; ++k) {
+      float bv = top.v[0];
+      int bi = top.i[0];
+      wave_best(bv, bi);
+      if (lane == 0) {
+        win_v[wave] = bv;
+        win_i[wave] = bi;
+      }
+      __syncthreads();
+      float gv = win_v[0];
+      int gi = win_i[0];
+#pragma unroll
+      for (int w = 1; w < kScanThreads / 64; ++w)
+        if (better(win_v[w], win_i[w], gv, gi)) {
+          gv = win_v[w];
+          gi = win_i[w];
+        }
+      if (top.i[0] == gi && gi != 0x7FFFFFFF) top.pop();  // indices are unique: one owner
+      if (tid == 0) {
+        out->v[k] = gv;
+        out->i[k] = gi;
+      }
+      __syncthreads();
+    }
   }
   if (tid == 0) {
     float gm = red_m[0], gs = red_s[0];
@@ -327,23 +382,30 @@ __global__ __launch_bounds__(64) void topw_finish(TopwArgs a) {
   }
 }
 
-template <int K>
+template <int K, bool ONE>
 static void launch_topw_scan_k(bool f32, bool vec, dim3 g, dim3 t, hipStream_t st,
                                const TopwArgs& a) {
   if (f32) {
-    if (vec) hipLaunchKernelGGL((topw_scan<true, true, K>), g, t, 0, st, a);
-    else hipLaunchKernelGGL((topw_scan<true, false, K>), g, t, 0, st, a);
+    if (vec) hipLaunchKernelGGL((topw_scan<true, true, K, ONE>), g, t, 0, st, a);
+    else hipLaunchKernelGGL((topw_scan<true, false, K, ONE>), g, t, 0, st, a);
   } else {
-    if (vec) hipLaunchKernelGGL((topw_scan<false, true, K>), g, t, 0, st, a);
-    else hipLaunchKernelGGL((topw_scan<false, false, K>), g, t, 0, st, a);
+    if (vec) hipLaunchKernelGGL((topw_scan<false, true, K, ONE>), g, t, 0, st, a);
+    else hipLaunchKernelGGL((topw_scan<false, false, K, ONE>), g, t, 0, st, a);
   }
 }
 
-static void launch_topw_scan(bool f32, bool vec, int K, dim3 g, dim3 t, hipStream_t st,
-                             const TopwArgs& a) {
-  if (K == 4) launch_topw_scan_k<4>(f32, vec, g, t, st, a);
-  else if (K == 8) launch_topw_scan_k<8>(f32, vec, g, t, st, a);
-  else launch_topw_scan_k<kTopwMax>(f32, vec, g, t, st, a);
+template <bool ONE>
+static void launch_topw_scan_one(bool f32, bool vec, int K, dim3 g, dim3 t, hipStream_t st,
+                                 const TopwArgs& a) {
+  if (K == 4) launch_topw_scan_k<4, ONE>(f32, vec, g, t, st, a);
+  else if (K == 8) launch_topw_scan_k<8, ONE>(f32, vec, g, t, st, a);
+  else launch_topw_scan_k<kTopwMax, ONE>(f32, vec, g, t, st, a);
+}
+
+static void launch_topw_scan(bool f32, bool vec, int K, bool one, dim3 g, dim3 t,
+                             hipStream_t st, const TopwArgs& a) {
+  if (one) launch_topw_scan_one<true>(f32, vec, K, g, t, st, a);
+  else launch_topw_scan_one<false>(f32, vec, K, g, t, st, a);
 }
 
 hipError_t launch_topw(const void* logits, int f32, int B, int Nd, int V, int W, int32_t* tok,
@@ -363,7 +425,9 @@ hipError_t launch_topw(const void* logits, int f32, int B, int Nd, int V, int W,
   a.cps = p.chunks_per_split;
   const dim3 g(p.grid), t(kScanThreads);
   const int K = W <= 4 ? 4 : (W <= 8 ? 8 : 16);
-  launch_topw_scan(f32 != 0, vec, K, g, t, st, a);
+  // one load round per workgroup: every split's slice fits in one
+  const bool one = p.chunks_per_split <= (long long)kScanThreads * kScanLoadsPerThread;
+  launch_topw_scan(f32 != 0, vec, K, one, g, t, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(topw_finish, dim3(a.rows), dim3(64), 0, st, a);

@@ -48,6 +48,7 @@ TOPW_CASES = [
     (1, 2, 300, 16, "f32", "ties"),
     (4, 64, 2048, 2, "bf16", "normal"),        # deepest draft
     (1, 1, 1, 1, "f32", "normal"),
+    (16, 64, 20000, 3, "f32", "normal"),       # several load rounds per vocabulary split
 ]
 
 

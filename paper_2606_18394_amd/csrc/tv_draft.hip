@@ -462,8 +462,9 @@ __device__ __forceinline__ float key_score(unsigned k) {
 
 // Wave-wide maximum / minimum of an unsigned value, returned to every lane
 // as a wave-uniform value: DPP steps inside each row of 16 lanes (lane ^ 1,
-// lane ^ 2, then the mirrored quads and halves), then the four rows' values
-// are read out as scalars and combined on the scalar unit.
+// lane ^ 2, then the mirrored quads and halves); the maximum then carries
+// the rows' values to lane 63 with the two row broadcasts, the minimum (off
+// the hot loop) reads the four rows out as scalars.
 template <int CTRL>
 __device__ __forceinline__ unsigned dpp_u32(unsigned x) {
   return (unsigned)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);

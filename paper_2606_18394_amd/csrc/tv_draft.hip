@@ -134,12 +134,94 @@ __device__ __forceinline__ void wave_best(float& v, int& i) {
   i = gi;
 }
 
+// Order-preserving map of a score to a nonzero key: a larger score gives a
+// larger key, so one unsigned maximum compares scores.  (-0.0 would sort
+// below +0.0; no score takes that value, since the root's is +0.0 and a
+// sum that cancels to zero rounds to +0.0.)  Key 0 marks "no open node".
+__device__ __forceinline__ unsigned score_key(float s) {
+  const unsigned u = __float_as_uint(s);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key_score(unsigned k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+}
+
+// Wave-wide maximum / minimum of an unsigned value, returned to every lane
+// as a wave-uniform value: DPP steps inside each row of 16 lanes (lane ^ 1,
+// lane ^ 2, then the mirrored quads and halves); the maximum then carries
+// the rows' values to lane 63 with the two row broadcasts, the minimum (off
+// the hot loop) reads the four rows out as scalars.
+template <int CTRL>
+__device__ __forceinline__ unsigned dpp_u32(unsigned x) {
+  return (unsigned)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
+}
+__device__ __forceinline__ unsigned wave_max_u32(unsigned x) {
+  x = max(x, dpp_u32<0xB1>(x));
+  x = max(x, dpp_u32<0x4E>(x));
+  x = max(x, dpp_u32<0x141>(x));
+  x = max(x, dpp_u32<0x140>(x));
+  // row 1 takes row 0's maximum and row 3 row 2's, then rows 2 and 3 take
+  // row 1's: lane 63 holds the wave's
+  x = max(x, (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x142, 0xA, 0xF, false));
+  x = max(x, (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x143, 0xC, 0xF, false));
+  return __builtin_amdgcn_readlane(x, 63);
+}
+__device__ __forceinline__ unsigned wave_min_u32(unsigned x) {
+  x = min(x, dpp_u32<0xB1>(x));
+  x = min(x, dpp_u32<0x4E>(x));
+  x = min(x, dpp_u32<0x141>(x));
+  x = min(x, dpp_u32<0x140>(x));
+  const unsigned r0 = __builtin_amdgcn_readlane(x, 0), r1 = __builtin_amdgcn_readlane(x, 16);
+  const unsigned r2 = __builtin_amdgcn_readlane(x, 32), r3 = __builtin_amdgcn_readlane(x, 48);
+  return min(min(r0, r1), min(r2, r3));
+}
+
 // (m, s) with s = sum exp(x - m): merge of two such states
 __device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2) {
   const float mn = fmaxf(m, m2);
   if (mn == -INFINITY) return;
   s = s * __expf(m - mn) + s2 * __expf(m2 - mn);
   m = mn;
+}
+template <int CTRL>
+__device__ __forceinline__ void lse_dpp_step(float& m, float& s) {
+  lse_merge(m, s, __int_as_float(dpp<CTRL>(__float_as_int(m))), __int_as_float(dpp<CTRL>(__float_as_int(s))));
+}
+// Wave-wide merge of (m, s): DPP pair merges inside each row of 16 lanes
+// (a merge of two states is symmetric, so both lanes of a pair hold the
+// same result), then the four rows' states merged as scalars.
+__device__ __forceinline__ void wave_lse(float& m, float& s) {
+  lse_dpp_step<0xB1>(m, s);
+  lse_dpp_step<0x4E>(m, s);
+  lse_dpp_step<0x141>(m, s);
+  lse_dpp_step<0x140>(m, s);
+  float gm = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(m), 0));
+  float gs = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(s), 0));
+#pragma unroll
+  for (int r = 16; r < 64; r += 16)
+    lse_merge(gm, gs, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(m), r)),
+              __int_as_float(__builtin_amdgcn_readlane(__float_as_int(s), r)));
+  m = gm;
+  s = gs;
+}
+
+// Key of a candidate value for the wave maximum: -0.0 counts as +0.0, as
+// the float comparison does; an empty entry (-inf at index 0x7FFFFFFF,
+// logits being finite) has key 0.
+__device__ __forceinline__ unsigned cand_key(float v, int i) {
+  return i == 0x7FFFFFFF ? 0u : score_key(v + 0.f);
+}
+// The lane holding the best (value, lower index) entry among the lanes'
+// heads: a wave maximum of the keys; the lanes holding it are a ballot, and
+// with several (equal values) the lowest index wins.  -1 if all are empty.
+__device__ __forceinline__ int best_head_lane(float v, int i) {
+  const unsigned k = cand_key(v, i);
+  const unsigned g = wave_max_u32(k);
+  if (g == 0u) return -1;
+  const unsigned long long hold = __ballot(k == g);
+  if (__popcll(hold) == 1) return __ffsll((unsigned long long)hold) - 1;
+  const unsigned bi = wave_min_u32(k == g ? (unsigned)i : 0xFFFFFFFFu);
+  return __ffsll((unsigned long long)__ballot(k == g && (unsigned)i == bi)) - 1;
 }
 
 // Slices of one load round (ONE) rank their candidates directly: every
@@ -239,14 +321,14 @@ __global__ __launch_bounds__(kScanThreads) void topw_scan(TopwArgs a) {
       constexpr int kWaves = kScanThreads / 64;
       __shared__ float s_tau[kWaves];
       const int q = (W + kWaves - 1) / kWaves;
-      float v = bm, kth = -INFINITY;
+      // q rounds of a key maximum; one lane holding it drops out each round
+      unsigned kv = bm == -INFINITY ? 0u : score_key(bm + 0.f), gk = 0u;
       for (int r = 0; r < q; ++r) {
-        float bv = v;
-        int bi = lane;
-        wave_best(bv, bi);
-        kth = bv;
-        if (lane == bi) v = -INFINITY;  // taken
+        gk = wave_max_u32(kv);
+        if (gk == 0u) break;  // fewer than q threads with data
+        if (lane == __ffsll((unsigned long long)__ballot(kv == gk)) - 1) kv = 0u;
       }
+      const float kth = gk == 0u ? -INFINITY : key_score(gk);
       if (lane == 0) s_tau[wave] = kth;
       __syncthreads();
       tau = s_tau[0];
@@ -291,8 +373,7 @@ __global__ __launch_bounds__(kScanThreads) void topw_scan(TopwArgs a) {
   __shared__ float red_m[kScanThreads / 64], red_s[kScanThreads / 64];
   __shared__ float win_v[kScanThreads / 64];
   __shared__ int win_i[kScanThreads / 64];
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) lse_merge(m, s, __shfl_xor(m, o), __shfl_xor(s, o));
+  wave_lse(m, s);
   if (lane == 0) {
     red_m[wave] = m;
     red_s[wave] = s;
@@ -348,12 +429,15 @@ __global__ __launch_bounds__(kScanThreads) void topw_scan(TopwArgs a) {
   }
 }
 
-// One wave per row: lane j < nsplit holds split j's sorted list.
+// One wave per row: lane j < nsplit holds split j's sorted list.  Each of
+// the W rounds takes the best head (one key maximum and a ballot) and the
+// owning lane drops it.
+template <int K>
 __global__ __launch_bounds__(64) void topw_finish(TopwArgs a) {
   const int row = blockIdx.x, lane = threadIdx.x;
   const int W = a.W;
   float m = -INFINITY, s = 0.f;
-  TopList<kTopwMax> top;
+  TopList<K> top;
   top.init();
   if (lane < a.nsplit) {
     const TopwPart* p =
@@ -361,20 +445,19 @@ __global__ __launch_bounds__(64) void topw_finish(TopwArgs a) {
     m = p->m;
     s = p->s;
 #pragma unroll
-    for (int k = 0; k < kTopwMax; ++k)
+    for (int k = 0; k < K; ++k)
       if (k < W) {
         top.v[k] = p->v[k];
         top.i[k] = p->i[k];
       }
   }
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) lse_merge(m, s, __shfl_xor(m, o), __shfl_xor(s, o));
+  wave_lse(m, s);
   const float lse = m + logf(s);
   for (int k = 0; k < W; ++k) {
-    float bv = top.v[0];
-    int bi = top.i[0];
-    wave_best(bv, bi);
-    if (top.i[0] == bi) top.pop();
+    const int owner = best_head_lane(top.v[0], top.i[0]);
+    const float bv = owner < 0 ? -INFINITY : __int_as_float(__builtin_amdgcn_readlane(__float_as_int(top.v[0]), owner < 0 ? 0 : owner));
+    const int bi = owner < 0 ? 0x7FFFFFFF : __builtin_amdgcn_readlane(top.i[0], owner < 0 ? 0 : owner);
+    if (lane == owner) top.pop();
     if (lane == 0) {
       a.tok[(size_t)row * W + k] = bi;
       a.logp[(size_t)row * W + k] = bv - lse;
@@ -430,7 +513,9 @@ hipError_t launch_topw(const void* logits, int f32, int B, int Nd, int V, int W,
   launch_topw_scan(f32 != 0, vec, K, one, g, t, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(topw_finish, dim3(a.rows), dim3(64), 0, st, a);
+  if (K == 4) hipLaunchKernelGGL(topw_finish<4>, dim3(a.rows), dim3(64), 0, st, a);
+  else if (K == 8) hipLaunchKernelGGL(topw_finish<8>, dim3(a.rows), dim3(64), 0, st, a);
+  else hipLaunchKernelGGL(topw_finish<kTopwMax>, dim3(a.rows), dim3(64), 0, st, a);
   return hipGetLastError();
 }
 
@@ -447,48 +532,6 @@ struct BuildArgs {
   int32_t* n_nodes;
   int Nd, W, budget;
 };
-
-// Order-preserving map of a score to a nonzero key: a larger score gives a
-// larger key, so one unsigned maximum compares scores.  (-0.0 would sort
-// below +0.0; no score takes that value, since the root's is +0.0 and a
-// sum that cancels to zero rounds to +0.0.)  Key 0 marks "no open node".
-__device__ __forceinline__ unsigned score_key(float s) {
-  const unsigned u = __float_as_uint(s);
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-__device__ __forceinline__ float key_score(unsigned k) {
-  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
-}
-
-// Wave-wide maximum / minimum of an unsigned value, returned to every lane
-// as a wave-uniform value: DPP steps inside each row of 16 lanes (lane ^ 1,
-// lane ^ 2, then the mirrored quads and halves); the maximum then carries
-// the rows' values to lane 63 with the two row broadcasts, the minimum (off
-// the hot loop) reads the four rows out as scalars.
-template <int CTRL>
-__device__ __forceinline__ unsigned dpp_u32(unsigned x) {
-  return (unsigned)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
-}
-__device__ __forceinline__ unsigned wave_max_u32(unsigned x) {
-  x = max(x, dpp_u32<0xB1>(x));
-  x = max(x, dpp_u32<0x4E>(x));
-  x = max(x, dpp_u32<0x141>(x));
-  x = max(x, dpp_u32<0x140>(x));
-  // row 1 takes row 0's maximum and row 3 row 2's, then rows 2 and 3 take
-  // row 1's: lane 63 holds the wave's
-  x = max(x, (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x142, 0xA, 0xF, false));
-  x = max(x, (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x143, 0xC, 0xF, false));
-  return __builtin_amdgcn_readlane(x, 63);
-}
-__device__ __forceinline__ unsigned wave_min_u32(unsigned x) {
-  x = min(x, dpp_u32<0xB1>(x));
-  x = min(x, dpp_u32<0x4E>(x));
-  x = min(x, dpp_u32<0x141>(x));
-  x = min(x, dpp_u32<0x140>(x));
-  const unsigned r0 = __builtin_amdgcn_readlane(x, 0), r1 = __builtin_amdgcn_readlane(x, 16);
-  const unsigned r2 = __builtin_amdgcn_readlane(x, 32), r3 = __builtin_amdgcn_readlane(x, 48);
-  return min(min(r0, r1), min(r2, r3));
-}
 
 // Best-first expansion for budgets of at most 64 S nodes, one wave per
 // sequence.  Node i belongs to lane i % 64, slot i / 64.  A lane keeps, per

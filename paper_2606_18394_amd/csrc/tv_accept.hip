@@ -63,14 +63,27 @@ __device__ __forceinline__ unsigned long long umax64(unsigned long long x, unsig
   return x > y ? x : y;
 }
 
+template <int CTRL>
+__device__ __forceinline__ unsigned long long dpp_u64(unsigned long long k) {
+  return ((unsigned long long)dpp_u32<CTRL>((unsigned int)(k >> 32)) << 32) | dpp_u32<CTRL>((unsigned int)k);
+}
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ unsigned long long dpp_bcast_u64(unsigned long long k) {
+  return ((unsigned long long)dpp_bcast_u32<CTRL, ROWMASK>((unsigned int)(k >> 32)) << 32) |
+         dpp_bcast_u32<CTRL, ROWMASK>((unsigned int)k);
+}
+// wave_max_u32's DPP steps on a 64-bit key; wave-uniform result
 __device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long k) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    const unsigned int lo = __shfl_xor((unsigned int)k, o);
-    const unsigned int hi = __shfl_xor((unsigned int)(k >> 32), o);
-    k = umax64(k, ((unsigned long long)hi << 32) | lo);
-  }
-  return k;
+  k = umax64(k, dpp_u64<0xB1>(k));
+  k = umax64(k, dpp_u64<0x4E>(k));
+  k = umax64(k, dpp_u64<0x141>(k));
+  k = umax64(k, dpp_u64<0x140>(k));
+  k = umax64(k, dpp_bcast_u64<0x142, 0xA>(k));
+  k = umax64(k, dpp_bcast_u64<0x143, 0xC>(k));
+  // readlane returns int: widen through unsigned int, not by sign extension
+  const unsigned int hi = (unsigned int)__builtin_amdgcn_readlane((unsigned int)(k >> 32), 63);
+  const unsigned int lo = (unsigned int)__builtin_amdgcn_readlane((unsigned int)k, 63);
+  return ((unsigned long long)hi << 32) | lo;
 }
 
 // Running first maximum over a thread's elements, visited in increasing
@@ -495,11 +508,7 @@ __global__ __launch_bounds__(64) void accept_finish_wave(AcceptArgs a) {
           node[q] && fail == 0u ? ((unsigned int)dep[q] << 16) | (0xFFFFu - (unsigned int)i) : 0u;
       k = kq > k ? kq : k;
     }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-      const unsigned int other = __shfl_xor(k, o);
-      k = other > k ? other : k;
-    }
+    k = wave_max_u32(k);
     depth = (int)(k >> 16);
     const int v = (int)(0xFFFFu - (k & 0xFFFFu));
     len = depth + 1 > a.Dmax ? -1 : depth + 1;

@@ -28,6 +28,7 @@
 
 #include "tv_plan.h"
 #include "tv_stream.h"
+#include "tv_walk.h"
 
 namespace tv {
 
@@ -146,26 +147,10 @@ __device__ __forceinline__ float key_score(unsigned k) {
   return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
 }
 
-// Wave-wide maximum / minimum of an unsigned value, returned to every lane
-// as a wave-uniform value: DPP steps inside each row of 16 lanes (lane ^ 1,
-// lane ^ 2, then the mirrored quads and halves); the maximum then carries
-// the rows' values to lane 63 with the two row broadcasts, the minimum (off
-// the hot loop) reads the four rows out as scalars.
-template <int CTRL>
-__device__ __forceinline__ unsigned dpp_u32(unsigned x) {
-  return (unsigned)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
-}
-__device__ __forceinline__ unsigned wave_max_u32(unsigned x) {
-  x = max(x, dpp_u32<0xB1>(x));
-  x = max(x, dpp_u32<0x4E>(x));
-  x = max(x, dpp_u32<0x141>(x));
-  x = max(x, dpp_u32<0x140>(x));
-  // row 1 takes row 0's maximum and row 3 row 2's, then rows 2 and 3 take
-  // row 1's: lane 63 holds the wave's
-  x = max(x, (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x142, 0xA, 0xF, false));
-  x = max(x, (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x143, 0xC, 0xF, false));
-  return __builtin_amdgcn_readlane(x, 63);
-}
+// Wave-wide minimum of an unsigned value (the maximum, wave_max_u32, is in
+// tv_walk.h), returned as a wave-uniform value: DPP steps inside each row of
+// 16 lanes, then the four rows' values read out as scalars (it runs only on
+// ties, off the hot loops).
 __device__ __forceinline__ unsigned wave_min_u32(unsigned x) {
   x = min(x, dpp_u32<0xB1>(x));
   x = min(x, dpp_u32<0x4E>(x));

@@ -1,6 +1,6 @@
 // Device helpers shared by the greedy and the non-greedy tree acceptance:
-// the pointer-jumping state of one node packed into a 32-bit word, and a
-// wave-wide unsigned maximum.  Pointer jumping over the parent links finds,
+// the pointer-jumping state of one node packed into a 32-bit word, and
+// wave-wide unsigned maxima on DPP exchanges.  Pointer jumping over the parent links finds,
 // for every node at once, its depth and whether every node on its root path
 // passed its test, in O(log depth) rounds.
 #pragma once
@@ -35,13 +35,30 @@ __device__ __forceinline__ unsigned int deepest_key(unsigned int w, int i) {
   return (w & kOkBit) ? (((w >> kDepShift) & kDepMask) << 16) | (0xFFFFu - (unsigned int)i) : 0u;
 }
 
-__device__ __forceinline__ unsigned int wave_max_u32(unsigned int k) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    const unsigned int other = __shfl_xor(k, o);
-    k = other > k ? other : k;
-  }
-  return k;
+// One DPP exchange of a 32-bit value (all rows and banks enabled).
+template <int CTRL>
+__device__ __forceinline__ unsigned dpp_u32(unsigned x) {
+  return (unsigned)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
+}
+// A row broadcast into the rows of ROWMASK; the other rows keep x.
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ unsigned dpp_bcast_u32(unsigned x) {
+  return (unsigned)__builtin_amdgcn_update_dpp((int)x, (int)x, CTRL, ROWMASK, 0xF, false);
+}
+
+// Wave-wide maximum, returned as a wave-uniform value: DPP steps inside each
+// row of 16 lanes (lane ^ 1, lane ^ 2, then the mirrored quads and halves),
+// then row 1 takes row 0's maximum and row 3 row 2's, and rows 2 and 3 take
+// row 1's (the two row broadcasts): lane 63 holds the wave's.  No step goes
+// through the LDS crossbar.
+__device__ __forceinline__ unsigned int wave_max_u32(unsigned int x) {
+  x = max(x, dpp_u32<0xB1>(x));
+  x = max(x, dpp_u32<0x4E>(x));
+  x = max(x, dpp_u32<0x141>(x));
+  x = max(x, dpp_u32<0x140>(x));
+  x = max(x, dpp_bcast_u32<0x142, 0xA>(x));
+  x = max(x, dpp_bcast_u32<0x143, 0xC>(x));
+  return __builtin_amdgcn_readlane(x, 63);
 }
 
 }  // namespace tv

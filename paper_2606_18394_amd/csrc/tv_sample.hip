@@ -94,6 +94,12 @@ __device__ __forceinline__ void lse_merge2(float& m, float& s, float m2, float s
   m = mn;
 }
 
+template <int CTRL>
+__device__ __forceinline__ void lse_dpp2(float& m, float& s) {
+  lse_merge2(m, s, __uint_as_float(dpp_u32<CTRL>(__float_as_uint(m))),
+             __uint_as_float(dpp_u32<CTRL>(__float_as_uint(s))));
+}
+
 template <bool F32>
 __device__ __forceinline__ float load_logit(const void* base, size_t idx) {
   if (F32) return reinterpret_cast<const float*>(base)[idx];
@@ -127,15 +133,24 @@ __device__ __forceinline__ unsigned long long race_key(float r, unsigned int x) 
   return ((unsigned long long)__float_as_uint(r) << 32) | (0xFFFFFFFFu - x);
 }
 
+// Wave-wide maximum of a 64-bit key on DPP exchanges (four steps inside
+// each row of 16 lanes, then the two row broadcasts into lane 63), returned
+// as a wave-uniform value.
 __device__ __forceinline__ unsigned long long wave_max_key(unsigned long long k) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    const unsigned int lo = __shfl_xor((unsigned int)k, o);
-    const unsigned int hi = __shfl_xor((unsigned int)(k >> 32), o);
-    const unsigned long long other = ((unsigned long long)hi << 32) | lo;
-    k = other > k ? other : k;
-  }
-  return k;
+  auto step = [](unsigned long long x, unsigned int hi, unsigned int lo) {
+    const unsigned long long o = ((unsigned long long)hi << 32) | lo;
+    return o > x ? o : x;
+  };
+  k = step(k, dpp_u32<0xB1>((unsigned int)(k >> 32)), dpp_u32<0xB1>((unsigned int)k));
+  k = step(k, dpp_u32<0x4E>((unsigned int)(k >> 32)), dpp_u32<0x4E>((unsigned int)k));
+  k = step(k, dpp_u32<0x141>((unsigned int)(k >> 32)), dpp_u32<0x141>((unsigned int)k));
+  k = step(k, dpp_u32<0x140>((unsigned int)(k >> 32)), dpp_u32<0x140>((unsigned int)k));
+  k = step(k, dpp_bcast_u32<0x142, 0xA>((unsigned int)(k >> 32)), dpp_bcast_u32<0x142, 0xA>((unsigned int)k));
+  k = step(k, dpp_bcast_u32<0x143, 0xC>((unsigned int)(k >> 32)), dpp_bcast_u32<0x143, 0xC>((unsigned int)k));
+  // readlane returns int: widen through unsigned int, not by sign extension
+  const unsigned int hi = (unsigned int)__builtin_amdgcn_readlane((unsigned int)(k >> 32), 63);
+  const unsigned int lo = (unsigned int)__builtin_amdgcn_readlane((unsigned int)k, 63);
+  return ((unsigned long long)hi << 32) | lo;
 }
 
 // ------------------------------------------------------------ lse_scan
@@ -219,8 +234,20 @@ __global__ __launch_bounds__(kLseScanThreads) void lse_scan(SampleArgs a, int ve
   const char* rowp = (const char*)a.logits + (size_t)row * a.V * (F32 ? 4 : 2);
   lse_slice<F32>(rowp, x0, x1, vec != 0, a.invT, m, s);
   __shared__ float rm[kLseScanThreads / 64], rs[kLseScanThreads / 64];
+  // pair merges inside each row of 16 lanes on DPP exchanges (a merge is
+  // symmetric, so both lanes of a pair hold the same state), then the rows
+  lse_dpp2<0xB1>(m, s);
+  lse_dpp2<0x4E>(m, s);
+  lse_dpp2<0x141>(m, s);
+  lse_dpp2<0x140>(m, s);
+  float wm = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(m), 0));
+  float ws = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(s), 0));
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) lse_merge2(m, s, __shfl_xor(m, o), __shfl_xor(s, o));
+  for (int r = 16; r < 64; r += 16)
+    lse_merge2(wm, ws, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(m), r)),
+               __int_as_float(__builtin_amdgcn_readlane(__float_as_int(s), r)));
+  m = wm;
+  s = ws;
   if (lane == 0) {
     rm[wave] = m;
     rs[wave] = s;

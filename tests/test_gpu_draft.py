@@ -49,6 +49,8 @@ TOPW_CASES = [
     (4, 64, 2048, 2, "bf16", "normal"),        # deepest draft
     (1, 1, 1, 1, "f32", "normal"),
     (16, 64, 20000, 3, "f32", "normal"),       # several load rounds per vocabulary split
+    (2, 4, 151936, 8, "bf16", "zeros"),        # signed zeros tie at the top
+    (1, 3, 5000, 16, "f32", "zeros"),
 ]
 
 
@@ -58,6 +60,11 @@ def test_topw_parity(case):
     rng = np.random.default_rng(50 + case)
     if kind == "ties":
         x = rng.integers(-4, 4, size=(B, Nd, V)).astype(np.float32)
+    elif kind == "zeros":   # the maxima are +0.0 and -0.0, which compare equal: lower index first
+        x = -np.abs(rng.standard_normal((B, Nd, V), dtype=np.float32)) - np.float32(0.5)
+        pick = rng.random((B, Nd, V))
+        x[pick < 0.01] = np.float32(0.0)
+        x[(pick >= 0.01) & (pick < 0.02)] = np.float32(-0.0)
     else:
         x = rng.standard_normal((B, Nd, V), dtype=np.float32) * 2
     if dtype == "bf16":
